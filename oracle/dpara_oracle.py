@@ -1,0 +1,368 @@
+"""CPU oracle for the DPara drafter hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product package imports this module;
+only tests, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline``
+leg may call it.  It shares no code with the HIP path: inputs come from the
+seeded generators in ``paper_2609_27396_amd.synth`` and everything here is
+plain numpy in float64, one request at a time, in the order the paper states
+the method.
+
+What it follows (paper: "When Parallel Drafter Meets Parallel Speculative
+Decoding"):
+
+* Algorithm 1 (one steady-state DPara round): precompute on the spine
+  t_{0:d} and the feature cache C, verify, select branch r, run the AR head
+  with y_0 = b, emit the next block (b, y_{1:d}).
+* Section 3.2, "Shared causal spine with isolated bidirectional branches" and
+  the d=3 mask figure: the tree attention mask.
+* Section 3.2, "Loss" equation: the AR head z_i = l_i + W E(y_{i-1}), y_0 = b.
+* Section 2.1: greedy acceptance (longest prefix of drafts equal to the
+  target's argmax; the bonus is the target's token right after it).
+* Section 3.3 and Appendix D: C grows by the features of t_{0:r}
+  (incremental projection of cached history features).
+
+The paper does not spell out the drafter layer internals; the readings used
+here (Qwen3-shaped pre-norm blocks, mask-token positions, how cached features
+enter each layer, bf16 rounding points) are listed in the design doc and restated
+at each function.  Parity unpinned: agreement with a trained DSpark/M-DFlash
+checkpoint (none is available); everything else is pinned by tests under
+``tests/test_oracle_*.py``.
+
+Precision modes (``mode``):
+  "exact" - no rounding anywhere (float64 throughout);
+  "f32"   - values rounded to float32 at the op boundaries listed below;
+  "bf16"  - the 16-bit points below rounded to bfloat16, the rest to float32.
+16-bit rounding points: RMSNorm outputs that feed a projection; Q/K/V after
+q/k-norm and RoPE (this includes the context K/V cache); the attention output;
+silu(gate)*up.  Float32 points: the residual stream after each add, the
+representations (reps), the base logits l and the head logits z.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+MASK_POS_OFFSET = 1  # branch r's i-th mask sits at position n_b + r + i (reading A)
+
+
+# ----------------------------------------------------------------------------
+# rounding
+# ----------------------------------------------------------------------------
+def round_bf16(x) -> np.ndarray:
+    """Round float64 values to bfloat16 precision, ties to even (direct, no double rounding).
+
+    bfloat16 keeps 8 significant bits; normal numbers have spacing 2^(e-8) where
+    x = m * 2^e with m in [0.5, 1); below 2^-126 the spacing is 2^-133."""
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)
+    spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
+    return np.rint(x / spacing) * spacing
+
+
+def round_f32(x) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+class Rounding:
+    def __init__(self, mode: str):
+        if mode not in ("exact", "f32", "bf16"):
+            raise ValueError(mode)
+        self.mode = mode
+
+    def r16(self, x):
+        if self.mode == "bf16":
+            return round_bf16(x)
+        if self.mode == "f32":
+            return round_f32(x)
+        return np.asarray(x, np.float64)
+
+    def r32(self, x):
+        if self.mode == "exact":
+            return np.asarray(x, np.float64)
+        return round_f32(x)
+
+
+def _f64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+# ----------------------------------------------------------------------------
+# textbook building blocks
+# ----------------------------------------------------------------------------
+def rmsnorm(x, g, eps):
+    """x / sqrt(mean(x^2) + eps) * g over the last axis."""
+    x = _f64(x)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * _f64(g)
+
+
+def silu(x):
+    x = _f64(x)
+    return x / (1.0 + np.exp(-x))
+
+
+def rope(x, pos, base):
+    """Rotary embedding, rotate-half pairing (j, j + hd/2), angle pos * base^(-2j/hd).
+
+    x: [n, heads, hd]; pos: [n]."""
+    x = _f64(x)
+    hd = x.shape[-1]
+    half = hd // 2
+    inv_freq = np.power(float(base), -2.0 * np.arange(half, dtype=np.float64) / hd)
+    ang = _f64(pos)[:, None] * inv_freq[None, :]          # [n, half]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def softmax_rows(s):
+    m = np.max(s, axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def attention(q, k, v, allowed):
+    """Masked multi-head attention with grouped KV heads.
+
+    q: [R, n_q, hd]; k, v: [N, n_kv, hd]; allowed: [R, N] bool.
+    Query head h reads KV head floor(h * n_kv / n_q).  Scale 1/sqrt(hd)."""
+    R, n_q, hd = q.shape
+    n_kv = k.shape[1]
+    out = np.empty((R, n_q, hd), np.float64)
+    for h in range(n_q):
+        kvh = (h * n_kv) // n_q
+        s = q[:, h, :] @ k[:, kvh, :].T / math.sqrt(hd)
+        s = np.where(allowed, s, -np.inf)
+        out[:, h, :] = softmax_rows(s) @ v[:, kvh, :]
+    return out
+
+
+# ----------------------------------------------------------------------------
+# the all-boundary layout (Section 3.2 mask figure)
+# ----------------------------------------------------------------------------
+def row_index(gamma: int, branch: int | None, i: int) -> int:
+    """Row of spine token t_i (branch None) or of branch `branch`'s mask i (1..gamma)."""
+    if branch is None:
+        return i
+    return (gamma + 1) + branch * gamma + (i - 1)
+
+
+def tree_visibility(gamma: int) -> np.ndarray:
+    """In-block visibility [R, R], R = (gamma+1)^2, of the M-DFlash tree mask.
+
+    Spine t_j sees spine t_0..t_j (shared causal spine) and no mask token.
+    Branch r's masks (the branch for accepted prefix t_0..t_r) see t_0..t_r and
+    every mask of branch r (bidirectional within the branch); other branches
+    are invisible.  Every row also sees the whole cached context (not part of
+    this matrix)."""
+    R = (gamma + 1) ** 2
+    vis = np.zeros((R, R), bool)
+    for j in range(gamma + 1):
+        for k in range(j + 1):
+            vis[row_index(gamma, None, j), row_index(gamma, None, k)] = True
+    for r in range(gamma + 1):
+        for i in range(1, gamma + 1):
+            row = row_index(gamma, r, i)
+            for k in range(r + 1):
+                vis[row, row_index(gamma, None, k)] = True
+            for i2 in range(1, gamma + 1):
+                vis[row, row_index(gamma, r, i2)] = True
+    return vis
+
+
+def row_positions(gamma: int, n_b: int) -> np.ndarray:
+    """Position ids: t_j at n_b + j; branch r's mask i at n_b + r + i."""
+    pos = np.empty((gamma + 1) ** 2, np.int64)
+    for j in range(gamma + 1):
+        pos[row_index(gamma, None, j)] = n_b + j
+    for r in range(gamma + 1):
+        for i in range(1, gamma + 1):
+            pos[row_index(gamma, r, i)] = n_b + r + MASK_POS_OFFSET + (i - 1)
+    return pos
+
+
+# ----------------------------------------------------------------------------
+# drafter layers
+# ----------------------------------------------------------------------------
+def context_kv(shape, w, layer: int, feats, pos0: int, rnd: Rounding):
+    """Per-layer K/V of cached fused target features (incremental projection).
+
+    k = RoPE(kNorm(W_k f)), v = W_v f for every cached position; no input norm is
+    applied to cached features (reading Q3).  Returns [n, n_kv, hd] each."""
+    f = _f64(feats)
+    n = f.shape[0]
+    hd, n_kv = shape.head_dim, shape.n_kv_heads
+    k = (f @ _f64(w[f"L{layer}.wk"]).T).reshape(n, n_kv, hd)
+    v = (f @ _f64(w[f"L{layer}.wv"]).T).reshape(n, n_kv, hd)
+    if shape.qk_norm:
+        k = rmsnorm(k, w[f"L{layer}.k_norm"], shape.rms_eps)
+    k = rope(k, np.arange(pos0, pos0 + n), shape.rope_base)
+    return rnd.r16(k), rnd.r16(v)
+
+
+def layer_forward(shape, w, layer: int, X, pos, ctx_k, ctx_v, vis, rnd: Rounding):
+    """One pre-norm drafter block on block rows X [R, H] (residual stream).
+
+    Attention reads every cached context key plus the in-block keys allowed by
+    `vis`; then O-projection + residual, RMSNorm, SwiGLU MLP + residual."""
+    p = f"L{layer}."
+    R = X.shape[0]
+    hd, n_q, n_kv = shape.head_dim, shape.n_q_heads, shape.n_kv_heads
+    a = rnd.r16(rmsnorm(X, w[p + "attn_norm"], shape.rms_eps))
+    q = (a @ _f64(w[p + "wq"]).T).reshape(R, n_q, hd)
+    k = (a @ _f64(w[p + "wk"]).T).reshape(R, n_kv, hd)
+    v = (a @ _f64(w[p + "wv"]).T).reshape(R, n_kv, hd)
+    if shape.qk_norm:
+        q = rmsnorm(q, w[p + "q_norm"], shape.rms_eps)
+        k = rmsnorm(k, w[p + "k_norm"], shape.rms_eps)
+    q = rnd.r16(rope(q, pos, shape.rope_base))
+    k = rnd.r16(rope(k, pos, shape.rope_base))
+    v = rnd.r16(v)
+    n_ctx = ctx_k.shape[0]
+    keys = np.concatenate([ctx_k, k], axis=0)
+    vals = np.concatenate([ctx_v, v], axis=0)
+    allowed = np.concatenate([np.ones((R, n_ctx), bool), vis], axis=1)
+    o = rnd.r16(attention(q, keys, vals, allowed)).reshape(R, n_q * hd)
+    X = rnd.r32(X + o @ _f64(w[p + "wo"]).T)
+    m = rnd.r16(rmsnorm(X, w[p + "mlp_norm"], shape.rms_eps))
+    gate = m @ _f64(w[p + "w_gate"]).T
+    up = m @ _f64(w[p + "w_up"]).T
+    hmid = rnd.r16(silu(gate) * up)
+    X = rnd.r32(X + hmid @ _f64(w[p + "w_down"]).T)
+    return X
+
+
+def _run_block(shape, w, X, pos, vis, ctx_feats, mode):
+    rnd = Rounding(mode)
+    X = rnd.r32(X)
+    for l in range(shape.n_layers):
+        ck, cv = context_kv(shape, w, l, ctx_feats, 0, rnd)
+        X = layer_forward(shape, w, l, X, pos, ck, cv, vis, rnd)
+    return X
+
+
+def backbone_all_boundaries(shape, w, ctx_feats, spine, mode: str = "bf16"):
+    """Algorithm 1, Precompute: one forward of all (gamma+1)^2 rows of one request.
+
+    ctx_feats: [n_b, H] cached fused target features; spine: [gamma+1] token ids
+    (t_0 = previous bonus).  Returns dict(reps [gamma+1, gamma, H], X [R, H] final
+    residual, pos [R])."""
+    g = shape.gamma
+    n_b = int(np.asarray(ctx_feats).shape[0])
+    R = (g + 1) ** 2
+    emb = w["embed"]
+    X = np.empty((R, shape.hidden), np.float64)
+    for j in range(g + 1):
+        X[row_index(g, None, j)] = _f64(emb[int(spine[j])])
+    X[g + 1:] = _f64(w["mask_emb"])[None, :]
+    pos = row_positions(g, n_b)
+    Xf = _run_block(shape, w, X, pos, tree_visibility(g), ctx_feats, mode)
+    rnd = Rounding(mode)
+    reps = rnd.r32(rmsnorm(Xf[g + 1:], w["final_norm"], shape.rms_eps)).reshape(g + 1, g, shape.hidden)
+    return {"reps": reps, "X": Xf, "pos": pos}
+
+
+def backbone_single_boundary(shape, w, ctx_feats, spine, r: int, mode: str = "bf16"):
+    """Brute force for one acceptance boundary: the sequence [t_0..t_r, mask x gamma]
+    run alone over the context.  The anchors are causal among themselves; the masks
+    see every anchor and each other.  This is what branch r of the tree pass must
+    reproduce (Section 3.2: each branch's predictions stay valid for its boundary).
+
+    Returns dict(reps [gamma, H], X [r+1+gamma, H])."""
+    g = shape.gamma
+    n_b = int(np.asarray(ctx_feats).shape[0])
+    n = r + 1 + g
+    X = np.empty((n, shape.hidden), np.float64)
+    for j in range(r + 1):
+        X[j] = _f64(w["embed"][int(spine[j])])
+    X[r + 1:] = _f64(w["mask_emb"])[None, :]
+    pos = np.concatenate([n_b + np.arange(r + 1), n_b + r + MASK_POS_OFFSET + np.arange(g)])
+    vis = np.zeros((n, n), bool)
+    for i in range(n):
+        if i <= r:
+            vis[i, :i + 1] = True          # causal anchors
+        else:
+            vis[i, :] = True               # masks: all anchors and all masks
+    Xf = _run_block(shape, w, X, pos, vis, ctx_feats, mode)
+    rnd = Rounding(mode)
+    reps = rnd.r32(rmsnorm(Xf[r + 1:], w["final_norm"], shape.rms_eps))
+    return {"reps": reps, "X": Xf}
+
+
+# ----------------------------------------------------------------------------
+# greedy verification (Section 2.1; Algorithm 1, Verify)
+# ----------------------------------------------------------------------------
+def verify_greedy(logits, spine):
+    """logits [gamma+1, V]: target scores after t_0..t_gamma.  spine [gamma+1].
+
+    g_j = argmax_v logits[j] (lowest index on ties); r = number of leading drafts
+    with t_i == g_{i-1}; bonus = g_r.  Returns (r, bonus, g)."""
+    L = np.asarray(logits)
+    gamma = L.shape[0] - 1
+    g = np.array([int(np.argmax(L[j])) for j in range(gamma + 1)], np.int64)
+    r = 0
+    while r < gamma and int(spine[r + 1]) == int(g[r]):
+        r += 1
+    return r, int(g[r]), g
+
+
+# ----------------------------------------------------------------------------
+# select + AR head (Algorithm 1, lines after the barrier; Section 3.2 head equation)
+# ----------------------------------------------------------------------------
+def argmax_margin(z):
+    """(lowest-index argmax, top1 - top2) of a vector."""
+    z = np.asarray(z, np.float64)
+    i = int(np.argmax(z))
+    if z.size < 2:
+        return i, math.inf
+    rest = np.delete(z, i)
+    return i, float(z[i] - rest.max())
+
+
+def base_logits(w, h, mode: str = "bf16"):
+    """l = h E_tok^T with the tied token embedding as LM head.  h: [n, H]."""
+    return Rounding(mode).r32(_f64(h) @ _f64(w["embed"]).T)
+
+
+def head_step(w, ell_i, y_prev: int, mode: str = "bf16"):
+    """z_i = l_i + W E(y_{i-1}); returns (y_i, margin, z_i)."""
+    c = _f64(w["ar_W"]) @ _f64(w["ar_E"][int(y_prev)])
+    z = Rounding(mode).r32(_f64(ell_i) + c)
+    y, m = argmax_margin(z)
+    return y, m, z
+
+
+def select_and_head(shape, w, reps, r: int, bonus: int, mode: str = "bf16", teacher=None):
+    """Select branch r, then y_0 = b and y_i = argmax(l_i + W E(y_{i-1})), i = 1..gamma.
+
+    reps: [gamma+1, gamma, H].  `teacher` (optional [gamma] ids) replaces the
+    previous token fed to step i by teacher[i-1] for i >= 2 (teacher forcing),
+    so a GPU run can be checked step by step.  Returns dict(gathered, logits,
+    drafts, margins, next_spine)."""
+    g = shape.gamma
+    h = _f64(reps[r])
+    ell = base_logits(w, h, mode)
+    drafts = np.zeros(g, np.int64)
+    margins = np.zeros(g, np.float64)
+    y_prev = int(bonus)
+    for i in range(1, g + 1):
+        y, m, _ = head_step(w, ell[i - 1], y_prev, mode)
+        drafts[i - 1], margins[i - 1] = y, m
+        y_prev = y if teacher is None else int(teacher[i - 1])
+    next_spine = np.concatenate([[int(bonus)], drafts])
+    return {"gathered": h, "logits": ell, "drafts": drafts, "margins": margins,
+            "next_spine": next_spine}
+
+
+def dpara_round(shape, w, ctx_feats, spine, target_logits, mode: str = "bf16"):
+    """Algorithm 1 for one request: precompute, verify, select, head.
+
+    Returns dict(reps, r, bonus, g, drafts, margins, next_spine, n_ctx_next) where
+    n_ctx_next = n_b + r + 1 (the cache grows by the features of t_{0:r})."""
+    bb = backbone_all_boundaries(shape, w, ctx_feats, spine, mode)
+    r, bonus, g = verify_greedy(target_logits, spine)
+    hd = select_and_head(shape, w, bb["reps"], r, bonus, mode)
+    n_b = int(np.asarray(ctx_feats).shape[0])
+    return {"reps": bb["reps"], "r": r, "bonus": bonus, "g": g, "drafts": hd["drafts"],
+            "margins": hd["margins"], "next_spine": hd["next_spine"], "n_ctx_next": n_b + r + 1}
