@@ -1,0 +1,203 @@
+#!/usr/bin/env python3
+"""Benchmark of the DPara drafter hot path on one MI355X.
+
+One step = one steady-state round for the whole batch, all in libdpara's HIP kernels:
+    dpara_ctx_append (r+1 new feature rows per request, incremental projection)
+    -> dpara_backbone_all_boundaries (all gamma+1 boundaries, tree mask)
+    -> dpara_verify_greedy (planted target logits)
+    -> dpara_select_and_head (gather branch r, LM head, gamma-step AR head)
+Inputs are resident in HBM before the timed region.  Before each append the
+context length is rewound by the append size, so every round runs at the
+workload's context length (a steady state at fixed context).
+
+Prints one JSON line (see the fields below).  `--gpus N` with N > 1 exits: the
+path runs on one GPU (requests would shard independently across GPUs).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "all-boundary backbone rounds/sec + head µs/round at b=1..16; % HBM/MFMA peak"
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_F32_TFLOPS = 157.3
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gateup_work(shape, M):
+    """Algorithmic bytes and flops of one gate/up SwiGLU GEMM launch over M rows."""
+    esz = 2 if shape.dtype == "bf16" else 4
+    H, F = shape.hidden, shape.ffn
+    bytes_ = 2 * F * H * esz + M * H * esz + M * F * esz
+    flops = 2.0 * M * (2 * F) * H
+    return bytes_, flops
+
+
+def backbone_work(shape, B, ctx_lens):
+    """Algorithmic bytes (weights + context K/V read + reps written) and flops of one backbone call."""
+    esz = 2 if shape.dtype == "bf16" else 4
+    H, F, nq, nkv, hd, L, g = (shape.hidden, shape.ffn, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                               shape.n_layers, shape.gamma)
+    R = (g + 1) ** 2
+    M = B * R
+    per_layer_w = (nq + 2 * nkv) * hd * H + nq * hd * H + 3 * F * H
+    wbytes = L * per_layer_w * esz
+    kv_bytes = L * sum(int(n) for n in ctx_lens) * 2 * nkv * hd * esz
+    reps_bytes = B * (g + 1) * g * H * 4
+    dense = 2.0 * M * per_layer_w * L
+    vis_in_block = (g + 1) * (g + 2) // 2 + sum(g * (r + 1 + g) for r in range(g + 1))
+    attn = 0.0
+    for n in ctx_lens:
+        attn += 4.0 * nq * hd * (R * int(n) + vis_in_block) * L
+    return wbytes + kv_bytes + reps_bytes, dense + attn
+
+
+def cpu_baseline(wl, weights, ri):
+    """The CPU oracle (as it stands) on a bounded sample: one full round of request 0."""
+    from oracle import dpara_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    t = time.perf_counter()
+    O.dpara_round(wl.shape, weights, ri.ctx_feats[0], ri.spine[0], ri.target_logits[0], "bf16"
+                  if wl.shape.dtype == "bf16" else "f32")
+    dt = time.perf_counter() - t
+    per_round = dt * wl.batch  # a batch round = B requests; scaled linearly from request 0
+    return {"value": 1.0 / per_round, "unit": "rounds/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"one full round (context K/V projection of {int(ri.ctx_lens[0])} positions, all-boundary "
+                       f"backbone, greedy verify, select + AR head) of request 0, {dt:.1f} s"
+                       + (f", scaled x{wl.batch} to the batch" if wl.batch > 1 else ""))}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3_8b_b1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); requests are independent, so several "
+              f"GPUs would each run this path on their own share of the batch.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_27396_amd import dpara as D
+    from paper_2609_27396_amd import synth
+    from paper_2609_27396_amd.harness import DeviceRound
+
+    wl = synth.WORKLOADS[args.workload]
+    shape = wl.shape
+    log(f"[bench] workload {wl.name}: {wl.description}")
+    t0 = time.time()
+    weights = synth.make_weights(shape, seed=wl.seed_w)
+    ri = synth.make_round(wl)
+    log(f"[bench] inputs generated in {time.time() - t0:.1f} s")
+    dr = DeviceRound(shape, weights, ri)
+    torch.cuda.synchronize()
+    log(f"[bench] weights resident, context prefilled ({time.time() - t0:.1f} s)")
+
+    B = wl.batch
+    n_new_h = (ri.accept_planted.astype(np.int32) + 1)
+    n_new = torch.from_numpy(n_new_h).cuda()
+    base_len = torch.from_numpy((ri.ctx_lens - n_new_h).astype(np.int32)).cuda()
+
+    def step():
+        dr.ctx.ctx_len[:B].copy_(base_len)
+        dr.append(n_new)
+        dr.backbone()
+        dr.verify()
+        dr.head()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert dr.status() == 0, f"device status {dr.status()}"
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"[bench] {args.steps} steps: {ms:.3f} ms/step")
+
+    # per-phase durations (HIP events recorded by the library on the launching stream)
+    prof_steps = 5
+    D.dpara_profile_enable(True)
+    for _ in range(prof_steps):
+        step()
+    torch.cuda.synchronize()
+    phases = {}
+    for ph in D.PHASES:
+        tot, n = D.dpara_profile_read(ph)
+        if n:
+            phases[ph] = {"ms_per_step": tot / prof_steps, "launches_per_step": n / prof_steps,
+                          "avg_us": 1000.0 * tot / n}
+    D.dpara_profile_enable(False)
+    sum_ms = lambda names: sum(phases.get(p, {}).get("ms_per_step", 0.0) for p in names)
+    backbone_ms = sum_ms(["assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx", "attn_merge", "o_gemm",
+                          "gateup_gemm", "down_gemm", "final_norm"])
+    head_us = 1000.0 * sum_ms(["gather", "lm_head", "ar_step"])
+
+    # roofline of the dominant kernel: the gate/up SwiGLU GEMM
+    M = B * shape.rows
+    gb, gf = gateup_work(shape, M)
+    g_avg_s = phases["gateup_gemm"]["avg_us"] * 1e-6
+    peak_flops = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
+    hbm_bound = gb / (PEAK_HBM_GBS * 1e9) >= gf / (peak_flops * 1e12)
+    if hbm_bound:
+        roof = {"bound": "hbm", "achieved": gb / g_avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": gf / g_avg_s / 1e12, "peak": peak_flops, "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = "gemm_mfma_kernel (gate/up SwiGLU epilogue)"
+    roof["algorithmic_bytes_per_launch"] = gb
+    roof["algorithmic_flops_per_launch"] = gf
+    roof["avg_launch_us"] = g_avg_s * 1e6
+
+    bb_bytes, bb_flops = backbone_work(shape, B, ri.ctx_lens)
+    bb_s = backbone_ms * 1e-3
+    out = {
+        "metric": METRIC, "value": 1000.0 / ms, "unit": "rounds/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "gamma": shape.gamma,
+                   "ctx": int(ri.ctx_lens[0]) if wl.ctx_min == wl.ctx_max else [wl.ctx_min, wl.ctx_max],
+                   "layers": shape.n_layers, "hidden": shape.hidden, "heads": [shape.n_q_heads, shape.n_kv_heads],
+                   "head_dim": shape.head_dim, "ffn": shape.ffn, "vocab": shape.vocab, "ar_rank": shape.ar_rank,
+                   "rows_per_request": shape.rows},
+        "roofline": roof,
+        "backbone": {"ms": backbone_ms, "algorithmic_GB": bb_bytes / 1e9, "GFLOP": bb_flops / 1e9,
+                     "GB_s": bb_bytes / bb_s / 1e9, "TFLOP_s": bb_flops / bb_s / 1e12,
+                     "hbm_frac": bb_bytes / bb_s / 1e9 / PEAK_HBM_GBS,
+                     "mfma_frac": bb_flops / bb_s / 1e12 / peak_flops},
+        "head_us_per_round": head_us,
+        "verify_us_per_round": 1000.0 * sum_ms(["verify"]),
+        "append_us_per_round": 1000.0 * sum_ms(["append_gemm", "append_store"]),
+        "phases": phases,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample ...")
+        out["cpu_baseline"] = cpu_baseline(wl, weights, ri)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,200 @@
+/*
+ * dpara.h - C ABI of the DPara drafter hot path on MI355X (gfx950).
+ *
+ * Method: "When Parallel Drafter Meets Parallel Speculative Decoding" (DPara).
+ * One steady-state round (Algorithm 1) is:
+ *   dpara_ctx_append               C <- [C, C_new]           (Section 3.3; Appendix D,
+ *                                                              incremental projection)
+ *   dpara_backbone_all_boundaries  Precompute: all d+1 acceptance boundaries in one
+ *                                  forward under the tree mask (Section 3.2)
+ *   dpara_verify_greedy            Verify verdict (r, b) from target logits (Section 2.1)
+ *   dpara_select_and_head          select branch r, AR head y_i = argmax(l_i + W E(y_{i-1})),
+ *                                  y_0 = b; next block (b, y_1..y_d) (Algorithm 1; the head
+ *                                  equation of Section 3.2)
+ * "d" in the paper is `gamma` here (draft length; gamma+1 boundaries).
+ *
+ * Conventions shared by every call:
+ *  - Every pointer marked (device) is device memory owned by the caller.  The library
+ *    never allocates or frees memory; scratch space is the caller's workspace `ws`.
+ *  - Calls are asynchronous on the caller's HIP stream (`stream` is a hipStream_t; NULL
+ *    means the default stream).  Nothing is read back to the host.
+ *  - Return value: DPARA_OK or a negative DPARA_E_* code; dpara_last_error() then holds a
+ *    message (thread-local).  Host-detected errors launch nothing.
+ *  - Data errors only the device can see (token id outside [0, vocab), accepted length
+ *    outside [0, gamma], context capacity exceeded) set bits in the int32 status word at
+ *    byte offset 0 of the workspace (DPARA_STATUS_*); the offending item is clamped so
+ *    no access leaves its buffer.  The library never clears the word itself:
+ *    dpara_clear_status() enqueues a clear.
+ *  - Matrices follow the Linear orientation [out, in]: y = x W^T.  Row-major throughout.
+ *  - dtype (DPARA_F32 or DPARA_BF16) applies to matrices, embeddings, context features
+ *    and the K/V cache; norm gains are always float32; the residual stream, the
+ *    representations, logits and softmax are float32 in both modes.
+ *  - Calls on one workspace must not overlap (same stream, or ordered by events).
+ */
+#ifndef DPARA_H
+#define DPARA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  DPARA_OK = 0,
+  DPARA_E_INVALID = -1,     /* null or misaligned pointer, bad shape, unsupported size */
+  DPARA_E_UNSUPPORTED = -2, /* dtype / device architecture not supported */
+  DPARA_E_WORKSPACE = -3,   /* ws_bytes smaller than dpara_workspace_bytes() */
+  DPARA_E_CAPACITY = -4,    /* batch larger than the context cache's batch capacity */
+  DPARA_E_HIP = -5          /* a HIP launch or runtime call failed */
+};
+
+enum { DPARA_F32 = 0, DPARA_BF16 = 1 };
+
+enum {
+  DPARA_STATUS_TOKEN_RANGE = 1,  /* a token id was outside [0, vocab) */
+  DPARA_STATUS_CTX_FULL = 2,     /* an append would exceed ctx_cap; rows beyond it dropped */
+  DPARA_STATUS_VERDICT_RANGE = 4, /* accept_len outside [0, gamma] */
+  DPARA_STATUS_COUNT_RANGE = 8    /* an append count n_new outside [0, n_max] (clamped) */
+};
+
+/* Drafter shape.  Constraints: gamma in [1, 63]; head_dim in {64, 128};
+ * n_q_heads % n_kv_heads == 0; hidden, ffn, n_q_heads*head_dim and ar_rank multiples
+ * of 64; vocab >= 2.  qk_norm: per-head RMSNorm of q and k before RoPE (Qwen3). */
+typedef struct dpara_config {
+  int32_t n_layers;
+  int32_t hidden;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t ffn;
+  int32_t vocab;
+  int32_t gamma;
+  int32_t ar_rank;
+  int32_t qk_norm;
+  int32_t dtype;
+  float rms_eps;
+  float rope_base;
+} dpara_config_t;
+
+/* One pre-norm drafter block (device pointers; matrices in cfg dtype). */
+typedef struct dpara_layer_weights {
+  const float* attn_norm; /* [hidden] */
+  const void* wq;         /* [n_q_heads*head_dim, hidden] */
+  const void* wk;         /* [n_kv_heads*head_dim, hidden] */
+  const void* wv;         /* [n_kv_heads*head_dim, hidden] */
+  const float* q_norm;    /* [head_dim]; unused when qk_norm == 0 */
+  const float* k_norm;    /* [head_dim]; unused when qk_norm == 0 */
+  const void* wo;         /* [hidden, n_q_heads*head_dim] */
+  const float* mlp_norm;  /* [hidden] */
+  const void* w_gate;     /* [ffn, hidden] */
+  const void* w_up;       /* [ffn, hidden] */
+  const void* w_down;     /* [hidden, ffn] */
+} dpara_layer_weights_t;
+
+/* Frozen drafter parts (Section 3.2, "Trainable and frozen parameters"): the token
+ * embedding doubles as the full-vocabulary LM head (tied); the AR head's low-rank token
+ * embedding E and its vocabulary projection W (head equation, Section 3.2). */
+typedef struct dpara_weights {
+  const void* embed;                   /* [vocab, hidden] (device) */
+  const void* mask_emb;                /* [hidden] (device): the mask-token input row */
+  const float* final_norm;             /* [hidden] (device) */
+  const void* ar_E;                    /* [vocab, ar_rank] (device) */
+  const void* ar_W;                    /* [vocab, ar_rank] (device) */
+  const dpara_layer_weights_t* layers; /* [n_layers] (HOST array of device pointers) */
+} dpara_weights_t;
+
+/* Feature cache C kept as per-layer context K/V (Section 3.3: C over the accepted
+ * history; Appendix D: incremental projection of cached history features).
+ *   k: [n_layers, batch_cap, n_kv_heads, ctx_cap, head_dim]   (device, cfg dtype)
+ *   v: [n_layers, batch_cap, n_kv_heads, head_dim, ctx_cap]   (device, cfg dtype; the
+ *      value cache is stored transposed, positions contiguous)
+ *   ctx_len: [batch_cap] int32 (device): cached positions per request.
+ * Request b of a call uses slot b.  Positions are 0..ctx_len[b]-1. */
+typedef struct dpara_ctx {
+  void* k;
+  void* v;
+  int32_t* ctx_len;
+  int32_t batch_cap;
+  int32_t ctx_cap;
+} dpara_ctx_t;
+
+/* Bytes of workspace every call below needs for `batch` requests and a cache of
+ * `ctx_cap` positions (the same workspace serves all four calls).  0 on invalid input. */
+size_t dpara_workspace_bytes(const dpara_config_t* cfg, int32_t batch, int32_t ctx_cap);
+
+/* C <- [C, C_new] (Algorithm 1, cache update; Section 3.3).
+ * feats: [batch, n_max, hidden] (device, cfg dtype): fused target features of the newly
+ *        verified positions (t_0..t_r of the last round).
+ * n_new: [batch] int32 (device): rows of feats to append per request (0..n_max).
+ * For every layer: k = RoPE(kNorm(W_k f)), v = W_v f at positions ctx_len[b] + i, written
+ * into the cache; then ctx_len[b] += n_new[b].  Rows past ctx_cap are dropped and set
+ * DPARA_STATUS_CTX_FULL.  Any n_max >= 1 is accepted (long prefills are chunked). */
+int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx,
+                     int32_t batch, const void* feats, const int32_t* n_new, int32_t n_max,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Algorithm 1, Precompute: the M-DFlash backbone on the spine t_0..t_gamma for all
+ * gamma+1 acceptance boundaries in one forward (Section 3.2, tree mask).
+ * spine: [batch, gamma+1] int32 (device); t_0 is the previous bonus.
+ * reps:  [batch, gamma+1, gamma, hidden] float32 (device, output): final-norm hidden state
+ *        of branch r's mask i at reps[b][r][i-1]; branch r assumes t_1..t_r accepted.
+ * Rows per request: gamma+1 spine rows (position ctx_len[b]+j) and (gamma+1)*gamma mask
+ * rows (branch r, mask i at position ctx_len[b]+r+i).  Spine t_j sees t_0..t_j; branch r's
+ * masks see t_0..t_r and each other; every row sees the whole cache. */
+int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights_t* w,
+                                  const dpara_ctx_t* ctx, int32_t batch, const int32_t* spine,
+                                  float* reps, void* ws, size_t ws_bytes, void* stream);
+
+/* Greedy verification (Section 2.1; Algorithm 1, Verify).
+ * target_logits: [batch, gamma+1, vocab] (device), logits_dtype DPARA_F32 or DPARA_BF16:
+ *                row j scores the token after t_j.
+ * g_j = argmax_v logits[b][j][v] (lowest index on ties); accept_len[b] = number of leading
+ * drafts with t_i == g_{i-1}; bonus[b] = g_{accept_len}.  Outputs (device, int32):
+ * accept_len [batch], bonus [batch], target_argmax [batch, gamma+1] (may be NULL).
+ * Out-of-range draft ids in spine set DPARA_STATUS_TOKEN_RANGE (they never match). */
+int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* target_logits,
+                        int32_t logits_dtype, const int32_t* spine, int32_t* accept_len,
+                        int32_t* bonus, int32_t* target_argmax, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/* Select + AR head (Algorithm 1 after the barrier; head equation of Section 3.2).
+ * reps: [batch, gamma+1, gamma, hidden] float32 (device) from the backbone.
+ * accept_len, bonus: [batch] int32 (device) from verification.
+ * gathered: [batch, gamma, hidden] float32 (device, may be NULL): reps[b][accept_len[b]],
+ *           copied bit for bit.
+ * drafts: [batch, gamma] int32 (device): y_1..y_gamma with
+ *         l_i = gathered_i . embed^T, z_i = l_i + ar_W ar_E[y_{i-1}], y_0 = bonus,
+ *         y_i = argmax z_i (lowest index on ties).
+ * next_spine: [batch, gamma+1] int32 (device): (bonus, y_1..y_gamma).
+ * margins: [batch, gamma] float32 (device, may be NULL): top1 - top2 of z_i. */
+int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
+                          const float* reps, const int32_t* accept_len, const int32_t* bonus,
+                          float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/* Enqueue a clear of the status word at byte offset 0 of `ws` (a fill kernel). */
+int dpara_clear_status(void* ws, void* stream);
+
+/* Per-phase tracing with HIP events recorded on the launching stream (off by default).
+ * dpara_profile_enable(1) clears earlier records and starts recording a start/end event
+ * pair around every kernel launch of a phase; dpara_profile_enable(0) stops.
+ * dpara_profile_read(phase, &total_ms, &count) waits for the recorded events of `phase`
+ * and returns their summed duration and launch count.  Phases: "append_gemm",
+ * "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
+ * "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather",
+ * "lm_head", "ar_step".  Not for use while a stream is being captured into a graph. */
+int dpara_profile_enable(int32_t on);
+int dpara_profile_read(const char* phase, double* total_ms, int64_t* count);
+
+/* Message for the last non-OK return on this thread ("" if none). */
+const char* dpara_last_error(void);
+
+/* ABI version: 100 * major + minor. */
+int32_t dpara_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DPARA_H */

@@ -1,0 +1,545 @@
+// C ABI of the DPara drafter hot path: argument validation, workspace planning and the
+// launch sequence of each call on the caller's stream.  No allocation, no host sync.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/dpara.h"
+#include "internal.h"
+
+using namespace dpara;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(DPARA_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                    \
+  do {                                         \
+    hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int check_cfg(const dpara_config_t* c) {
+  if (!c) return fail(DPARA_E_INVALID, "cfg is NULL");
+  if (c->n_layers < 1) return fail(DPARA_E_INVALID, "n_layers must be >= 1");
+  if (c->hidden < 64 || c->hidden % 64) return fail(DPARA_E_INVALID, "hidden must be a positive multiple of 64");
+  if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads % c->n_kv_heads)
+    return fail(DPARA_E_INVALID, "n_q_heads must be a positive multiple of n_kv_heads");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(DPARA_E_INVALID, "head_dim must be 64 or 128");
+  if (c->ffn < 64 || c->ffn % 64) return fail(DPARA_E_INVALID, "ffn must be a positive multiple of 64");
+  if (c->vocab < 2) return fail(DPARA_E_INVALID, "vocab must be >= 2");
+  if (c->gamma < 1 || c->gamma > 63) return fail(DPARA_E_INVALID, "gamma must be in [1, 63]");
+  if (c->ar_rank < 64 || c->ar_rank % 64 || c->ar_rank > 1024)
+    return fail(DPARA_E_INVALID, "ar_rank must be a multiple of 64 in [64, 1024]");
+  if (c->qk_norm != 0 && c->qk_norm != 1) return fail(DPARA_E_INVALID, "qk_norm must be 0 or 1");
+  if (c->dtype != DPARA_F32 && c->dtype != DPARA_BF16) return fail(DPARA_E_UNSUPPORTED, "dtype must be F32 or BF16");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base > 1.f)) return fail(DPARA_E_INVALID, "rms_eps >= 0 and rope_base > 1 required");
+  return DPARA_OK;
+}
+
+#define CHECK_PTR(p, name)                                                         \
+  do {                                                                             \
+    if (!(p)) return fail(DPARA_E_INVALID, "%s is NULL", name);                    \
+    if (!aligned16(p)) return fail(DPARA_E_INVALID, "%s is not 16-byte aligned", name); \
+  } while (0)
+
+int check_weights(const dpara_config_t* c, const dpara_weights_t* w, bool need_layers) {
+  if (!w) return fail(DPARA_E_INVALID, "weights is NULL");
+  CHECK_PTR(w->embed, "embed");
+  if (need_layers) {
+    CHECK_PTR(w->mask_emb, "mask_emb");
+    CHECK_PTR(w->final_norm, "final_norm");
+    if (!w->layers) return fail(DPARA_E_INVALID, "layers is NULL");
+    for (int l = 0; l < c->n_layers; ++l) {
+      const dpara_layer_weights_t& L = w->layers[l];
+      CHECK_PTR(L.attn_norm, "attn_norm");
+      CHECK_PTR(L.wq, "wq");
+      CHECK_PTR(L.wk, "wk");
+      CHECK_PTR(L.wv, "wv");
+      CHECK_PTR(L.wo, "wo");
+      CHECK_PTR(L.mlp_norm, "mlp_norm");
+      CHECK_PTR(L.w_gate, "w_gate");
+      CHECK_PTR(L.w_up, "w_up");
+      CHECK_PTR(L.w_down, "w_down");
+      if (c->qk_norm) {
+        CHECK_PTR(L.q_norm, "q_norm");
+        CHECK_PTR(L.k_norm, "k_norm");
+      }
+    }
+  } else {
+    CHECK_PTR(w->ar_E, "ar_E");
+    CHECK_PTR(w->ar_W, "ar_W");
+  }
+  return DPARA_OK;
+}
+
+int check_ctx(const dpara_ctx_t* x, int batch) {
+  if (!x) return fail(DPARA_E_INVALID, "ctx is NULL");
+  CHECK_PTR(x->k, "ctx.k");
+  CHECK_PTR(x->v, "ctx.v");
+  if (!x->ctx_len) return fail(DPARA_E_INVALID, "ctx.ctx_len is NULL");
+  if (x->ctx_cap < 64 || x->ctx_cap % 64) return fail(DPARA_E_INVALID, "ctx_cap must be a positive multiple of 64");
+  if (batch > x->batch_cap) return fail(DPARA_E_CAPACITY, "batch %d exceeds ctx batch_cap %d", batch, x->batch_cap);
+  return DPARA_OK;
+}
+
+// Workspace layout (byte offsets), shared by all calls.
+struct Plan {
+  int B, R, M, S, chunk, CH, esz;
+  int v_chunk, v_chunks, h_chunk, h_chunks;
+  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, rope, vpart, G, logits, hpart, counters, F, KV32;
+  size_t total;
+};
+
+Plan make_plan(const dpara_config_t* c, int B, int ctx_cap) {
+  Plan p{};
+  p.B = B;
+  p.R = (c->gamma + 1) * (c->gamma + 1);
+  p.M = B * p.R;
+  p.esz = c->dtype == DPARA_BF16 ? 2 : 4;
+  const int hd = c->head_dim, nq = c->n_q_heads, nkv = c->n_kv_heads, H = c->hidden;
+  const int grp = nq / nkv;
+  if (c->dtype == DPARA_BF16) {
+    // split the context so that the MFMA pass launches a few hundred workgroups
+    const int base = B * nkv * ((grp * p.R + 63) / 64);
+    int S = (512 + base - 1) / base;
+    const int max_s = (ctx_cap + 255) / 256;
+    if (S > max_s) S = max_s;
+    if (S < 1) S = 1;
+    int chunk = (ctx_cap + S - 1) / S;
+    chunk = (chunk + 63) / 64 * 64;
+    p.chunk = chunk;
+    p.S = (ctx_cap + chunk - 1) / chunk;
+  } else {
+    p.S = 1;
+    p.chunk = ctx_cap;
+  }
+  p.CH = p.R;
+  p.v_chunk = 4096;
+  p.v_chunks = (c->vocab + p.v_chunk - 1) / p.v_chunk;
+  p.h_chunk = 512;
+  p.h_chunks = (c->vocab + p.h_chunk - 1) / p.h_chunk;
+  const size_t M = p.M;
+  size_t off = 256;  // status header
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += up256(bytes);
+    return o;
+  };
+  p.X = take(M * H * 4);
+  p.A = take(M * H * p.esz);
+  p.QKV = take(M * (size_t)(nq + 2 * nkv) * hd * 4);
+  p.Q = take(M * (size_t)nq * hd * p.esz);
+  p.Kb = take(M * (size_t)nkv * hd * p.esz);
+  p.Vb = take(M * (size_t)nkv * hd * p.esz);
+  p.Opart = take((size_t)B * nq * p.R * p.S * hd * 4);
+  p.ML = take((size_t)B * nq * p.R * p.S * 2 * 4);
+  p.O = take(M * (size_t)nq * hd * p.esz);
+  p.Hmid = take(M * (size_t)c->ffn * p.esz);
+  p.rope = take((size_t)B * (2 * c->gamma + 1) * (hd / 2) * 8);
+  p.vpart = take((size_t)B * (c->gamma + 1) * p.v_chunks * 8);
+  p.G = take((size_t)B * c->gamma * H * 4);
+  p.logits = take((size_t)B * c->gamma * c->vocab * 4);
+  p.hpart = take((size_t)B * p.h_chunks * 16);
+  p.counters = take((size_t)B * 4);
+  p.F = take((size_t)B * p.CH * H * p.esz);
+  p.KV32 = take((size_t)B * p.CH * 2 * nkv * hd * 4);
+  p.total = off;
+  return p;
+}
+
+std::mutex g_dev_mu;
+int g_dev_ok[64];  // 0 unknown, 1 gfx950, -1 other
+
+int check_device() {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(DPARA_E_UNSUPPORTED, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_dev_mu);
+  if (g_dev_ok[dev] == 0) {
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, dev), "hipGetDeviceProperties");
+    g_dev_ok[dev] = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+  }
+  if (g_dev_ok[dev] != 1) return fail(DPARA_E_UNSUPPORTED, "device %d is not gfx950 (MI355X)", dev);
+  return DPARA_OK;
+}
+
+int check_ws(const Plan& p, void* ws, size_t ws_bytes) {
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
+  if (ws_bytes < p.total)
+    return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, p.total);
+  return DPARA_OK;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return (T*)((char*)ws + off);
+}
+
+// ---------------------------------------------------------------- phase tracing
+struct ProfRec {
+  const char* phase;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;   // events are created once and reused across enables
+size_t g_prof_used = 0;
+
+}  // namespace
+
+namespace dpara {
+Phase::Phase(const char* name, hipStream_t s) : slot(-1), st(s) {
+  if (!g_prof_on) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (g_prof_used == g_prof.size()) {
+    ProfRec r{name, nullptr, nullptr};
+    if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return;
+    g_prof.push_back(r);
+  }
+  slot = (int)g_prof_used++;
+  g_prof[slot].phase = name;
+  (void)hipEventRecord(g_prof[slot].a, st);
+}
+Phase::~Phase() {
+  if (slot < 0) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  (void)hipEventRecord(g_prof[slot].b, st);
+}
+}  // namespace dpara
+
+extern "C" {
+
+int dpara_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (on) {
+    for (size_t i = 0; i < g_prof_used; ++i) (void)hipEventSynchronize(g_prof[i].b);
+    g_prof_used = 0;
+  }
+  g_prof_on = on != 0;
+  return DPARA_OK;
+}
+
+int dpara_profile_read(const char* phase, double* total_ms, int64_t* count) {
+  if (!phase || !total_ms || !count) return fail(DPARA_E_INVALID, "phase, total_ms and count must be non-NULL");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  double t = 0.0;
+  int64_t n = 0;
+  for (size_t i = 0; i < g_prof_used; ++i) {
+    if (strcmp(g_prof[i].phase, phase) != 0) continue;
+    HIP_TRY(hipEventSynchronize(g_prof[i].b), "hipEventSynchronize");
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, g_prof[i].a, g_prof[i].b), "hipEventElapsedTime");
+    t += ms;
+    ++n;
+  }
+  *total_ms = t;
+  *count = n;
+  return DPARA_OK;
+}
+
+
+int32_t dpara_version(void) { return 100; }
+
+const char* dpara_last_error(void) { return g_err.c_str(); }
+
+size_t dpara_workspace_bytes(const dpara_config_t* cfg, int32_t batch, int32_t ctx_cap) {
+  if (check_cfg(cfg) != DPARA_OK || batch < 1 || ctx_cap < 64 || ctx_cap % 64) return 0;
+  return make_plan(cfg, batch, ctx_cap).total;
+}
+
+int dpara_clear_status(void* ws, void* stream) {
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  int rc = check_device();
+  if (rc) return rc;
+  HIP_TRY(launch_clear_status((int*)ws, (hipStream_t)stream), "clear_status");
+  return DPARA_OK;
+}
+
+int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx, int32_t batch,
+                     const void* feats, const int32_t* n_new, int32_t n_max, void* ws, size_t ws_bytes,
+                     void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if ((rc = check_ctx(ctx, batch))) return rc;
+  if (!w || !w->layers) return fail(DPARA_E_INVALID, "weights or layers is NULL");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    CHECK_PTR(w->layers[l].wk, "wk");
+    CHECK_PTR(w->layers[l].wv, "wv");
+    if (cfg->qk_norm) CHECK_PTR(w->layers[l].k_norm, "k_norm");
+  }
+  CHECK_PTR(feats, "feats");
+  if (!n_new) return fail(DPARA_E_INVALID, "n_new is NULL");
+  if (n_max < 1) return fail(DPARA_E_INVALID, "n_max must be >= 1");
+  const Plan p = make_plan(cfg, batch, ctx->ctx_cap);
+  if ((rc = check_ws(p, ws, ws_bytes))) return rc;
+  if ((rc = check_device())) return rc;
+
+  hipStream_t st = (hipStream_t)stream;
+  const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nkv = cfg->n_kv_heads;
+  int* status = at<int>(ws, 0);
+  const size_t layer_elems = (size_t)ctx->batch_cap * nkv * ctx->ctx_cap * hd;
+  const size_t esz = p.esz;
+  for (int c0 = 0; c0 < n_max; c0 += p.CH) {
+    HIP_TRY(launch_gather_feats(dt, batch, p.CH, c0, n_max, H, feats, at<void>(ws, p.F), st), "gather_feats");
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      GemmArgs g{};
+      g.A = at<void>(ws, p.F);
+      g.lda = H;
+      g.B0 = w->layers[l].wk;
+      g.B1 = w->layers[l].wv;
+      g.B2 = w->layers[l].wv;
+      g.n1 = nkv * hd;
+      g.n2 = 2 * nkv * hd;
+      g.M = batch * p.CH;
+      g.N = 2 * nkv * hd;
+      g.K = H;
+      g.C = at<void>(ws, p.KV32);
+      g.ldc = g.N;
+      {
+        Phase ph("append_gemm", st);
+        HIP_TRY(launch_gemm(dt == DPARA_BF16 ? A_BF16 : A_F32, EPI_STORE_F32, g, st), "append kv gemm");
+      }
+      char* kc = (char*)ctx->k + l * layer_elems * esz;
+      char* vc = (char*)ctx->v + l * layer_elems * esz;
+      Phase ph("append_store", st);
+      HIP_TRY(launch_kv_store(dt, batch, p.CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps, cfg->rope_base,
+                              at<float>(ws, p.KV32), w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
+                              vc, status, st),
+              "kv_store");
+    }
+  }
+  HIP_TRY(launch_ctx_len_update(batch, n_max, ctx->ctx_cap, n_new, ctx->ctx_len, status, st), "ctx_len_update");
+  return DPARA_OK;
+}
+
+int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx,
+                                  int32_t batch, const int32_t* spine, float* reps, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if ((rc = check_weights(cfg, w, true))) return rc;
+  if ((rc = check_ctx(ctx, batch))) return rc;
+  if (!spine) return fail(DPARA_E_INVALID, "spine is NULL");
+  CHECK_PTR(reps, "reps");
+  const Plan p = make_plan(cfg, batch, ctx->ctx_cap);
+  if ((rc = check_ws(p, ws, ws_bytes))) return rc;
+  if ((rc = check_device())) return rc;
+
+  hipStream_t st = (hipStream_t)stream;
+  const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q_heads, nkv = cfg->n_kv_heads;
+  const int g = cfg->gamma, R = p.R, M = p.M, F = cfg->ffn;
+  const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
+  int* status = at<int>(ws, 0);
+  float* X = at<float>(ws, p.X);
+  const size_t layer_elems = (size_t)ctx->batch_cap * nkv * ctx->ctx_cap * hd;
+
+  {
+  Phase ph("assemble", st);
+  HIP_TRY(launch_assemble_rows(dt, batch, R, g, H, cfg->vocab, spine, w->embed, w->mask_emb, X, status, st),
+          "assemble_rows");
+  HIP_TRY(launch_rope_table(batch, 2 * g + 1, hd, cfg->rope_base, ctx->ctx_len, 0, at<float2>(ws, p.rope), st),
+          "rope_table");
+  }
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const dpara_layer_weights_t& Lw = w->layers[l];
+    {
+    Phase ph("rmsnorm", st);
+    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.attn_norm, cfg->rms_eps, at<void>(ws, p.A), st), "attn_norm");
+    }
+    GemmArgs q{};
+    q.A = at<void>(ws, p.A);
+    q.lda = H;
+    q.B0 = Lw.wq;
+    q.B1 = Lw.wk;
+    q.B2 = Lw.wv;
+    q.n1 = nq * hd;
+    q.n2 = (nq + nkv) * hd;
+    q.M = M;
+    q.N = (nq + 2 * nkv) * hd;
+    q.K = H;
+    q.C = at<void>(ws, p.QKV);
+    q.ldc = q.N;
+    {
+    Phase ph("qkv_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_STORE_F32, q, st), "qkv gemm");
+    }
+    {
+    Phase ph("qk_norm_rope", st);
+    HIP_TRY(launch_qk_norm_rope(dt, batch, R, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
+                                Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
+                                at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
+            "qk_norm_rope");
+    }
+    AttnArgs aa{};
+    aa.B = batch;
+    aa.R = R;
+    aa.gamma = g;
+    aa.n_q = nq;
+    aa.n_kv = nkv;
+    aa.hd = hd;
+    aa.Q = at<void>(ws, p.Q);
+    aa.Kb = at<void>(ws, p.Kb);
+    aa.Vb = at<void>(ws, p.Vb);
+    aa.Kc = (const char*)ctx->k + l * layer_elems * p.esz;
+    aa.Vc = (const char*)ctx->v + l * layer_elems * p.esz;
+    aa.cap = ctx->ctx_cap;
+    aa.ctx_len = ctx->ctx_len;
+    aa.S = p.S;
+    aa.chunk = p.chunk;
+    aa.Opart = at<float>(ws, p.Opart);
+    aa.MLpart = at<float>(ws, p.ML);
+    aa.O = at<void>(ws, p.O);
+    aa.spine_only = 0;
+    HIP_TRY(launch_attention(dt, aa, st), "attention");
+    GemmArgs o{};
+    o.A = at<void>(ws, p.O);
+    o.lda = nq * hd;
+    o.B0 = o.B1 = o.B2 = Lw.wo;
+    o.n1 = o.n2 = H;
+    o.M = M;
+    o.N = H;
+    o.K = nq * hd;
+    o.C = X;
+    o.ldc = H;
+    {
+    Phase ph("o_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, o, st), "o-proj gemm");
+    }
+    {
+    Phase ph("rmsnorm", st);
+    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.mlp_norm, cfg->rms_eps, at<void>(ws, p.A), st), "mlp_norm");
+    }
+    GemmArgs gu{};
+    gu.A = at<void>(ws, p.A);
+    gu.lda = H;
+    gu.B0 = Lw.w_gate;
+    gu.B1 = Lw.w_up;
+    gu.B2 = Lw.w_up;
+    gu.n1 = gu.n2 = F;
+    gu.M = M;
+    gu.N = F;
+    gu.K = H;
+    gu.C = at<void>(ws, p.Hmid);
+    gu.ldc = F;
+    {
+    Phase ph("gateup_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_SWIGLU, gu, st), "gate/up gemm");
+    }
+    GemmArgs dn{};
+    dn.A = at<void>(ws, p.Hmid);
+    dn.lda = F;
+    dn.B0 = dn.B1 = dn.B2 = Lw.w_down;
+    dn.n1 = dn.n2 = H;
+    dn.M = M;
+    dn.N = H;
+    dn.K = F;
+    dn.C = X;
+    dn.ldc = H;
+    {
+    Phase ph("down_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, dn, st), "down gemm");
+    }
+  }
+  // reps[b][r][i-1] = final_norm of mask rows: input row (m / (R-g-1)) * R*H + (g+1 + m % (R-g-1)) * H
+  const int nmask = R - g - 1;
+  Phase ph("final_norm", st);
+  HIP_TRY(launch_rmsnorm(0, batch * nmask, H, X, nmask, (int64_t)R * H, g + 1, w->final_norm, cfg->rms_eps, reps,
+                         st),
+          "final_norm");
+  return DPARA_OK;
+}
+
+int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* target_logits, int32_t logits_dtype,
+                        const int32_t* spine, int32_t* accept_len, int32_t* bonus, int32_t* target_argmax,
+                        void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if (logits_dtype != DPARA_F32 && logits_dtype != DPARA_BF16)
+    return fail(DPARA_E_UNSUPPORTED, "logits_dtype must be F32 or BF16");
+  if (!target_logits || !spine || !accept_len || !bonus)
+    return fail(DPARA_E_INVALID, "target_logits, spine, accept_len and bonus must be non-NULL");
+  const Plan p = make_plan(cfg, batch, 64);
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  const size_t need = p.vpart + up256((size_t)batch * (cfg->gamma + 1) * p.v_chunks * 8);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if ((rc = check_device())) return rc;
+  HIP_TRY(launch_verify(logits_dtype, batch, cfg->gamma, cfg->vocab, target_logits, spine, accept_len, bonus,
+                        target_argmax, at<uint64_t>(ws, p.vpart), p.v_chunks, p.v_chunk, at<int>(ws, 0),
+                        (hipStream_t)stream),
+          "verify");
+  return DPARA_OK;
+}
+
+int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch, const float* reps,
+                          const int32_t* accept_len, const int32_t* bonus, float* gathered, int32_t* drafts,
+                          int32_t* next_spine, float* margins, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if ((rc = check_weights(cfg, w, false))) return rc;
+  CHECK_PTR(reps, "reps");
+  if (gathered && !aligned16(gathered)) return fail(DPARA_E_INVALID, "gathered is not 16-byte aligned");
+  if (!accept_len || !bonus || !drafts || !next_spine)
+    return fail(DPARA_E_INVALID, "accept_len, bonus, drafts and next_spine must be non-NULL");
+  const Plan p = make_plan(cfg, batch, 64);
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
+  const size_t need = p.counters + up256((size_t)batch * 4);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if ((rc = check_device())) return rc;
+
+  hipStream_t st = (hipStream_t)stream;
+  const int g = cfg->gamma, H = cfg->hidden, V = cfg->vocab;
+  int* status = at<int>(ws, 0);
+  float* G = at<float>(ws, p.G);
+  HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, G, gathered, status, st), "gather_branch");
+  GemmArgs lm{};
+  lm.A = G;
+  lm.lda = H;
+  lm.B0 = lm.B1 = lm.B2 = w->embed;
+  lm.n1 = lm.n2 = V;
+  lm.M = batch * g;
+  lm.N = V;
+  lm.K = H;
+  lm.C = at<void>(ws, p.logits);
+  lm.ldc = V;
+  {
+    Phase ph("lm_head", st);
+    HIP_TRY(launch_gemm(cfg->dtype == DPARA_BF16 ? A_F32SPLIT : A_F32, EPI_STORE_F32, lm, st), "lm head gemm");
+  }
+  HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
+                         drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
+                         at<unsigned>(ws, p.counters), status, st),
+          "ar head");
+  return DPARA_OK;
+}
+
+}  // extern "C"

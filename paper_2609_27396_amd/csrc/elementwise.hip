@@ -1,0 +1,280 @@
+// Row assembly, RMSNorm, q/k-norm + RoPE and the context-append kernels.
+#include <math.h>
+
+#include "common.h"
+#include "internal.h"
+
+namespace dpara {
+namespace {
+
+// Row layout of one request (Section 3.2): rows 0..gamma are the spine t_0..t_gamma;
+// row gamma+1 + r*gamma + (i-1) is mask i of branch r.  Position offset from the
+// context length: spine j -> j; branch r mask i -> r + i.
+__device__ __forceinline__ int row_pos_offset(int row, int gamma) {
+  if (row <= gamma) return row;
+  const int k = row - gamma - 1;
+  return k / gamma + k % gamma + 1;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, int V, const int* spine,
+                                                     const T* embed, const T* mask_emb, float* X,
+                                                     int* status) {
+  const int row = blockIdx.x, b = blockIdx.y;
+  const T* src = mask_emb;
+  if (row <= gamma) {
+    int t = spine[b * (gamma + 1) + row];
+    if (t < 0 || t >= V) {
+      if (threadIdx.x == 0) raise_status(status, 1);
+      t = 0;
+    }
+    src = embed + (int64_t)t * H;
+  }
+  float* dst = X + ((int64_t)b * R + row) * H;
+  for (int i = threadIdx.x; i < H; i += 256) dst[i] = ld_f(src + i);
+}
+
+template <typename TO>
+__global__ __launch_bounds__(256) void rmsnorm_rows(int H, const float* X, int grp, int64_t in_stride,
+                                                    int in_off, const float* g, float eps, TO* Y) {
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  const float* x = X + (int64_t)(m / grp) * in_stride + (int64_t)(in_off + m % grp) * H;
+  float ss = 0.f;
+  for (int i = threadIdx.x * 4; i < H; i += 1024) {
+    const float4 v = *(const float4*)(x + i);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum256(ss, red);
+  const float r = 1.0f / sqrtf(ss / (float)H + eps);
+  TO* y = Y + (int64_t)m * H;
+  for (int i = threadIdx.x * 4; i < H; i += 1024) {
+    const float4 v = *(const float4*)(x + i);
+    const float4 gg = *(const float4*)(g + i);
+    st_f(y + i + 0, v.x * r * gg.x);
+    st_f(y + i + 1, v.y * r * gg.y);
+    st_f(y + i + 2, v.z * r * gg.z);
+    st_f(y + i + 3, v.w * r * gg.w);
+  }
+}
+
+__global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx_len, int pos_off,
+                                  float2* table) {
+  const int b = blockIdx.y;
+  const int half = hd / 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n_pos * half) return;
+  const int i = idx / half, p = idx % half;
+  float c, s;
+  rope_cs(ctx_len[b] + pos_off + i, p, hd, base, &c, &s);
+  table[((int64_t)b * n_pos + i) * half + p] = make_float2(c, s);
+}
+
+// One block per row; waves loop over head slots (q heads, k heads, v heads).
+template <typename T>
+__global__ __launch_bounds__(256) void qk_norm_rope(int R, int gamma, int n_q, int n_kv, int hd, int qk_norm,
+                                                    float eps, const float* QKV, const float* qn,
+                                                    const float* kn, const float2* table, T* Q, T* Kb,
+                                                    T* Vb) {
+  const int m = blockIdx.x;
+  const int b = m / R, row = m % R;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = hd / 2, grp = n_q / n_kv;
+  const int n_slots = n_q + 2 * n_kv;
+  const float* src = QKV + (int64_t)m * n_slots * hd;
+  const float2* cs = table + ((int64_t)b * (2 * gamma + 1) + row_pos_offset(row, gamma)) * half;
+  for (int slot = wave; slot < n_slots; slot += 4) {
+    const float* x = src + slot * hd;
+    if (slot < n_q + n_kv) {
+      const bool isq = slot < n_q;
+      const bool act = lane < half;
+      float x1 = act ? x[lane] : 0.f, x2 = act ? x[lane + half] : 0.f;
+      if (qk_norm) {
+        const float ss = wave_sum(x1 * x1 + x2 * x2);
+        const float r = 1.0f / sqrtf(ss / (float)hd + eps);
+        const float* gn = isq ? qn : kn;
+        if (act) {
+          x1 = x1 * r * gn[lane];
+          x2 = x2 * r * gn[lane + half];
+        }
+      }
+      if (act) {
+        const float2 c = cs[lane];
+        const float y1 = x1 * c.x - x2 * c.y;
+        const float y2 = x2 * c.x + x1 * c.y;
+        T* dst;
+        if (isq) {
+          const int h = slot, kvh = h / grp, gi = h % grp;
+          dst = Q + (((int64_t)(b * n_kv + kvh) * grp + gi) * R + row) * hd;
+        } else {
+          const int kvh = slot - n_q;
+          dst = Kb + ((int64_t)(b * n_kv + kvh) * R + row) * hd;
+        }
+        st_f(dst + lane, y1);
+        st_f(dst + lane + half, y2);
+      }
+    } else {
+      const int kvh = slot - n_q - n_kv;
+      T* dst = Vb + ((int64_t)(b * n_kv + kvh) * R + row) * hd;
+      for (int d = lane; d < hd; d += 64) st_f(dst + d, x[d]);
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gather_feats(int CH, int c0, int n_max, int H, const T* feats, T* F) {
+  const int m = blockIdx.x, b = m / CH, i = m % CH;
+  const int c = c0 + i;
+  T* dst = F + (int64_t)m * H;
+  if (c >= n_max) {
+    for (int k = threadIdx.x; k < H; k += 256) dst[k] = (T)0;
+    return;
+  }
+  const T* src = feats + ((int64_t)b * n_max + c) * H;
+  for (int k = threadIdx.x; k < H; k += 256) dst[k] = src[k];
+}
+
+__device__ __forceinline__ int clamp_count(int n, int n_max) { return n < 0 ? 0 : (n > n_max ? n_max : n); }
+
+// K/V of appended rows: k = RoPE(kNorm(W_k f)) at its position, v = W_v f; K rows go to
+// [pos][hd], V to the transposed cache [hd][pos].
+template <typename T>
+__global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n_kv, int hd, int qk_norm, float eps,
+                                                double base, const float* KV, const float* kn,
+                                                const int* n_new, const int* ctx_len, int cap, T* Kc,
+                                                T* Vc) {
+  const int m = blockIdx.x, b = m / CH, i = m % CH;
+  const int c = c0 + i;
+  if (c >= clamp_count(n_new[b], n_max)) return;
+  const int pos = max(ctx_len[b], 0) + c;
+  if (pos >= cap) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = hd / 2;
+  const float* src = KV + (int64_t)m * 2 * n_kv * hd;
+  for (int kvh = wave; kvh < n_kv; kvh += 4) {
+    const float* x = src + kvh * hd;
+    const bool act = lane < half;
+    float x1 = act ? x[lane] : 0.f, x2 = act ? x[lane + half] : 0.f;
+    if (qk_norm) {
+      const float ss = wave_sum(x1 * x1 + x2 * x2);
+      const float r = 1.0f / sqrtf(ss / (float)hd + eps);
+      if (act) {
+        x1 = x1 * r * kn[lane];
+        x2 = x2 * r * kn[lane + half];
+      }
+    }
+    const int64_t kvb = (int64_t)(b * n_kv + kvh);
+    if (act) {
+      float cc, ss;
+      rope_cs(pos, lane, hd, base, &cc, &ss);
+      T* kd = Kc + (kvb * cap + pos) * hd;
+      st_f(kd + lane, x1 * cc - x2 * ss);
+      st_f(kd + lane + half, x2 * cc + x1 * ss);
+    }
+    const float* xv = src + (n_kv + kvh) * hd;
+    for (int d = lane; d < hd; d += 64) st_f(Vc + (kvb * hd + d) * cap + pos, xv[d]);
+  }
+}
+
+__global__ void ctx_len_update_kernel(int B, int n_max, int cap, const int* n_new, int* ctx_len, int* status) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int raw = n_new[b];
+  const int n = clamp_count(raw, n_max);
+  if (n != raw) raise_status(status, 8);
+  int L = max(ctx_len[b], 0) + n;
+  if (L > cap) {
+    raise_status(status, 2);
+    L = cap;
+  }
+  ctx_len[b] = L;
+}
+
+__global__ void clear_status_kernel(int* status) { status[threadIdx.x] = 0; }
+
+}  // namespace
+
+hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V, const int* spine,
+                                const void* embed, const void* mask_emb, float* X, int* status,
+                                hipStream_t st) {
+  dim3 grid(R, B);
+  if (dtype == 1)
+    hipLaunchKernelGGL(assemble_rows<bf16_t>, grid, dim3(256), 0, st, R, gamma, H, V, spine,
+                       (const bf16_t*)embed, (const bf16_t*)mask_emb, X, status);
+  else
+    hipLaunchKernelGGL(assemble_rows<float>, grid, dim3(256), 0, st, R, gamma, H, V, spine,
+                       (const float*)embed, (const float*)mask_emb, X, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int out_dtype, int rows, int H, const float* X, int grp, int64_t in_stride,
+                          int in_off, const float* g, float eps, void* Y, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (out_dtype == 1)
+    hipLaunchKernelGGL(rmsnorm_rows<bf16_t>, dim3(rows), dim3(256), 0, st, H, X, grp, in_stride, in_off, g,
+                       eps, (bf16_t*)Y);
+  else
+    hipLaunchKernelGGL(rmsnorm_rows<float>, dim3(rows), dim3(256), 0, st, H, X, grp, in_stride, in_off, g,
+                       eps, (float*)Y);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len, int pos_off,
+                             float2* table, hipStream_t st) {
+  const int n = n_pos * (hd / 2);
+  dim3 grid((n + 255) / 256, B);
+  hipLaunchKernelGGL(rope_table_kernel, grid, dim3(256), 0, st, n_pos, hd, (double)base, ctx_len, pos_off,
+                     table);
+  return hipGetLastError();
+}
+
+hipError_t launch_qk_norm_rope(int dtype, int B, int R, int gamma, int n_q, int n_kv, int hd, int qk_norm,
+                               float eps, const float* QKV, const float* qn, const float* kn,
+                               const float2* table, void* Q, void* Kb, void* Vb, hipStream_t st) {
+  dim3 grid(B * R);
+  if (dtype == 1)
+    hipLaunchKernelGGL(qk_norm_rope<bf16_t>, grid, dim3(256), 0, st, R, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
+                       qn, kn, table, (bf16_t*)Q, (bf16_t*)Kb, (bf16_t*)Vb);
+  else
+    hipLaunchKernelGGL(qk_norm_rope<float>, grid, dim3(256), 0, st, R, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
+                       qn, kn, table, (float*)Q, (float*)Kb, (float*)Vb);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int H, const void* feats,
+                               void* F, hipStream_t st) {
+  if (dtype == 1)
+    hipLaunchKernelGGL(gather_feats<bf16_t>, dim3(B * CH), dim3(256), 0, st, CH, c0, n_max, H,
+                       (const bf16_t*)feats, (bf16_t*)F);
+  else
+    hipLaunchKernelGGL(gather_feats<float>, dim3(B * CH), dim3(256), 0, st, CH, c0, n_max, H,
+                       (const float*)feats, (float*)F);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd, int qk_norm,
+                           float eps, float base, const float* KV, const float* kn, const int* n_new,
+                           const int* ctx_len, int cap, void* Kc, void* Vc, int* status, hipStream_t st) {
+  (void)status;
+  if (dtype == 1)
+    hipLaunchKernelGGL(kv_store<bf16_t>, dim3(B * CH), dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
+                       (double)base, KV, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc);
+  else
+    hipLaunchKernelGGL(kv_store<float>, dim3(B * CH), dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
+                       (double)base, KV, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc);
+  return hipGetLastError();
+}
+
+hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, int* ctx_len, int* status,
+                                 hipStream_t st) {
+  hipLaunchKernelGGL(ctx_len_update_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, n_max, cap, n_new, ctx_len,
+                     status);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_status(int* status, hipStream_t st) {
+  hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, status);
+  return hipGetLastError();
+}
+
+}  // namespace dpara

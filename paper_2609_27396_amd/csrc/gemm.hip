@@ -1,0 +1,310 @@
+// Dense projections of the drafter: C[M, N] (op)= A[M, K] . B[N, K]^T.
+//
+// bf16 path: LDS-tiled v_mfma_f32_16x16x32_bf16 kernel, 256 threads (2 x 2 waves),
+// BK = 64, double-buffered LDS with register prefetch of the next K tile, fp32
+// accumulation, fused epilogues (store fp32, add into the fp32 residual stream,
+// SwiGLU -> bf16).  The tile order is XCD-aware: the M tiles that share one weight
+// tile run on the same XCD back to back, so a weight tile is fetched from HBM once
+// and served to the others from that XCD's L2.
+// float32 path: a plain LDS-tiled FMA kernel for the float32 model configuration.
+#include "common.h"
+#include "internal.h"
+
+namespace dpara {
+namespace {
+
+constexpr int BK = 64;
+constexpr int LDK = BK + 8;  // padded LDS row in bf16 elements (144 bytes)
+
+__device__ __forceinline__ float silu_f(float g) { return g / (1.0f + expf(-g)); }
+
+// Logical tile for physical workgroup p: tiles are split into 8 contiguous ranges, one per
+// XCD (workgroups are dispatched round-robin over the 8 XCDs), M fastest inside a range.
+__device__ __forceinline__ void tile_of(int p, int MT, int NT, int& mt, int& nt) {
+  const int total = MT * NT;
+  const int per = total >> 3;
+  int L = p;
+  if (p < (per << 3)) L = (p & 7) * per + (p >> 3);
+  mt = L % MT;
+  nt = L / MT;
+}
+
+// Base pointer of tile-local B row `lr` of N tile `nt` (B rows may come from segments).
+template <typename TB, int BN, int EPI>
+__device__ __forceinline__ const TB* b_row(const GemmArgs& a, int nt, int lr, bool& ok) {
+  if (EPI == EPI_SWIGLU) {
+    constexpr int half = BN / 2;
+    const int f = nt * half + (lr % half);
+    ok = f < a.N;
+    const TB* base = (const TB*)(lr < half ? a.B0 : a.B1);
+    return base + (int64_t)(ok ? f : 0) * a.K;
+  } else {
+    int n = nt * BN + lr;
+    ok = n < a.N;
+    if (!ok) n = 0;
+    if (n < a.n1) return (const TB*)a.B0 + (int64_t)n * a.K;
+    if (n < a.n2) return (const TB*)a.B1 + (int64_t)(n - a.n1) * a.K;
+    return (const TB*)a.B2 + (int64_t)(n - a.n2) * a.K;
+  }
+}
+
+// LDS row of B fragment ni for wave column wn.  SwiGLU tiles hold BN/2 gate rows then
+// BN/2 up rows; each wave takes the same FFN columns from both halves so that gate and
+// up of one output land in the same thread.
+template <int BN, int WN, int FN, int EPI>
+__device__ __forceinline__ int b_frag_row(int wn, int ni) {
+  if (EPI == EPI_SWIGLU) {
+    return ni < FN / 2 ? wn * (WN / 2) + ni * 16 : BN / 2 + wn * (WN / 2) + (ni - FN / 2) * 16;
+  }
+  return wn * WN + ni * 16;
+}
+
+template <int BM, int BN, int EPI, int AMODE>
+__global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs a, int MT, int NT) {
+  constexpr int NA = (AMODE == A_F32SPLIT) ? 2 : 1;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 16, FN = WN / 16;
+  constexpr int A_LD = (AMODE == A_F32SPLIT) ? BM * BK / 4 / 256 : BM * BK / 8 / 256;
+  constexpr int B_LD = BN * BK / 8 / 256;
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][NA][BM * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LDK];
+
+  int mt, nt;
+  tile_of(blockIdx.x, MT, NT, mt, nt);
+  const int m0 = mt * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // global source rows of this thread's loads
+  const bf16_t* bp[B_LD];
+  bool bok[B_LD];
+#pragma unroll
+  for (int i = 0; i < B_LD; ++i) bp[i] = b_row<bf16_t, BN, EPI>(a, nt, tid / 8 + 32 * i, bok[i]);
+  const int bcol = (tid & 7) * 8;
+
+  uint4 ra[A_LD];
+  float4 rf[(AMODE == A_F32SPLIT) ? A_LD : 1];
+  uint4 rb[B_LD];
+
+  auto load_tile = [&](int kt) {
+    const int k0 = kt * BK;
+    if constexpr (AMODE == A_F32SPLIT) {
+      const float* A = (const float*)a.A;
+#pragma unroll
+      for (int i = 0; i < A_LD; ++i) {
+        const int gm = m0 + tid / 16 + 16 * i;
+        rf[i] = gm < a.M ? *(const float4*)(A + (int64_t)gm * a.lda + k0 + (tid & 15) * 4)
+                         : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    } else {
+      const bf16_t* A = (const bf16_t*)a.A;
+#pragma unroll
+      for (int i = 0; i < A_LD; ++i) {
+        const int gm = m0 + tid / 8 + 32 * i;
+        ra[i] = gm < a.M ? *(const uint4*)(A + (int64_t)gm * a.lda + k0 + (tid & 7) * 8)
+                         : make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i)
+      rb[i] = bok[i] ? *(const uint4*)(bp[i] + k0 + bcol) : make_uint4(0, 0, 0, 0);
+  };
+
+  auto store_tile = [&](int buf) {
+    if constexpr (AMODE == A_F32SPLIT) {
+#pragma unroll
+      for (int i = 0; i < A_LD; ++i) {
+        const int r = tid / 16 + 16 * i, c = (tid & 15) * 4;
+        const float x[4] = {rf[i].x, rf[i].y, rf[i].z, rf[i].w};
+        bf16_t hi[4], lo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          hi[j] = f2bf(x[j]);
+          lo[j] = f2bf(x[j] - bf2f(hi[j]));
+        }
+        *(uint2*)&As[buf][0][r * LDK + c] =
+            make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+        *(uint2*)&As[buf][NA - 1][r * LDK + c] =
+            make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < A_LD; ++i)
+        *(uint4*)&As[buf][0][(tid / 8 + 32 * i) * LDK + (tid & 7) * 8] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) *(uint4*)&Bs[buf][(tid / 8 + 32 * i) * LDK + bcol] = rb[i];
+  };
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int KT = a.K / BK;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) load_tile(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8_t bfr[FN];
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni)
+        bfr[ni] = *(const bf16x8_t*)&Bs[buf][(b_frag_row<BN, WN, FN, EPI>(wn, ni) + lr) * LDK +
+                                             ks * 32 + lk];
+#pragma unroll
+      for (int h = 0; h < NA; ++h) {
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi) {
+          const bf16x8_t afr =
+              *(const bf16x8_t*)&As[buf][h][(wm * WM + mi * 16 + lr) * LDK + ks * 32 + lk];
+#pragma unroll
+          for (int ni = 0; ni < FN; ++ni)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[ni], acc[mi][ni], 0, 0, 0);
+        }
+      }
+    }
+    if (kt + 1 < KT) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // epilogue: acc[mi][ni][r] = C[row = .. + 4*(lane/16) + r][col = .. + lane%16]
+#pragma unroll
+  for (int mi = 0; mi < FM; ++mi) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + wm * WM + mi * 16 + (lane >> 4) * 4 + r;
+      if (row >= a.M) continue;
+      if constexpr (EPI == EPI_SWIGLU) {
+        bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
+#pragma unroll
+        for (int ni = 0; ni < FN / 2; ++ni) {
+          const int f = nt * (BN / 2) + wn * (WN / 2) + ni * 16 + lr;
+          if (f < a.N) C[f] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+        }
+      } else {
+        float* C = (float*)a.C + (int64_t)row * a.ldc;
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) {
+          const int col = nt * BN + wn * WN + ni * 16 + lr;
+          if (col < a.N) {
+            if constexpr (EPI == EPI_ADD_F32) C[col] += acc[mi][ni][r];
+            else C[col] = acc[mi][ni][r];
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ float32 FMA path
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int MT, int NT) {
+  constexpr int BM = 64, BN = 64, BKF = 16;
+  __shared__ float As[BKF][BM + 4];
+  __shared__ float Bs[BKF][BN + 4];
+  const int mt = blockIdx.x % MT, nt = blockIdx.x / MT;
+  const int m0 = mt * BM;
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int lrow = tid >> 2, lk = (tid & 3) * 4;
+  bool bok;
+  const float* bsrc = b_row<float, BN, EPI>(a, nt, lrow, bok);
+  const float* A = (const float*)a.A;
+  const int gm = m0 + lrow;
+  float acc[4][4] = {};
+  int cols[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    cols[j] = (EPI == EPI_SWIGLU) ? (j < 2 ? tx * 2 + j : BN / 2 + tx * 2 + (j - 2)) : tx * 4 + j;
+  for (int k0 = 0; k0 < a.K; k0 += BKF) {
+    float4 va = gm < a.M ? *(const float4*)(A + (int64_t)gm * a.lda + k0 + lk) : make_float4(0, 0, 0, 0);
+    float4 vb = bok ? *(const float4*)(bsrc + k0 + lk) : make_float4(0, 0, 0, 0);
+    As[lk + 0][lrow] = va.x; As[lk + 1][lrow] = va.y; As[lk + 2][lrow] = va.z; As[lk + 3][lrow] = va.w;
+    Bs[lk + 0][lrow] = vb.x; Bs[lk + 1][lrow] = vb.y; Bs[lk + 2][lrow] = vb.z; Bs[lk + 3][lrow] = vb.w;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < BKF; ++k) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[k][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = Bs[k][cols[j]];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + ty * 4 + i;
+    if (row >= a.M) continue;
+    float* C = (float*)a.C + (int64_t)row * a.ldc;
+    if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int f = nt * (BN / 2) + tx * 2 + j;
+        if (f < a.N) C[f] = silu_f(acc[i][j]) * acc[i][j + 2];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = nt * BN + tx * 4 + j;
+        if (col < a.N) {
+          if constexpr (EPI == EPI_ADD_F32) C[col] += acc[i][j];
+          else C[col] = acc[i][j];
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int EPI, int AMODE>
+hipError_t run_mfma(const GemmArgs& a, hipStream_t st) {
+  const int MT = (a.M + BM - 1) / BM;
+  const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
+  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, EPI, AMODE>), dim3(MT * NT), dim3(256), 0, st, a, MT, NT);
+  return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t run_f32(const GemmArgs& a, hipStream_t st) {
+  const int MT = (a.M + 63) / 64;
+  const int NT = EPI == EPI_SWIGLU ? (a.N + 31) / 32 : (a.N + 63) / 64;
+  hipLaunchKernelGGL((gemm_f32_kernel<EPI>), dim3(MT * NT), dim3(256), 0, st, a, MT, NT);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (amode == A_F32) {
+    switch (epi) {
+      case EPI_STORE_F32: return run_f32<EPI_STORE_F32>(a, st);
+      case EPI_ADD_F32: return run_f32<EPI_ADD_F32>(a, st);
+      default: return run_f32<EPI_SWIGLU>(a, st);
+    }
+  }
+  const bool small = a.M <= 512;
+  if (amode == A_F32SPLIT) {
+    return small ? run_mfma<64, 128, EPI_STORE_F32, A_F32SPLIT>(a, st)
+                 : run_mfma<128, 128, EPI_STORE_F32, A_F32SPLIT>(a, st);
+  }
+  switch (epi) {
+    case EPI_STORE_F32:
+      return small ? run_mfma<64, 128, EPI_STORE_F32, A_BF16>(a, st) : run_mfma<128, 128, EPI_STORE_F32, A_BF16>(a, st);
+    case EPI_ADD_F32:
+      return small ? run_mfma<64, 128, EPI_ADD_F32, A_BF16>(a, st) : run_mfma<128, 128, EPI_ADD_F32, A_BF16>(a, st);
+    default:
+      return small ? run_mfma<64, 128, EPI_SWIGLU, A_BF16>(a, st) : run_mfma<128, 128, EPI_SWIGLU, A_BF16>(a, st);
+  }
+}
+
+}  // namespace dpara

@@ -1,0 +1,98 @@
+// Host-side launchers shared between the DPara translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dpara {
+
+// Per-phase tracing: when enabled (dpara_profile_enable), records a HIP event pair on `st`
+// around the scope.  A no-op otherwise.
+struct Phase {
+  Phase(const char* name, hipStream_t st);
+  ~Phase();
+  Phase(const Phase&) = delete;
+  Phase& operator=(const Phase&) = delete;
+  int slot;
+  hipStream_t st;
+};
+
+// ---------------------------------------------------------------- GEMM
+// C[M, N] (op)= A[M, K] . B[N, K]^T with B given in up to three row segments
+// (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2).
+enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+// A_BF16: A is bf16.  A_F32SPLIT: A is float32 and is applied as hi + lo bf16 parts
+// (two MFMA passes), which keeps ~16 significant bits of A.  A_F32: float32 FMA kernel
+// (the float32 model path; B is then float32 too).
+enum GemmAMode { A_BF16 = 0, A_F32SPLIT = 1, A_F32 = 2 };
+
+struct GemmArgs {
+  const void* A;
+  int64_t lda;
+  const void* B0;
+  const void* B1;
+  const void* B2;
+  int n1, n2;
+  int M, N, K;
+  void* C;
+  int64_t ldc;
+  // EPI_SWIGLU: B0 = gate [N, K], B1 = up [N, K], C = bf16/f32 [M, N] of silu(g) * u,
+  // where N is the FFN width.
+};
+
+hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  int B, R, gamma, n_q, n_kv, hd;
+  const void* Q;    // [B, n_kv, grp*R, hd] (row index g*R + row for query head kvh*grp + g)
+  const void* Kb;   // [B, n_kv, R, hd]     in-block keys
+  const void* Vb;   // [B, n_kv, R, hd]     in-block values
+  const void* Kc;   // context K cache of this layer  [batch_cap, n_kv, cap, hd]
+  const void* Vc;   // context V cache of this layer  [batch_cap, n_kv, hd, cap]
+  int cap;
+  const int* ctx_len;  // [B] device
+  int S, chunk;        // context split into S chunks of `chunk` positions
+  float* Opart;        // [B, n_q, R, S, hd]
+  float* MLpart;       // [B, n_q, R, S, 2]  (running max in log2 units, running sum)
+  void* O;             // [B*R, n_q*hd]
+  int spine_only;      // 1: rows are only the causal spine (no branches)
+};
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- elementwise
+hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V,
+                                const int* spine, const void* embed, const void* mask_emb,
+                                float* X, int* status, hipStream_t st);
+// Y[m] = rmsnorm(X[in_row(m)]) * g, in_row(m) = (m / grp) * in_stride + in_off + m % grp
+hipError_t launch_rmsnorm(int out_dtype, int rows, int H, const float* X, int grp,
+                          int64_t in_stride, int in_off, const float* g, float eps, void* Y,
+                          hipStream_t st);
+hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len,
+                             int pos_off, float2* table, hipStream_t st);
+hipError_t launch_qk_norm_rope(int dtype, int B, int R, int gamma, int n_q, int n_kv, int hd,
+                               int qk_norm, float eps, const float* QKV, const float* qn,
+                               const float* kn, const float2* table, void* Q, void* Kb,
+                               void* Vb, hipStream_t st);
+hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int H,
+                               const void* feats, void* F, hipStream_t st);
+hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd,
+                           int qk_norm, float eps, float base, const float* KV,
+                           const float* kn, const int* n_new, const int* ctx_len, int cap,
+                           void* Kc, void* Vc, int* status, hipStream_t st);
+hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, int* ctx_len,
+                                 int* status, hipStream_t st);
+hipError_t launch_clear_status(int* status, hipStream_t st);
+
+// ---------------------------------------------------------------- verify / head
+hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits,
+                         const int* spine, int* accept_len, int* bonus, int* target_argmax,
+                         uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st);
+hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
+                                const int* accept_len, float* G, float* G_out, int* status,
+                                hipStream_t st);
+hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits,
+                          const void* E, const void* W, const int* bonus, int* drafts,
+                          int* next_spine, float* margins, uint64_t* part, int n_chunks,
+                          int chunk, unsigned* counters, int* status, hipStream_t st);
+
+}  // namespace dpara

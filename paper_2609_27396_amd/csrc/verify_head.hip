@@ -1,0 +1,278 @@
+// Greedy verification, branch gather and the Markov AR head.
+//
+// verify: per (row, vocab chunk) a workgroup reduces its slice to one packed 64-bit
+// (value, lowest index) key; one wave per request then takes each row's argmax g_j
+// (lane j), compares the drafts t_{j+1} with g_j, and a wave ballot of the mismatches
+// gives the accepted length r = index of the first mismatch (gamma if none) and the
+// bonus g_r (Section 2.1; Algorithm 1, Verify).
+//
+// head: y_0 = bonus; step i computes z_i = l_i + W E(y_{i-1}) over the vocabulary in
+// chunks (8 lanes per vocabulary row, E(y_{i-1}) staged in LDS), keeps a per-chunk
+// top-2, and the last workgroup of the step (atomic ticket, no spinning) reduces the
+// chunks to y_i and the top1 - top2 margin (head equation of Section 3.2).
+#include <math.h>
+
+#include "common.h"
+#include "internal.h"
+
+namespace dpara {
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(256) void verify_partial(const T* logits, int V, int chunk, int n_chunks,
+                                                      uint64_t* part) {
+  __shared__ uint64_t red[4];
+  const int rowid = blockIdx.y, c = blockIdx.x;
+  const T* x = logits + (int64_t)rowid * V;
+  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  uint64_t best = 0;
+  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+    const uint64_t k = argmax_key(ld_f(x + v), (uint32_t)v);
+    best = k > best ? k : best;
+  }
+  best = wave_max_u64(best);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t m = red[0];
+    for (int i = 1; i < 4; ++i) m = red[i] > m ? red[i] : m;
+    part[(int64_t)rowid * n_chunks + c] = m;
+  }
+}
+
+__global__ __launch_bounds__(64) void verify_finalize(int gamma, int V, int n_chunks, const uint64_t* part,
+                                                      const int* spine, int* accept_len, int* bonus,
+                                                      int* target_argmax, int* status) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  int g = 0;
+  if (lane <= gamma) {
+    const uint64_t* p = part + ((int64_t)b * (gamma + 1) + lane) * n_chunks;
+    uint64_t best = 0;
+    for (int c = 0; c < n_chunks; ++c) best = p[c] > best ? p[c] : best;
+    g = (int)key_index(best);
+    if (target_argmax) target_argmax[b * (gamma + 1) + lane] = g;
+  }
+  bool mismatch = false;
+  if (lane < gamma) {
+    const int t = spine[b * (gamma + 1) + lane + 1];
+    if (t < 0 || t >= V) raise_status(status, 1);
+    mismatch = (t != g);
+  }
+  const uint64_t mask = __ballot(mismatch);
+  const int r = mask ? (__ffsll((unsigned long long)mask) - 1) : gamma;
+  const int bon = __shfl(g, r, kWave);
+  if (lane == 0) {
+    accept_len[b] = r;
+    bonus[b] = bon;
+  }
+}
+
+__global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const float* reps, const int* accept_len,
+                                                     float* G, float* G_out, int* status) {
+  const int i = blockIdx.x, b = blockIdx.y;
+  int r = accept_len[b];
+  if (r < 0 || r > gamma) {
+    if (threadIdx.x == 0) raise_status(status, 4);
+    r = r < 0 ? 0 : gamma;
+  }
+  const float4* src = (const float4*)(reps + (((int64_t)b * (gamma + 1) + r) * gamma + i) * H);
+  float4* dst = (float4*)(G + ((int64_t)b * gamma + i) * H);
+  float4* dst2 = G_out ? (float4*)(G_out + ((int64_t)b * gamma + i) * H) : nullptr;
+  for (int k = threadIdx.x; k < H / 4; k += 256) {
+    const float4 v = src[k];
+    dst[k] = v;
+    if (dst2) dst2[k] = v;
+  }
+}
+
+__global__ void fill_u32(unsigned* p, int n, unsigned v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Merge (key1, second-best value) pairs.
+__device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1, float ov2) {
+  const float va = k1 ? key_value(k1) : -INFINITY;
+  const float vb = ok1 ? key_value(ok1) : -INFINITY;
+  if (ok1 > k1) {
+    v2 = fmaxf(fmaxf(v2, ov2), va);
+    k1 = ok1;
+  } else {
+    v2 = fmaxf(fmaxf(v2, ov2), vb);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ float dot_row8(const T* w, const float* e, int rank, int j);
+
+// bf16 row: lane j of the 8-lane group loads 16-byte pieces (t*8 + j), t < rank/64.
+template <>
+__device__ __forceinline__ float dot_row8<bf16_t>(const bf16_t* w, const float* e, int rank, int j) {
+  float acc = 0.f;
+  for (int t = 0; t < rank / 64; ++t) {
+    const int k0 = (t * 8 + j) * 8;
+    const uint4 u = *(const uint4*)(w + k0);
+    const uint32_t ws[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc = fmaf(__uint_as_float(ws[q] << 16), e[k0 + 2 * q], acc);
+      acc = fmaf(__uint_as_float(ws[q] & 0xFFFF0000u), e[k0 + 2 * q + 1], acc);
+    }
+  }
+  return acc;
+}
+template <>
+__device__ __forceinline__ float dot_row8<float>(const float* w, const float* e, int rank, int j) {
+  float acc = 0.f;
+  for (int t = 0; t < rank / 32; ++t) {
+    const int k0 = (t * 8 + j) * 4;
+    const float4 u = *(const float4*)(w + k0);
+    acc = fmaf(u.x, e[k0], acc);
+    acc = fmaf(u.y, e[k0 + 1], acc);
+    acc = fmaf(u.z, e[k0 + 2], acc);
+    acc = fmaf(u.w, e[k0 + 3], acc);
+  }
+  return acc;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int rank, const float* logits,
+                                               const T* E, const T* W, const int* bonus, int* drafts,
+                                               int* next_spine, float* margins, uint64_t* part,
+                                               int n_chunks, int chunk, unsigned* counters, int* status) {
+  __shared__ float e[1024];
+  __shared__ uint64_t rk[4];
+  __shared__ float rv[4];
+  __shared__ bool last;
+  const int c = blockIdx.x, b = blockIdx.y;
+  int y_prev = step == 1 ? bonus[b] : drafts[b * gamma + step - 2];
+  if (y_prev < 0 || y_prev >= V) {
+    if (threadIdx.x == 0 && c == 0) raise_status(status, 1);
+    y_prev = 0;
+  }
+  for (int k = threadIdx.x; k < rank; k += 256) e[k] = ld_f(E + (int64_t)y_prev * rank + k);
+  __syncthreads();
+  const float* lrow = logits + ((int64_t)b * gamma + step - 1) * V;
+  const int j = threadIdx.x & 7, grp = threadIdx.x >> 3;
+  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  uint64_t k1 = 0;
+  float v2 = -INFINITY;
+  for (int v = v0 + grp; v < v1; v += 32) {
+    float d = dot_row8<T>(W + (int64_t)v * rank, e, rank, j);
+    d += __shfl_xor(d, 1, kWave);
+    d += __shfl_xor(d, 2, kWave);
+    d += __shfl_xor(d, 4, kWave);
+    if (j == 0) {
+      const float z = lrow[v] + d;
+      top2_merge(k1, v2, argmax_key(z, (uint32_t)v), -INFINITY);
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t ok = __shfl_xor(k1, o, kWave);
+    const float ov = __shfl_xor(v2, o, kWave);
+    top2_merge(k1, v2, ok, ov);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    rk[w] = k1;
+    rv[w] = v2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 4; ++i) top2_merge(rk[0], rv[0], rk[i], rv[i]);
+    uint64_t* pp = part + ((int64_t)b * n_chunks + c) * 2;
+    pp[0] = rk[0];
+    pp[1] = (uint64_t)__float_as_uint(rv[0]);
+    __threadfence();
+    const unsigned ticket = atomicAdd(&counters[b], 1u);
+    last = (ticket == (unsigned)(n_chunks - 1));
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  // last workgroup of this request: reduce all chunks
+  uint64_t K1 = 0;
+  float V2 = -INFINITY;
+  for (int i = threadIdx.x; i < n_chunks; i += 256) {
+    const uint64_t* pp = part + ((int64_t)b * n_chunks + i) * 2;
+    const uint64_t kk = __atomic_load_n(pp, __ATOMIC_RELAXED);
+    const float vv = __uint_as_float((uint32_t)__atomic_load_n(pp + 1, __ATOMIC_RELAXED));
+    top2_merge(K1, V2, kk, vv);
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t ok = __shfl_xor(K1, o, kWave);
+    const float ov = __shfl_xor(V2, o, kWave);
+    top2_merge(K1, V2, ok, ov);
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    rk[w] = K1;
+    rv[w] = V2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 4; ++i) top2_merge(rk[0], rv[0], rk[i], rv[i]);
+    const int y = (int)key_index(rk[0]);
+    drafts[b * gamma + step - 1] = y;
+    next_spine[b * (gamma + 1) + step] = y;
+    if (step == 1) next_spine[b * (gamma + 1)] = bonus[b] < 0 || bonus[b] >= V ? 0 : bonus[b];
+    if (margins) margins[b * gamma + step - 1] = key_value(rk[0]) - rv[0];
+    counters[b] = 0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits, const int* spine,
+                         int* accept_len, int* bonus, int* target_argmax, uint64_t* part, int n_chunks,
+                         int chunk, int* status, hipStream_t st) {
+  Phase ph("verify", st);
+  dim3 grid(n_chunks, B * (gamma + 1));
+  if (logits_dtype == 1)
+    hipLaunchKernelGGL(verify_partial<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)logits, V, chunk, n_chunks,
+                       part);
+  else
+    hipLaunchKernelGGL(verify_partial<float>, grid, dim3(256), 0, st, (const float*)logits, V, chunk, n_chunks,
+                       part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(verify_finalize, dim3(B), dim3(64), 0, st, gamma, V, n_chunks, part, spine, accept_len,
+                     bonus, target_argmax, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, const int* accept_len, float* G,
+                                float* G_out, int* status, hipStream_t st) {
+  Phase ph("gather", st);
+  hipLaunchKernelGGL(gather_branch, dim3(gamma, B), dim3(256), 0, st, gamma, H, reps, accept_len, G, G_out,
+                     status);
+  return hipGetLastError();
+}
+
+hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
+                          const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
+                          uint64_t* part, int n_chunks, int chunk, unsigned* counters, int* status,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(fill_u32, dim3((B + 255) / 256), dim3(256), 0, st, counters, B, 0u);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 grid(n_chunks, B);
+  for (int step = 1; step <= gamma; ++step) {
+    Phase ph("ar_step", st);
+    if (dtype == 1)
+      hipLaunchKernelGGL(ar_step<bf16_t>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const bf16_t*)E,
+                         (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, counters,
+                         status);
+    else
+      hipLaunchKernelGGL(ar_step<float>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const float*)E,
+                         (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, counters,
+                         status);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace dpara

@@ -1,0 +1,114 @@
+"""Host-side checks of the C ABI: exports, workspace sizing and argument validation.
+
+These run without a GPU: every call here fails validation before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_27396_amd import dpara as D
+from paper_2609_27396_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    txt = open(os.path.join(ROOT, "include", "dpara.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:size_t|int|int32_t|const char\s*\*)\s*(dpara_\w+)\s*\(", txt, re.M)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    names = _header_functions()
+    assert len(names) >= 8
+    L = D.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(D.EXPORTS) == set(names)
+    assert D.dpara_version() == 100
+
+
+def test_workspace_bytes():
+    cfg = D.make_config(synth.QWEN3_8B)
+    a = D.dpara_workspace_bytes(cfg, 1, 2112)
+    b = D.dpara_workspace_bytes(cfg, 16, 4160)
+    assert 0 < a < b
+    assert D.dpara_workspace_bytes(cfg, 1, 100) == 0        # ctx_cap not a multiple of 64
+    assert D.dpara_workspace_bytes(cfg, 0, 2112) == 0
+    bad = D.make_config(synth.shrink(synth.QWEN3_8B, head_dim=96))
+    assert D.dpara_workspace_bytes(bad, 1, 2112) == 0
+    bad = D.make_config(synth.shrink(synth.QWEN3_8B, gamma=64))
+    assert D.dpara_workspace_bytes(bad, 1, 2112) == 0
+    bad = D.make_config(synth.shrink(synth.QWEN3_8B, n_kv_heads=7))
+    assert D.dpara_workspace_bytes(bad, 1, 2112) == 0
+
+
+FAKE = 1 << 20  # a 16-byte aligned non-null address; never dereferenced (validation fails first)
+
+
+def _fake_weights(shape):
+    layers = (D.DparaLayerWeights * shape.n_layers)()
+    for l in range(shape.n_layers):
+        for f, _ in D.DparaLayerWeights._fields_:
+            setattr(layers[l], f, FAKE)
+    w = D.DparaWeights(embed=FAKE, mask_emb=FAKE, final_norm=FAKE, ar_E=FAKE, ar_W=FAKE,
+                       layers=ctypes.cast(layers, ctypes.POINTER(D.DparaLayerWeights)))
+    return w, layers
+
+
+def _rc(fn, *args):
+    return getattr(D.lib(), fn)(*args)
+
+
+def test_validation_errors_without_gpu():
+    s = synth.shrink(synth.QWEN3_8B, n_layers=2)
+    cfg = D.make_config(s)
+    w, _keep = _fake_weights(s)
+    ctx = D.DparaCtx(k=FAKE, v=FAKE, ctx_len=FAKE, batch_cap=2, ctx_cap=2112)
+    need = D.dpara_workspace_bytes(cfg, 2, 2112)
+    R = ctypes.byref
+    # workspace too small
+    assert _rc("dpara_backbone_all_boundaries", R(cfg), R(w), R(ctx), 2, FAKE, FAKE, FAKE, need - 1, None) \
+        == D.DPARA_E_WORKSPACE
+    assert "needs" in D.dpara_last_error()
+    # batch above the cache's batch capacity
+    assert _rc("dpara_backbone_all_boundaries", R(cfg), R(w), R(ctx), 3, FAKE, FAKE, FAKE, need, None) \
+        == D.DPARA_E_CAPACITY
+    # null / misaligned pointers
+    assert _rc("dpara_backbone_all_boundaries", R(cfg), R(w), R(ctx), 2, None, FAKE, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    assert _rc("dpara_backbone_all_boundaries", R(cfg), R(w), R(ctx), 2, FAKE, FAKE + 4, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    w.mask_emb = None
+    assert _rc("dpara_backbone_all_boundaries", R(cfg), R(w), R(ctx), 2, FAKE, FAKE, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    assert "mask_emb" in D.dpara_last_error()
+    # bad configuration
+    bad = D.make_config(synth.shrink(s, gamma=0))
+    assert _rc("dpara_backbone_all_boundaries", R(bad), R(w), R(ctx), 2, FAKE, FAKE, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    bad = D.make_config(s)
+    bad.dtype = 7
+    assert _rc("dpara_verify_greedy", R(bad), 1, FAKE, 0, FAKE, FAKE, FAKE, None, FAKE, need, None) \
+        == D.DPARA_E_UNSUPPORTED
+    # verify: unsupported logits dtype, null outputs
+    assert _rc("dpara_verify_greedy", R(cfg), 1, FAKE, 5, FAKE, FAKE, FAKE, None, FAKE, need, None) \
+        == D.DPARA_E_UNSUPPORTED
+    assert _rc("dpara_verify_greedy", R(cfg), 1, FAKE, 1, FAKE, None, FAKE, None, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    # append: n_max < 1, ctx_cap not a multiple of 64
+    assert _rc("dpara_ctx_append", R(cfg), R(w), R(ctx), 2, FAKE, FAKE, 0, FAKE, need, None) == D.DPARA_E_INVALID
+    ctx_bad = D.DparaCtx(k=FAKE, v=FAKE, ctx_len=FAKE, batch_cap=2, ctx_cap=100)
+    assert _rc("dpara_ctx_append", R(cfg), R(w), R(ctx_bad), 2, FAKE, FAKE, 4, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    # head: null drafts
+    assert _rc("dpara_select_and_head", R(cfg), R(w), 1, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, need,
+               None) == D.DPARA_E_INVALID
+
+
+def test_binding_raises_loudly_on_error():
+    s = synth.TINY
+    cfg = D.make_config(s)
+    with pytest.raises(D.DparaError) as e:
+        D.dpara_verify_greedy(cfg, 1, FAKE, 9, FAKE, FAKE, FAKE, None, FAKE, 1 << 20, None)
+    assert e.value.code == D.DPARA_E_UNSUPPORTED

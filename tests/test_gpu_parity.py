@@ -1,0 +1,226 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the same seeded inputs.
+
+Bars: accepted lengths, bonus, target argmax and gathered rows bit-exact;
+representations within 1e-5 (float32 model) or 2e-2 (bf16 model) max-abs; draft
+ids exact wherever the oracle's top1 - top2 margin of z_i exceeds 1e-2, checked
+teacher-forced (the oracle's step i is fed the GPU's y_{i-1}).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import dpara_oracle as O  # noqa: E402
+from paper_2609_27396_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+MARGIN = 1e-2
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _harness():
+    from paper_2609_27396_amd.harness import DeviceRound
+    return DeviceRound
+
+
+def check_verify(ri, dr):
+    acc, bon, tg = dr.accept.cpu().numpy(), dr.bonus.cpu().numpy(), dr.targmax.cpu().numpy()
+    for b in range(dr.B):
+        r, bonus, g = O.verify_greedy(ri.target_logits[b], ri.spine[b])
+        assert acc[b] == r and bon[b] == bonus, (b, acc[b], r, bon[b], bonus)
+        np.testing.assert_array_equal(tg[b], g)
+        assert r == ri.accept_planted[b] and bonus == ri.bonus_planted[b]
+
+
+def check_head(shape, w, dr, mode, b):
+    """Teacher-forced check of the AR head on the GPU's own gathered rows."""
+    gathered = dr.gathered[b].cpu().numpy()
+    r = int(dr.accept[b].item())
+    np.testing.assert_array_equal(gathered, dr.reps[b, r].cpu().numpy())   # bit-exact gather
+    drafts = dr.drafts[b].cpu().numpy()
+    nxt = dr.next_spine[b].cpu().numpy()
+    bonus = int(dr.bonus[b].item())
+    assert nxt[0] == bonus
+    np.testing.assert_array_equal(nxt[1:], drafts)
+    ell = O.base_logits(w, gathered, mode)
+    y_prev, skipped = bonus, 0
+    gm = dr.margins[b].cpu().numpy()
+    for i in range(shape.gamma):
+        y, m, _ = O.head_step(w, ell[i], y_prev, mode)
+        if m > MARGIN:
+            assert drafts[i] == y, (b, i, drafts[i], y, m)
+            assert abs(gm[i] - m) < 1e-3 + 1e-3 * abs(m)
+        else:
+            skipped += 1
+        y_prev = int(drafts[i])
+    return skipped
+
+
+def run_full(wl: synth.Workload, weights, ri, ctx_cap=None):
+    DeviceRound = _harness()
+    dr = DeviceRound(wl.shape, weights, ri, ctx_cap=ctx_cap)
+    dr.backbone()
+    dr.verify()
+    dr.head()
+    torch.cuda.synchronize()
+    assert dr.status() == 0
+    return dr
+
+
+# ----------------------------------------------------------------------------- tiny fp32 config
+def test_tiny_round_parity():
+    wl = synth.WORKLOADS["tiny"]
+    _say("case tiny fp32 round", wl.description)
+    w = synth.make_weights(wl.shape, seed=wl.seed_w, gain_jitter=0.1)
+    ri = synth.make_round(wl)
+    dr = run_full(wl, w, ri)
+    check_verify(ri, dr)
+    for b in range(wl.batch):
+        ref = O.backbone_all_boundaries(wl.shape, w, ri.ctx_feats[b], ri.spine[b], "f32")["reps"]
+        err = np.abs(dr.reps[b].cpu().numpy() - ref).max()
+        _say("tiny max|reps-oracle|", err)
+        assert err <= TOL["f32"]
+        check_head(wl.shape, w, dr, "f32", b)
+
+
+# ----------------------------------------------------------------------------- small bf16 shapes
+SMALL_CASES = {
+    # several GEMM tiles with ragged M/N tails, hd 128, qk-norm, ragged contexts incl. an empty one
+    "h256_hd128_g5": (synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=576,
+                                         vocab=4000, gamma=5, ar_rank=64, qk_norm=True, dtype="bf16"),
+                      [0, 77, 300]),
+    # head_dim 64, no qk-norm, GQA 4:1
+    "h512_hd64_g3": (synth.DrafterShape(n_layers=1, hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=64, ffn=640,
+                                        vocab=1000, gamma=3, ar_rank=128, qk_norm=False, dtype="bf16"),
+                     [64, 129]),
+    # float32 model with several tiles, hd 128
+    "f32_h256_g7": (synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=1, head_dim=128, ffn=320,
+                                       vocab=3001, gamma=7, ar_rank=64, qk_norm=True, dtype="f32"),
+                    [33, 150]),
+}
+
+
+@pytest.mark.parametrize("case", sorted(SMALL_CASES))
+def test_small_parity(case):
+    shape, ctx = SMALL_CASES[case]
+    _say("case", case)
+    wl = synth.Workload(case, shape, batch=len(ctx), ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=7,
+                        logits_dtype="bf16" if shape.dtype == "bf16" else "f32")
+    w = synth.make_weights(shape, seed=3, gain_jitter=0.1, ar_e_std=1.0)
+    ri = synth.make_round(wl, ctx_lens=ctx)
+    dr = run_full(wl, w, ri)
+    check_verify(ri, dr)
+    mode = shape.dtype
+    worst, skipped = 0.0, 0
+    for b in range(wl.batch):
+        ref = O.backbone_all_boundaries(shape, w, ri.ctx_feats[b], ri.spine[b], mode)["reps"]
+        worst = max(worst, np.abs(dr.reps[b].cpu().numpy() - ref).max())
+        skipped += check_head(shape, w, dr, mode, b)
+    _say(case, "max|reps-oracle|", worst, "head steps skipped (margin<=1e-2):", skipped)
+    assert worst <= TOL[mode]
+
+
+def test_append_equivalence_and_determinism():
+    shape, _ = SMALL_CASES["h256_hd128_g5"]
+    wl = synth.Workload("app", shape, batch=2, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=9)
+    w = synth.make_weights(shape, seed=4)
+    ri = synth.make_round(wl, ctx_lens=[120, 61])
+    DeviceRound = _harness()
+    a = DeviceRound(shape, w, ri, ctx_cap=256)
+    # b: prefill all but the last k rows, then append them
+    k = np.array([6, 3], np.int32)
+    ri_short = synth.RoundInputs(ctx_lens=ri.ctx_lens - k, ctx_feats=[f[:-kk] for f, kk in zip(ri.ctx_feats, k)],
+                                 spine=ri.spine, accept_planted=ri.accept_planted, bonus_planted=ri.bonus_planted,
+                                 target_logits=ri.target_logits, new_feats=ri.new_feats)
+    bdr = DeviceRound(shape, w, ri_short, ctx_cap=256, drafter=a.d)
+    tail = np.zeros((2, 6, shape.hidden), np.float32)
+    for i, (f, kk) in enumerate(zip(ri.ctx_feats, k)):
+        tail[i, :kk] = f[-kk:]
+    bdr.append(torch.from_numpy(k).cuda(), torch.from_numpy(tail).cuda().to(torch.bfloat16))
+    torch.cuda.synchronize()
+    assert torch.equal(a.ctx.ctx_len, bdr.ctx.ctx_len)
+    for b in range(2):
+        n = int(ri.ctx_lens[b])
+        assert torch.equal(a.ctx.k[:, b, :, :n], bdr.ctx.k[:, b, :, :n])
+        assert torch.equal(a.ctx.v[:, b, :, :, :n], bdr.ctx.v[:, b, :, :, :n])
+    a.backbone()
+    r1 = a.reps.clone()
+    a.backbone()
+    bdr.backbone()
+    torch.cuda.synchronize()
+    assert torch.equal(r1, a.reps)          # determinism
+    assert torch.equal(a.reps, bdr.reps)    # same cache => same result
+    assert a.status() == 0
+
+
+def test_device_status_flags_and_clamping():
+    shape, _ = SMALL_CASES["h512_hd64_g3"]
+    wl = synth.Workload("st", shape, batch=2, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=11)
+    w = synth.make_weights(shape, seed=5)
+    ri = synth.make_round(wl, ctx_lens=[10, 20])
+    DeviceRound = _harness()
+    dr = DeviceRound(shape, w, ri, ctx_cap=64)
+    from paper_2609_27396_amd import dpara as D
+    dr.spine[0, 1] = shape.vocab + 5           # out-of-range draft id: clamped, flagged
+    dr.backbone()
+    dr.verify()
+    assert dr.status() & D.STATUS_TOKEN_RANGE
+    assert int(dr.accept[0]) == 0              # an invalid draft never matches
+    D.dpara_clear_status(dr.ws.ptr, D._stream(None))
+    assert dr.status() == 0
+    dr.accept[1] = shape.gamma + 3             # verdict out of range: clamped, flagged
+    dr.head()
+    assert dr.status() & D.STATUS_VERDICT_RANGE
+    D.dpara_clear_status(dr.ws.ptr, D._stream(None))
+    n_new = torch.tensor([60, 2], dtype=torch.int32, device="cuda")  # 10 + 60 > 64
+    feats = torch.zeros((2, 60, shape.hidden), dtype=torch.bfloat16, device="cuda")
+    dr.append(n_new, feats)
+    assert dr.status() & D.STATUS_CTX_FULL
+    assert dr.ctx.ctx_len.cpu().tolist() == [64, 22]
+    D.dpara_clear_status(dr.ws.ptr, D._stream(None))
+    dr.append(torch.tensor([-1, 99], dtype=torch.int32, device="cuda"), feats)
+    assert dr.status() & D.STATUS_COUNT_RANGE
+    assert dr.ctx.ctx_len.cpu().tolist() == [64, 64]
+
+
+# ----------------------------------------------------------------------------- full-size configs
+def _full_size(name, samples):
+    wl = synth.WORKLOADS[name]
+    _say("case", name, wl.description)
+    w = synth.make_weights(wl.shape, seed=wl.seed_w)
+    ri = synth.make_round(wl)
+    dr = run_full(wl, w, ri)
+    check_verify(ri, dr)
+    worst, skipped = 0.0, 0
+    for b, branches in samples:
+        for r in branches:
+            one = O.backbone_single_boundary(wl.shape, w, ri.ctx_feats[b], ri.spine[b], r, "bf16")
+            err = np.abs(dr.reps[b, r].cpu().numpy() - one["reps"]).max()
+            _say(f"{name} request {b} (ctx {ri.ctx_lens[b]}) branch {r}: max|reps-oracle| = {err:.3e}")
+            worst = max(worst, err)
+        skipped += check_head(wl.shape, w, dr, "bf16", b)
+    _say(name, "worst", worst, "head steps skipped:", skipped)
+    assert worst <= TOL["bf16"]
+    return dr, ri
+
+
+def test_full_size_qwen3_8b_b1():
+    wl = synth.WORKLOADS["qwen3_8b_b1"]
+    ri = synth.make_round(wl)
+    r = int(ri.accept_planted[0])
+    _full_size("qwen3_8b_b1", [(0, sorted({0, r, wl.shape.gamma}))])
+
+
+def test_full_size_qwen3_8b_b16():
+    wl = synth.WORKLOADS["qwen3_8b_b16"]
+    ri = synth.make_round(wl)
+    samples = [(b, [int(ri.accept_planted[b])]) for b in (0, 7, 15)]
+    _full_size("qwen3_8b_b16", samples)
