@@ -6,7 +6,10 @@
 // one workgroup per (request, KV head, 64 query rows, context chunk) stages the chunk's
 // K (keys x head_dim) and V^T (head_dim x keys, the cache stores V transposed) in LDS
 // and computes S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_16x16x32_bf16, keeping an
-// online softmax in log2 units.  Each chunk emits an unnormalised partial (O, m, l).
+// online softmax in log2 units.  P enters the PV product as a bf16 hi + lo pair (two
+// MFMAs), so the probabilities keep ~16 significant bits: a single bf16 rounding of P
+// moves the result by about one bf16 ulp of the hidden state, which is as large as the
+// whole error budget.  Each chunk emits an unnormalised partial (O, m, l).
 //
 // The merge kernel (one wave per row and query head) folds the context partials and
 // then walks the row's in-block keys under the tree mask -- spine t_j sees t_0..t_j,
@@ -114,7 +117,7 @@ __global__ __launch_bounds__(256) void attn_ctx_mfma(AttnArgs a) {
     const float m_new = fmaxf(m_run, mx);  // finite: key kb0 < k_end is in this block
     const float alpha = exp2f(m_run - m_new);
     float psum = 0.f;
-    bf16_t pb[4][4];
+    bf16_t pb[4][4], pl[4][4];  // p = hi + lo, both bf16 (16 significant bits of p)
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -122,6 +125,7 @@ __global__ __launch_bounds__(256) void attn_ctx_mfma(AttnArgs a) {
         const float p = exp2f(s[kb][r] - m_new);
         psum += p;
         pb[kb][r] = f2bf(p);
+        pl[kb][r] = f2bf(p - bf2f(pb[kb][r]));
       }
     l_run = l_run * alpha + psum;
     m_run = m_new;
@@ -131,13 +135,16 @@ __global__ __launch_bounds__(256) void attn_ctx_mfma(AttnArgs a) {
     // O^T += V^T P^T over 64 keys = 2 k-steps of 32.  Lane (g4) slot j of k-step t holds
     // key t*32 + g4*4 + j (j < 4) or t*32 + 16 + g4*4 + (j-4): the same key set is used
     // for the V^T operand, so the contraction pairs matching keys.
+    // P enters as hi + lo so the product keeps ~16 bits of p (V is exact in bf16).
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      bf16x8_t pf;
+      bf16x8_t pf, pfl;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         pf[j] = __builtin_bit_cast(__bf16, pb[2 * t][j]);
         pf[j + 4] = __builtin_bit_cast(__bf16, pb[2 * t + 1][j]);
+        pfl[j] = __builtin_bit_cast(__bf16, pl[2 * t][j]);
+        pfl[j + 4] = __builtin_bit_cast(__bf16, pl[2 * t + 1][j]);
       }
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb) {
@@ -147,6 +154,7 @@ __global__ __launch_bounds__(256) void attn_ctx_mfma(AttnArgs a) {
         const uint4 packed = make_uint4(lo.x, lo.y, hi.x, hi.y);
         const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, packed);
         o[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[hb], 0, 0, 0);
+        o[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl, o[hb], 0, 0, 0);
       }
     }
   }
