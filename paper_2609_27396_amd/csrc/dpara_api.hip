@@ -162,7 +162,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap) {
   p.vpart = take((size_t)B * (c->gamma + 1) * p.v_chunks * 8);
   p.G = take((size_t)B * c->gamma * H * 4);
   p.logits = take((size_t)B * c->gamma * c->vocab * 4);
-  p.hpart = take((size_t)B * p.h_chunks * 16);
+  p.hpart = take((size_t)2 * B * p.h_chunks * 16);  // two step-parity slots
   p.counters = take((size_t)B * 4);
   p.F = take((size_t)B * p.CH * H * p.esz);
   p.KV32 = take((size_t)B * p.CH * 2 * nkv * hd * 4);
@@ -305,8 +305,9 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
   int* status = at<int>(ws, 0);
   const size_t layer_elems = (size_t)ctx->batch_cap * nkv * ctx->ctx_cap * hd;
   const size_t esz = p.esz;
-  for (int c0 = 0; c0 < n_max; c0 += p.CH) {
-    HIP_TRY(launch_gather_feats(dt, batch, p.CH, c0, n_max, H, feats, at<void>(ws, p.F), st), "gather_feats");
+  const int CH = n_max < p.CH ? n_max : p.CH;  // rows per request per chunk
+  for (int c0 = 0; c0 < n_max; c0 += CH) {
+    HIP_TRY(launch_gather_feats(dt, batch, CH, c0, n_max, H, feats, at<void>(ws, p.F), st), "gather_feats");
     for (int l = 0; l < cfg->n_layers; ++l) {
       GemmArgs g{};
       g.A = at<void>(ws, p.F);
@@ -316,7 +317,7 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
       g.B2 = w->layers[l].wv;
       g.n1 = nkv * hd;
       g.n2 = 2 * nkv * hd;
-      g.M = batch * p.CH;
+      g.M = batch * CH;
       g.N = 2 * nkv * hd;
       g.K = H;
       g.C = at<void>(ws, p.KV32);
@@ -328,7 +329,7 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
       char* kc = (char*)ctx->k + l * layer_elems * esz;
       char* vc = (char*)ctx->v + l * layer_elems * esz;
       Phase ph("append_store", st);
-      HIP_TRY(launch_kv_store(dt, batch, p.CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps, cfg->rope_base,
+      HIP_TRY(launch_kv_store(dt, batch, CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps, cfg->rope_base,
                               at<float>(ws, p.KV32), w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
                               vc, status, st),
               "kv_store");
@@ -537,7 +538,7 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   }
   HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
-                         at<unsigned>(ws, p.counters), status, st),
+                         status, st),
           "ar head");
   return DPARA_OK;
 }

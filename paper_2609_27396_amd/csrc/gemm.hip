@@ -1,9 +1,10 @@
 // Dense projections of the drafter: C[M, N] (op)= A[M, K] . B[N, K]^T.
 //
-// bf16 path: LDS-tiled v_mfma_f32_16x16x32_bf16 kernel, 256 threads (2 x 2 waves),
-// BK = 64, double-buffered LDS with register prefetch of the next K tile, fp32
-// accumulation, fused epilogues (store fp32, add into the fp32 residual stream,
-// SwiGLU -> bf16).  The tile order is XCD-aware: the M tiles that share one weight
+// bf16 path: v_mfma_f32_16x16x32_bf16 kernels with fp32 accumulation and fused
+// epilogues (store fp32, add into the fp32 residual stream, SwiGLU -> bf16).  The
+// projections use a multi-stage direct-to-LDS pipeline (gemm_pipe_kernel); the LM head,
+// whose fp32 A operand is split into bf16 hi + lo on the way into LDS, uses a
+// register-staged double-buffered kernel (gemm_mfma_kernel).  The tile order is XCD-aware: the M tiles that share one weight
 // tile run on the same XCD back to back, so a weight tile is fetched from HBM once
 // and served to the others from that XCD's L2.
 // float32 path: a plain LDS-tiled FMA kernel for the float32 model configuration.
@@ -57,6 +58,145 @@ __device__ __forceinline__ int b_frag_row(int wn, int ni) {
     return ni < FN / 2 ? wn * (WN / 2) + ni * 16 : BN / 2 + wn * (WN / 2) + (ni - FN / 2) * 16;
   }
   return wn * WN + ni * 16;
+}
+
+// ------------------------------------------------------------------ pipelined bf16 path
+// Tiles stream through a ring of STAGES LDS buffers filled by direct global->LDS DMA
+// (global_load_lds_dwordx4: lane i's 16 bytes land at M0 + 16*i, so one instruction moves
+// 1 KB = 1024/BKB rows of a tile).  A row's 16-byte chunk c is stored in slot
+// c ^ swizzle(row) so that the MFMA fragment reads (16 rows, same chunk) spread over the LDS
+// banks.  Each wave waits only for its own DMA of the stage it is about to read (vmcnt
+// counts outstanding DMA instructions), then one s_barrier makes every wave's part of that
+// stage visible; the refill of the ring slot freed by the previous iteration is issued
+// right after the barrier, so STAGES-1 stages are in flight while one is consumed.
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14];
+  // expcnt and lgkmcnt are left at their maxima (no wait on them).
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | (((N >> 4) & 3) << 14));
+}
+
+template <int CH>
+__device__ __forceinline__ int swz(int r, int c) {
+  if (CH == 8) return c ^ (r & 7);
+  return c ^ ((r >> 1) & 3);
+}
+
+template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI>
+__global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, int MT, int NT) {
+  constexpr int NW = WMW * WNW;
+  constexpr int CH = BKB / 16;      // 16-byte chunks per tile row per stage
+  constexpr int RPI = 1024 / BKB;   // tile rows per DMA instruction
+  constexpr int KB = BKB / 2;       // bf16 elements per tile row per stage
+  constexpr int WM = BM / WMW, WN = BN / WNW;
+  constexpr int FM = WM / 16, FN = WN / 16;
+  constexpr int A_INS = BM / RPI / NW, B_INS = BN / RPI / NW;
+  static_assert(A_INS * RPI * NW == BM && B_INS * RPI * NW == BN, "tile rows must split evenly over waves");
+  static_assert(KB % 32 == 0, "stage depth must be a multiple of the MFMA k");
+  constexpr int STAGE_BYTES = (BM + BN) * BKB;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+  int mt, nt;
+  tile_of(blockIdx.x, MT, NT, mt, nt);
+  const int m0 = mt * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WNW, wn = wave % WNW;
+
+  // Per-lane DMA sources.  Rows past M or N are clamped to the last valid row: their
+  // products land in accumulator rows/columns that the epilogue never stores.
+  const bf16_t* asrc[A_INS];
+  const bf16_t* bsrc[B_INS];
+  const int lrow = lane / CH, lslot = lane % CH;
+#pragma unroll
+  for (int j = 0; j < A_INS; ++j) {
+    const int r = (wave + NW * j) * RPI + lrow;
+    const int gm = min(m0 + r, a.M - 1);
+    asrc[j] = (const bf16_t*)a.A + (int64_t)gm * a.lda + swz<CH>(r, lslot) * 8;
+  }
+#pragma unroll
+  for (int j = 0; j < B_INS; ++j) {
+    const int r = (wave + NW * j) * RPI + lrow;
+    bool ok;
+    bsrc[j] = b_row<bf16_t, BN, EPI>(a, nt, r, ok) + swz<CH>(r, lslot) * 8;
+  }
+  auto issue = [&](int kt, int stage) {
+    unsigned char* sb = smem + stage * STAGE_BYTES;
+    const int k0 = kt * KB;
+#pragma unroll
+    for (int j = 0; j < A_INS; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + k0), (lds_void_t*)(sb + (wave + NW * j) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < B_INS; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(bsrc[j] + k0),
+                                       (lds_void_t*)(sb + BM * BKB + (wave + NW * j) * 1024), 16, 0, 0);
+  };
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int KT = a.K / KB;
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < KT) issue(st, st);
+  const int lr = lane & 15, lc = lane >> 4;
+  for (int kt = 0; kt < KT; ++kt) {
+    if (kt + STAGES - 2 < KT) wait_vmcnt<(STAGES - 2) * (A_INS + B_INS)>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    const unsigned char* sa = smem + (kt % STAGES) * STAGE_BYTES;
+    const unsigned char* sb = sa + BM * BKB;
+#pragma unroll
+    for (int ks = 0; ks < KB / 32; ++ks) {
+      const int c = ks * 4 + lc;
+      bf16x8_t bfr[FN];
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int r = b_frag_row<BN, WN, FN, EPI>(wn, ni) + lr;
+        bfr[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
+      }
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi) {
+        const int r = wm * WM + mi * 16 + lr;
+        const bf16x8_t afr = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[ni], acc[mi][ni], 0, 0, 0);
+      }
+    }
+  }
+
+#pragma unroll
+  for (int mi = 0; mi < FM; ++mi) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + wm * WM + mi * 16 + (lane >> 4) * 4 + r;
+      if (row >= a.M) continue;
+      if constexpr (EPI == EPI_SWIGLU) {
+        bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
+#pragma unroll
+        for (int ni = 0; ni < FN / 2; ++ni) {
+          const int f = nt * (BN / 2) + wn * (WN / 2) + ni * 16 + lr;
+          if (f < a.N) C[f] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+        }
+      } else {
+        float* C = (float*)a.C + (int64_t)row * a.ldc;
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) {
+          const int col = nt * BN + wn * WN + ni * 16 + lr;
+          if (col < a.N) {
+            if constexpr (EPI == EPI_ADD_F32) C[col] += acc[mi][ni][r];
+            else C[col] = acc[mi][ni][r];
+          }
+        }
+      }
+    }
+  }
 }
 
 template <int BM, int BN, int EPI, int AMODE>
@@ -281,6 +421,32 @@ hipError_t run_f32(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI>
+hipError_t run_pipe(const GemmArgs& a, hipStream_t st) {
+  const int MT = (a.M + BM - 1) / BM;
+  const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
+  constexpr int lds = STAGES * (BM + BN) * BKB;
+  auto kern = gemm_pipe_kernel<BM, BN, WMW, WNW, STAGES, BKB, EPI>;
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(64 * WMW * WNW), lds, st, a, MT, NT);
+  return hipGetLastError();
+}
+
+// Tile choice for the bf16 projections (measured on MI355X, Qwen3-8B-sized N/K):
+//  M <= 512 : weight streaming; 32x128 tiles, 4-deep ring (QKV, O, down), and a full-M
+//             320x128 tile with 8 waves for the SwiGLU GEMM when M <= 320;
+//  M <= 1024: 64x128 tiles, 3-deep ring;
+//  larger   : 256x256 tiles, 8 waves (128x64 per wave), 2-deep ring of 64-wide K steps.
+template <int EPI>
+hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
+  if (a.M > 1024) return run_pipe<256, 256, 2, 4, 2, 128, EPI>(a, st);
+  if (a.M > 512) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
+  if (EPI == EPI_SWIGLU && a.M > 64 && a.M <= 320) return run_pipe<320, 128, 4, 2, 2, 128, EPI>(a, st);
+  return run_pipe<32, 128, 1, 4, 4, 128, EPI>(a, st);
+}
+
 }  // namespace
 
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
@@ -298,12 +464,9 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
                  : run_mfma<128, 128, EPI_STORE_F32, A_F32SPLIT>(a, st);
   }
   switch (epi) {
-    case EPI_STORE_F32:
-      return small ? run_mfma<64, 128, EPI_STORE_F32, A_BF16>(a, st) : run_mfma<128, 128, EPI_STORE_F32, A_BF16>(a, st);
-    case EPI_ADD_F32:
-      return small ? run_mfma<64, 128, EPI_ADD_F32, A_BF16>(a, st) : run_mfma<128, 128, EPI_ADD_F32, A_BF16>(a, st);
-    default:
-      return small ? run_mfma<64, 128, EPI_SWIGLU, A_BF16>(a, st) : run_mfma<128, 128, EPI_SWIGLU, A_BF16>(a, st);
+    case EPI_STORE_F32: return run_bf16<EPI_STORE_F32>(a, st);
+    case EPI_ADD_F32: return run_bf16<EPI_ADD_F32>(a, st);
+    default: return run_bf16<EPI_SWIGLU>(a, st);
   }
 }
 

@@ -93,6 +93,6 @@ hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits,
                           const void* E, const void* W, const int* bonus, int* drafts,
                           int* next_spine, float* margins, uint64_t* part, int n_chunks,
-                          int chunk, unsigned* counters, int* status, hipStream_t st);
+                          int chunk, int* status, hipStream_t st);
 
 }  // namespace dpara

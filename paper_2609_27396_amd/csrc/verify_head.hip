@@ -7,9 +7,9 @@
 // bonus g_r (Section 2.1; Algorithm 1, Verify).
 //
 // head: y_0 = bonus; step i computes z_i = l_i + W E(y_{i-1}) over the vocabulary in
-// chunks (8 lanes per vocabulary row, E(y_{i-1}) staged in LDS), keeps a per-chunk
-// top-2, and the last workgroup of the step (atomic ticket, no spinning) reduces the
-// chunks to y_i and the top1 - top2 margin (head equation of Section 3.2).
+// chunks (8 lanes per vocabulary row, E(y_{i-1}) staged in LDS) and keeps a per-chunk
+// top-2; the next step's workgroups reduce those partials to y_i and the top1 - top2
+// margin before starting (head equation of Section 3.2).
 #include <math.h>
 
 #include "common.h"
@@ -85,10 +85,6 @@ __global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const flo
   }
 }
 
-__global__ void fill_u32(unsigned* p, int n, unsigned v) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = v;
-}
 
 // Merge (key1, second-best value) pairs.
 __device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1, float ov2) {
@@ -135,21 +131,66 @@ __device__ __forceinline__ float dot_row8<float>(const float* w, const float* e,
   return acc;
 }
 
+// Reduce the per-chunk (key1, second value) partials of one step to (y, margin).  Every
+// workgroup of the next step does this redundantly (a few KB from L2) instead of a
+// grid-wide handoff, so no workgroup waits on another and no device-scope fence is needed.
+__device__ __forceinline__ void reduce_step(const uint64_t* pp, int n_chunks, uint64_t* rk, float* rv,
+                                            int* y_out, float* m_out) {
+  uint64_t K1 = 0;
+  float V2 = -INFINITY;
+  for (int i = threadIdx.x; i < n_chunks; i += 256) top2_merge(K1, V2, pp[2 * i], __uint_as_float((uint32_t)pp[2 * i + 1]));
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t ok = __shfl_xor(K1, o, kWave);
+    const float ov = __shfl_xor(V2, o, kWave);
+    top2_merge(K1, V2, ok, ov);
+  }
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    rk[w] = K1;
+    rv[w] = V2;
+  }
+  __syncthreads();
+  uint64_t k = rk[0];
+  float v = rv[0];
+  for (int i = 1; i < 4; ++i) top2_merge(k, v, rk[i], rv[i]);
+  *y_out = (int)key_index(k);
+  *m_out = key_value(k) - v;
+}
+
+// Step `step` of the AR head (1 <= step <= gamma): y_{step-1} from the previous step's
+// partials (or the bonus), then this chunk's top-2 of z = l_step + W E(y_{step-1}).
+// step == gamma + 1 only reduces the last step.  Partials alternate between two slots by
+// step parity: part[slot][b][chunk][2].
 template <typename T>
 __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int rank, const float* logits,
                                                const T* E, const T* W, const int* bonus, int* drafts,
                                                int* next_spine, float* margins, uint64_t* part,
-                                               int n_chunks, int chunk, unsigned* counters, int* status) {
+                                               int n_chunks, int chunk, int B, int* status) {
   __shared__ float e[1024];
   __shared__ uint64_t rk[4];
   __shared__ float rv[4];
-  __shared__ bool last;
   const int c = blockIdx.x, b = blockIdx.y;
-  int y_prev = step == 1 ? bonus[b] : drafts[b * gamma + step - 2];
-  if (y_prev < 0 || y_prev >= V) {
-    if (threadIdx.x == 0 && c == 0) raise_status(status, 1);
-    y_prev = 0;
+  int y_prev;
+  if (step == 1) {
+    y_prev = bonus[b];
+    if (y_prev < 0 || y_prev >= V) {
+      if (threadIdx.x == 0 && c == 0) raise_status(status, 1);
+      y_prev = 0;
+    }
+    if (threadIdx.x == 0 && c == 0) next_spine[b * (gamma + 1)] = y_prev;
+  } else {
+    const uint64_t* pp = part + ((int64_t)((step - 1) & 1) * B + b) * n_chunks * 2;
+    float m;
+    reduce_step(pp, n_chunks, rk, rv, &y_prev, &m);
+    if (threadIdx.x == 0 && c == 0) {
+      drafts[b * gamma + step - 2] = y_prev;
+      next_spine[b * (gamma + 1) + step - 1] = y_prev;
+      if (margins) margins[b * gamma + step - 2] = m;
+    }
   }
+  if (step > gamma) return;
   for (int k = threadIdx.x; k < rank; k += 256) e[k] = ld_f(E + (int64_t)y_prev * rank + k);
   __syncthreads();
   const float* lrow = logits + ((int64_t)b * gamma + step - 1) * V;
@@ -174,6 +215,7 @@ __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int r
     top2_merge(k1, v2, ok, ov);
   }
   const int w = threadIdx.x >> 6;
+  __syncthreads();
   if ((threadIdx.x & 63) == 0) {
     rk[w] = k1;
     rv[w] = v2;
@@ -181,45 +223,9 @@ __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int r
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int i = 1; i < 4; ++i) top2_merge(rk[0], rv[0], rk[i], rv[i]);
-    uint64_t* pp = part + ((int64_t)b * n_chunks + c) * 2;
+    uint64_t* pp = part + (((int64_t)(step & 1) * B + b) * n_chunks + c) * 2;
     pp[0] = rk[0];
     pp[1] = (uint64_t)__float_as_uint(rv[0]);
-    __threadfence();
-    const unsigned ticket = atomicAdd(&counters[b], 1u);
-    last = (ticket == (unsigned)(n_chunks - 1));
-  }
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  // last workgroup of this request: reduce all chunks
-  uint64_t K1 = 0;
-  float V2 = -INFINITY;
-  for (int i = threadIdx.x; i < n_chunks; i += 256) {
-    const uint64_t* pp = part + ((int64_t)b * n_chunks + i) * 2;
-    const uint64_t kk = __atomic_load_n(pp, __ATOMIC_RELAXED);
-    const float vv = __uint_as_float((uint32_t)__atomic_load_n(pp + 1, __ATOMIC_RELAXED));
-    top2_merge(K1, V2, kk, vv);
-  }
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint64_t ok = __shfl_xor(K1, o, kWave);
-    const float ov = __shfl_xor(V2, o, kWave);
-    top2_merge(K1, V2, ok, ov);
-  }
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) {
-    rk[w] = K1;
-    rv[w] = V2;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int i = 1; i < 4; ++i) top2_merge(rk[0], rv[0], rk[i], rv[i]);
-    const int y = (int)key_index(rk[0]);
-    drafts[b * gamma + step - 1] = y;
-    next_spine[b * (gamma + 1) + step] = y;
-    if (step == 1) next_spine[b * (gamma + 1)] = bonus[b] < 0 || bonus[b] >= V ? 0 : bonus[b];
-    if (margins) margins[b * gamma + step - 1] = key_value(rk[0]) - rv[0];
-    counters[b] = 0;
   }
 }
 
@@ -253,23 +259,17 @@ hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, cons
 
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                           const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                          uint64_t* part, int n_chunks, int chunk, unsigned* counters, int* status,
-                          hipStream_t st) {
-  hipLaunchKernelGGL(fill_u32, dim3((B + 255) / 256), dim3(256), 0, st, counters, B, 0u);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  dim3 grid(n_chunks, B);
-  for (int step = 1; step <= gamma; ++step) {
+                          uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st) {
+  for (int step = 1; step <= gamma + 1; ++step) {
     Phase ph("ar_step", st);
+    dim3 grid(step <= gamma ? n_chunks : 1, B);
     if (dtype == 1)
       hipLaunchKernelGGL(ar_step<bf16_t>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const bf16_t*)E,
-                         (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, counters,
-                         status);
+                         (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
     else
       hipLaunchKernelGGL(ar_step<float>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const float*)E,
-                         (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, counters,
-                         status);
-    e = hipGetLastError();
+                         (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
