@@ -81,6 +81,120 @@ def cpu_baseline(wl, weights, ri):
                        + (f", scaled x{wl.batch} to the batch" if wl.batch > 1 else ""))}
 
 
+def full_round(args, wl):
+    """Single-GPU full round: the target's verification forward and the drafter's append +
+    all-boundary backbone on two streams, joined by an event, then greedy verify on the
+    target logits and select + AR head (Algorithm 1 with the colocated placement)."""
+    import numpy as np
+    import torch
+    from paper_2609_27396_amd import dpara as D
+    from paper_2609_27396_amd import synth
+    from paper_2609_27396_amd.harness import DeviceRound
+
+    shape, B = wl.shape, wl.batch
+    tshape = synth.QWEN3_8B_TARGET
+    t0 = time.time()
+    weights = synth.make_weights(shape, seed=wl.seed_w)
+    ri = synth.make_round(wl)
+    dr = DeviceRound(shape, weights, ri)
+    cap = dr.ctx_cap
+    tgt = D.DeviceTarget(tshape, None, seed=100)
+    tctx = D.DeviceContext(tshape, B, cap)
+    synth.device_normal_(tctx.k, 201)
+    synth.device_normal_(tctx.v, 202)
+    tctx.ctx_len[:B] = torch.from_numpy(ri.ctx_lens.astype(np.int32)).cuda()
+    tws = D.Workspace(tgt.cfg, B, cap, target=True)
+    logits = torch.empty((B, shape.gamma + 1, shape.vocab), dtype=torch.bfloat16, device="cuda")
+    torch.cuda.synchronize()
+    log(f"[bench] full round set up in {time.time() - t0:.1f} s (target {tshape.n_layers} layers on device)")
+
+    n_new_h = ri.accept_planted.astype(np.int32) + 1
+    n_new = torch.from_numpy(n_new_h).cuda()
+    base_len = torch.from_numpy((ri.ctx_lens - n_new_h).astype(np.int32)).cuda()
+    s_draft, s_ver = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def draft(st):
+        with torch.cuda.stream(st):
+            dr.ctx.ctx_len[:B].copy_(base_len)
+            dr.append(n_new, stream=st)
+            dr.backbone(stream=st)
+
+    def verify_pass(st):
+        with torch.cuda.stream(st):
+            D.target_forward(tgt, tctx, dr.spine, logits, tws, stream=st)
+
+    def serial(st):
+        with torch.cuda.stream(st):
+            D.verify_greedy(dr.d, logits, dr.spine, dr.accept, dr.bonus, dr.targmax, dr.ws, stream=st)
+            dr.head(stream=st)
+
+    def round_(overlap=True):
+        start = torch.cuda.Event()
+        start.record(torch.cuda.current_stream())
+        s_draft.wait_event(start)
+        s_ver.wait_event(start)
+        draft(s_draft)
+        if not overlap:
+            s_ver.wait_stream(s_draft)
+        verify_pass(s_ver)
+        s_ver.wait_stream(s_draft)  # barrier: (r, b) and all branches ready
+        serial(s_ver)
+        torch.cuda.current_stream().wait_stream(s_ver)
+
+    def timed(fn, k):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(k):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / k
+
+    def only(fn, st):
+        def go():
+            st.wait_stream(torch.cuda.current_stream())
+            fn(st)
+            torch.cuda.current_stream().wait_stream(st)
+        return go
+
+    def both():
+        start = torch.cuda.Event()
+        start.record(torch.cuda.current_stream())
+        s_draft.wait_event(start)
+        s_ver.wait_event(start)
+        draft(s_draft)
+        verify_pass(s_ver)
+        torch.cuda.current_stream().wait_stream(s_draft)
+        torch.cuda.current_stream().wait_stream(s_ver)
+
+    for _ in range(args.warmup):
+        round_()
+    K = args.steps
+    t_v = timed(only(verify_pass, s_ver), K)
+    t_bb = timed(only(draft, s_draft), K)
+    t_serial = timed(only(serial, s_ver), K)
+    t_both = timed(both, K)
+    t_seq = timed(lambda: round_(overlap=False), K)
+    ms = timed(round_, K)
+    assert dr.status() == 0
+    hidden = (t_v + t_bb - t_both) / t_bb
+    out = {
+        "metric": METRIC, "value": 1000.0 / ms, "unit": "rounds/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "gamma": shape.gamma, "ctx": int(ri.ctx_lens[0]),
+                   "drafter_layers": shape.n_layers, "target_layers": tshape.n_layers, "hidden": shape.hidden,
+                   "vocab": shape.vocab},
+        "overlap": {"target_verify_ms": t_v, "append_backbone_ms": t_bb, "both_concurrent_ms": t_both,
+                    "serial_verify_head_ms": t_serial, "round_overlapped_ms": ms, "round_sequential_ms": t_seq,
+                    "backbone_hidden_fraction": hidden,
+                    "paper_model_ms": max(t_v, t_bb) + t_serial,
+                    "serial_share_of_verify": t_serial / t_v},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -103,6 +217,9 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     shape = wl.shape
     log(f"[bench] workload {wl.name}: {wl.description}")
+    if wl.name == "full_round":
+        full_round(args, wl)
+        return
     t0 = time.time()
     weights = synth.make_weights(shape, seed=wl.seed_w)
     ri = synth.make_round(wl)

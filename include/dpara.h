@@ -174,6 +174,30 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
                           float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
                           void* ws, size_t ws_bytes, void* stream);
 
+/* Target verification forward, used for the single-GPU overlap of verification and drafting
+ * (Algorithm 1, Verify; Section 4.3.2 and Appendix D: both passes on two streams of one GPU).
+ * A causal Qwen3-shaped decoder (same layer structure and dpara_config_t fields as the drafter;
+ * gamma+1 = block length; ar_rank ignored; bf16 only) forwards each request's block
+ * t_0..t_gamma at positions ctx_len[b]+j over its own per-layer K/V cache `ctx` (stored as
+ * dpara_ctx_t describes; the cache is read, not updated), then the final RMSNorm (rounded to
+ * bf16) and the untied LM head.
+ * block:  [batch, gamma+1] int32 (device).
+ * logits: [batch, gamma+1, vocab] (device, output), logits_dtype DPARA_F32 or DPARA_BF16;
+ *         row j scores the token after t_j (the input of dpara_verify_greedy).
+ * ws: a workspace of dpara_target_workspace_bytes() bytes (separate from the drafter's, so
+ *     both passes can run concurrently on different streams). */
+typedef struct dpara_target_weights {
+  const void* embed;                   /* [vocab, hidden] (device) */
+  const void* lm_head;                 /* [vocab, hidden] (device), untied */
+  const float* final_norm;             /* [hidden] (device) */
+  const dpara_layer_weights_t* layers; /* [n_layers] (HOST array of device pointers) */
+} dpara_target_weights_t;
+
+size_t dpara_target_workspace_bytes(const dpara_config_t* cfg, int32_t batch, int32_t ctx_cap);
+int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t* w,
+                         const dpara_ctx_t* ctx, int32_t batch, const int32_t* block, void* logits,
+                         int32_t logits_dtype, void* ws, size_t ws_bytes, void* stream);
+
 /* Enqueue a clear of the status word at byte offset 0 of `ws` (a fill kernel). */
 int dpara_clear_status(void* ws, void* stream);
 

@@ -109,14 +109,14 @@ int check_ctx(const dpara_ctx_t* x, int batch) {
 struct Plan {
   int B, R, M, S, chunk, CH, esz;
   int v_chunk, v_chunks, h_chunk, h_chunks;
-  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, rope, vpart, G, logits, hpart, counters, F, KV32;
+  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, rope, vpart, G, Gsplit, logits, hpart, counters, F, KV32;
   size_t total;
 };
 
-Plan make_plan(const dpara_config_t* c, int B, int ctx_cap) {
+Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   Plan p{};
   p.B = B;
-  p.R = (c->gamma + 1) * (c->gamma + 1);
+  p.R = R > 0 ? R : (c->gamma + 1) * (c->gamma + 1);
   p.M = B * p.R;
   p.esz = c->dtype == DPARA_BF16 ? 2 : 4;
   const int hd = c->head_dim, nq = c->n_q_heads, nkv = c->n_kv_heads, H = c->hidden;
@@ -139,7 +139,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap) {
   p.CH = p.R;
   p.v_chunk = 4096;
   p.v_chunks = (c->vocab + p.v_chunk - 1) / p.v_chunk;
-  p.h_chunk = 512;
+  p.h_chunk = 256;
   p.h_chunks = (c->vocab + p.h_chunk - 1) / p.h_chunk;
   const size_t M = p.M;
   size_t off = 256;  // status header
@@ -161,6 +161,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap) {
   p.rope = take((size_t)B * (2 * c->gamma + 1) * (hd / 2) * 8);
   p.vpart = take((size_t)B * (c->gamma + 1) * p.v_chunks * 8);
   p.G = take((size_t)B * c->gamma * H * 4);
+  p.Gsplit = take((size_t)2 * B * c->gamma * H * 2);  // bf16 hi and lo planes of G
   p.logits = take((size_t)B * c->gamma * c->vocab * 4);
   p.hpart = take((size_t)2 * B * p.h_chunks * 16);  // two step-parity slots
   p.counters = take((size_t)B * 4);
@@ -231,6 +232,134 @@ Phase::~Phase() {
   (void)hipEventRecord(g_prof[slot].b, st);
 }
 }  // namespace dpara
+
+namespace {
+// Shared decoder pass over R block rows per request: row assembly, then every layer
+// (RMSNorm -> QKV -> q/k-norm + RoPE -> attention over the cache and the in-block keys ->
+// O + residual -> RMSNorm -> gate|up + SwiGLU -> down + residual).  spine_only selects the
+// causal block (the target's verification pass); otherwise rows follow the tree layout.
+// Leaves the residual stream in ws[p.X].
+int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, const void* embed,
+                const void* mask_emb, const dpara_ctx_t* ctx, int32_t batch, const int32_t* tokens,
+                int spine_only, const Plan& p, void* ws, hipStream_t st) {
+  const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q_heads, nkv = cfg->n_kv_heads;
+  const int g = cfg->gamma, R = p.R, M = p.M, F = cfg->ffn;
+  const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
+  int* status = at<int>(ws, 0);
+  float* X = at<float>(ws, p.X);
+  const size_t layer_elems = (size_t)ctx->batch_cap * nkv * ctx->ctx_cap * hd;
+
+  {
+  Phase ph("assemble", st);
+  HIP_TRY(launch_assemble_rows(dt, batch, R, g, H, cfg->vocab, tokens, embed, mask_emb, X, status, st),
+          "assemble_rows");
+  HIP_TRY(launch_rope_table(batch, 2 * g + 1, hd, cfg->rope_base, ctx->ctx_len, 0, at<float2>(ws, p.rope), st),
+          "rope_table");
+  }
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const dpara_layer_weights_t& Lw = layers[l];
+    {
+    Phase ph("rmsnorm", st);
+    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.attn_norm, cfg->rms_eps, at<void>(ws, p.A), st), "attn_norm");
+    }
+    GemmArgs q{};
+    q.A = at<void>(ws, p.A);
+    q.lda = H;
+    q.B0 = Lw.wq;
+    q.B1 = Lw.wk;
+    q.B2 = Lw.wv;
+    q.n1 = nq * hd;
+    q.n2 = (nq + nkv) * hd;
+    q.M = M;
+    q.N = (nq + 2 * nkv) * hd;
+    q.K = H;
+    q.C = at<void>(ws, p.QKV);
+    q.ldc = q.N;
+    {
+    Phase ph("qkv_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_STORE_F32, q, st), "qkv gemm");
+    }
+    {
+    Phase ph("qk_norm_rope", st);
+    HIP_TRY(launch_qk_norm_rope(dt, batch, R, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
+                                Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
+                                at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
+            "qk_norm_rope");
+    }
+    AttnArgs aa{};
+    aa.B = batch;
+    aa.R = R;
+    aa.gamma = g;
+    aa.n_q = nq;
+    aa.n_kv = nkv;
+    aa.hd = hd;
+    aa.Q = at<void>(ws, p.Q);
+    aa.Kb = at<void>(ws, p.Kb);
+    aa.Vb = at<void>(ws, p.Vb);
+    aa.Kc = (const char*)ctx->k + l * layer_elems * p.esz;
+    aa.Vc = (const char*)ctx->v + l * layer_elems * p.esz;
+    aa.cap = ctx->ctx_cap;
+    aa.ctx_len = ctx->ctx_len;
+    aa.S = p.S;
+    aa.chunk = p.chunk;
+    aa.Opart = at<float>(ws, p.Opart);
+    aa.MLpart = at<float>(ws, p.ML);
+    aa.O = at<void>(ws, p.O);
+    aa.spine_only = spine_only;
+    HIP_TRY(launch_attention(dt, aa, st), "attention");
+    GemmArgs o{};
+    o.A = at<void>(ws, p.O);
+    o.lda = nq * hd;
+    o.B0 = o.B1 = o.B2 = Lw.wo;
+    o.n1 = o.n2 = H;
+    o.M = M;
+    o.N = H;
+    o.K = nq * hd;
+    o.C = X;
+    o.ldc = H;
+    {
+    Phase ph("o_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, o, st), "o-proj gemm");
+    }
+    {
+    Phase ph("rmsnorm", st);
+    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.mlp_norm, cfg->rms_eps, at<void>(ws, p.A), st), "mlp_norm");
+    }
+    GemmArgs gu{};
+    gu.A = at<void>(ws, p.A);
+    gu.lda = H;
+    gu.B0 = Lw.w_gate;
+    gu.B1 = Lw.w_up;
+    gu.B2 = Lw.w_up;
+    gu.n1 = gu.n2 = F;
+    gu.M = M;
+    gu.N = F;
+    gu.K = H;
+    gu.C = at<void>(ws, p.Hmid);
+    gu.ldc = F;
+    {
+    Phase ph("gateup_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_SWIGLU, gu, st), "gate/up gemm");
+    }
+    GemmArgs dn{};
+    dn.A = at<void>(ws, p.Hmid);
+    dn.lda = F;
+    dn.B0 = dn.B1 = dn.B2 = Lw.w_down;
+    dn.n1 = dn.n2 = H;
+    dn.M = M;
+    dn.N = H;
+    dn.K = F;
+    dn.C = X;
+    dn.ldc = H;
+    {
+    Phase ph("down_gemm", st);
+    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, dn, st), "down gemm");
+    }
+  }
+  return DPARA_OK;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -352,128 +481,76 @@ int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights
   const Plan p = make_plan(cfg, batch, ctx->ctx_cap);
   if ((rc = check_ws(p, ws, ws_bytes))) return rc;
   if ((rc = check_device())) return rc;
-
   hipStream_t st = (hipStream_t)stream;
-  const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q_heads, nkv = cfg->n_kv_heads;
-  const int g = cfg->gamma, R = p.R, M = p.M, F = cfg->ffn;
-  const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
-  int* status = at<int>(ws, 0);
-  float* X = at<float>(ws, p.X);
-  const size_t layer_elems = (size_t)ctx->batch_cap * nkv * ctx->ctx_cap * hd;
-
-  {
-  Phase ph("assemble", st);
-  HIP_TRY(launch_assemble_rows(dt, batch, R, g, H, cfg->vocab, spine, w->embed, w->mask_emb, X, status, st),
-          "assemble_rows");
-  HIP_TRY(launch_rope_table(batch, 2 * g + 1, hd, cfg->rope_base, ctx->ctx_len, 0, at<float2>(ws, p.rope), st),
-          "rope_table");
-  }
-  for (int l = 0; l < cfg->n_layers; ++l) {
-    const dpara_layer_weights_t& Lw = w->layers[l];
-    {
-    Phase ph("rmsnorm", st);
-    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.attn_norm, cfg->rms_eps, at<void>(ws, p.A), st), "attn_norm");
-    }
-    GemmArgs q{};
-    q.A = at<void>(ws, p.A);
-    q.lda = H;
-    q.B0 = Lw.wq;
-    q.B1 = Lw.wk;
-    q.B2 = Lw.wv;
-    q.n1 = nq * hd;
-    q.n2 = (nq + nkv) * hd;
-    q.M = M;
-    q.N = (nq + 2 * nkv) * hd;
-    q.K = H;
-    q.C = at<void>(ws, p.QKV);
-    q.ldc = q.N;
-    {
-    Phase ph("qkv_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_STORE_F32, q, st), "qkv gemm");
-    }
-    {
-    Phase ph("qk_norm_rope", st);
-    HIP_TRY(launch_qk_norm_rope(dt, batch, R, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
-                                Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
-                                at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
-            "qk_norm_rope");
-    }
-    AttnArgs aa{};
-    aa.B = batch;
-    aa.R = R;
-    aa.gamma = g;
-    aa.n_q = nq;
-    aa.n_kv = nkv;
-    aa.hd = hd;
-    aa.Q = at<void>(ws, p.Q);
-    aa.Kb = at<void>(ws, p.Kb);
-    aa.Vb = at<void>(ws, p.Vb);
-    aa.Kc = (const char*)ctx->k + l * layer_elems * p.esz;
-    aa.Vc = (const char*)ctx->v + l * layer_elems * p.esz;
-    aa.cap = ctx->ctx_cap;
-    aa.ctx_len = ctx->ctx_len;
-    aa.S = p.S;
-    aa.chunk = p.chunk;
-    aa.Opart = at<float>(ws, p.Opart);
-    aa.MLpart = at<float>(ws, p.ML);
-    aa.O = at<void>(ws, p.O);
-    aa.spine_only = 0;
-    HIP_TRY(launch_attention(dt, aa, st), "attention");
-    GemmArgs o{};
-    o.A = at<void>(ws, p.O);
-    o.lda = nq * hd;
-    o.B0 = o.B1 = o.B2 = Lw.wo;
-    o.n1 = o.n2 = H;
-    o.M = M;
-    o.N = H;
-    o.K = nq * hd;
-    o.C = X;
-    o.ldc = H;
-    {
-    Phase ph("o_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, o, st), "o-proj gemm");
-    }
-    {
-    Phase ph("rmsnorm", st);
-    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.mlp_norm, cfg->rms_eps, at<void>(ws, p.A), st), "mlp_norm");
-    }
-    GemmArgs gu{};
-    gu.A = at<void>(ws, p.A);
-    gu.lda = H;
-    gu.B0 = Lw.w_gate;
-    gu.B1 = Lw.w_up;
-    gu.B2 = Lw.w_up;
-    gu.n1 = gu.n2 = F;
-    gu.M = M;
-    gu.N = F;
-    gu.K = H;
-    gu.C = at<void>(ws, p.Hmid);
-    gu.ldc = F;
-    {
-    Phase ph("gateup_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_SWIGLU, gu, st), "gate/up gemm");
-    }
-    GemmArgs dn{};
-    dn.A = at<void>(ws, p.Hmid);
-    dn.lda = F;
-    dn.B0 = dn.B1 = dn.B2 = Lw.w_down;
-    dn.n1 = dn.n2 = H;
-    dn.M = M;
-    dn.N = H;
-    dn.K = F;
-    dn.C = X;
-    dn.ldc = H;
-    {
-    Phase ph("down_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, dn, st), "down gemm");
-    }
-  }
-  // reps[b][r][i-1] = final_norm of mask rows: input row (m / (R-g-1)) * R*H + (g+1 + m % (R-g-1)) * H
+  if ((rc = run_decoder(cfg, w->layers, w->embed, w->mask_emb, ctx, batch, spine, 0, p, ws, st))) return rc;
+  // reps[b][r][i-1] = final norm of mask rows: input row (m / nmask) * R + (g + 1 + m % nmask)
+  const int g = cfg->gamma, R = p.R, H = cfg->hidden;
   const int nmask = R - g - 1;
   Phase ph("final_norm", st);
-  HIP_TRY(launch_rmsnorm(0, batch * nmask, H, X, nmask, (int64_t)R * H, g + 1, w->final_norm, cfg->rms_eps, reps,
-                         st),
+  HIP_TRY(launch_rmsnorm(0, batch * nmask, H, at<float>(ws, p.X), nmask, (int64_t)R * H, g + 1, w->final_norm,
+                         cfg->rms_eps, reps, st),
           "final_norm");
+  return DPARA_OK;
+}
+
+size_t dpara_target_workspace_bytes(const dpara_config_t* cfg, int32_t batch, int32_t ctx_cap) {
+  if (!cfg) return 0;
+  dpara_config_t c = *cfg;
+  c.ar_rank = 64;
+  if (check_cfg(&c) != DPARA_OK || batch < 1 || ctx_cap < 64 || ctx_cap % 64) return 0;
+  return make_plan(&c, batch, ctx_cap, cfg->gamma + 1).total;
+}
+
+int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t* w, const dpara_ctx_t* ctx,
+                         int32_t batch, const int32_t* block, void* logits, int32_t logits_dtype, void* ws,
+                         size_t ws_bytes, void* stream) {
+  if (!cfg) return fail(DPARA_E_INVALID, "cfg is NULL");
+  dpara_config_t c = *cfg;
+  c.ar_rank = 64;  // the target has no AR head
+  int rc = check_cfg(&c);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if (c.dtype != DPARA_BF16) return fail(DPARA_E_UNSUPPORTED, "the target forward runs in bf16 only");
+  if (logits_dtype != DPARA_F32 && logits_dtype != DPARA_BF16)
+    return fail(DPARA_E_UNSUPPORTED, "logits_dtype must be F32 or BF16");
+  if (!w || !w->layers) return fail(DPARA_E_INVALID, "target weights or layers is NULL");
+  CHECK_PTR(w->embed, "embed");
+  CHECK_PTR(w->lm_head, "lm_head");
+  CHECK_PTR(w->final_norm, "final_norm");
+  dpara_weights_t shim{};
+  shim.embed = w->embed;
+  shim.mask_emb = w->embed;
+  shim.final_norm = w->final_norm;
+  shim.layers = w->layers;
+  if ((rc = check_weights(&c, &shim, true))) return rc;
+  if ((rc = check_ctx(ctx, batch))) return rc;
+  if (!block) return fail(DPARA_E_INVALID, "block is NULL");
+  CHECK_PTR(logits, "logits");
+  const Plan p = make_plan(&c, batch, ctx->ctx_cap, c.gamma + 1);
+  if ((rc = check_ws(p, ws, ws_bytes))) return rc;
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  if ((rc = run_decoder(&c, w->layers, w->embed, w->embed, ctx, batch, block, 1, p, ws, st))) return rc;
+  const int H = c.hidden, M = p.M;
+  {
+    Phase ph("final_norm", st);
+    HIP_TRY(launch_rmsnorm(DPARA_BF16, M, H, at<float>(ws, p.X), M, 0, 0, w->final_norm, c.rms_eps,
+                           at<void>(ws, p.A), st),
+            "target final norm");
+  }
+  GemmArgs lm{};
+  lm.A = at<void>(ws, p.A);
+  lm.lda = H;
+  lm.B0 = lm.B1 = lm.B2 = w->lm_head;
+  lm.n1 = lm.n2 = c.vocab;
+  lm.M = M;
+  lm.N = c.vocab;
+  lm.K = H;
+  lm.C = logits;
+  lm.ldc = c.vocab;
+  Phase ph("lm_head", st);
+  HIP_TRY(launch_gemm(A_BF16, logits_dtype == DPARA_BF16 ? EPI_STORE_BF16 : EPI_STORE_F32, lm, st),
+          "target lm head");
   return DPARA_OK;
 }
 
@@ -521,9 +598,12 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   const int g = cfg->gamma, H = cfg->hidden, V = cfg->vocab;
   int* status = at<int>(ws, 0);
   float* G = at<float>(ws, p.G);
-  HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, G, gathered, status, st), "gather_branch");
+  bf16_t* Gs = at<bf16_t>(ws, p.Gsplit);
+  HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, G, gathered, Gs, status, st), "gather_branch");
+  const bool bf = cfg->dtype == DPARA_BF16;
   GemmArgs lm{};
-  lm.A = G;
+  lm.A = bf ? (const void*)Gs : (const void*)G;
+  lm.lo_off = (int64_t)batch * g * H;
   lm.lda = H;
   lm.B0 = lm.B1 = lm.B2 = w->embed;
   lm.n1 = lm.n2 = V;
@@ -534,7 +614,7 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   lm.ldc = V;
   {
     Phase ph("lm_head", st);
-    HIP_TRY(launch_gemm(cfg->dtype == DPARA_BF16 ? A_F32SPLIT : A_F32, EPI_STORE_F32, lm, st), "lm head gemm");
+    HIP_TRY(launch_gemm(bf ? A_BF16_DUAL : A_F32, EPI_STORE_F32, lm, st), "lm head gemm");
   }
   HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,

@@ -84,18 +84,22 @@ __device__ __forceinline__ int swz(int r, int c) {
   return c ^ ((r >> 1) & 3);
 }
 
-template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI>
+// DUAL: A is given as two bf16 planes (hi at A, lo at A + a.lo_off elements) whose sum is
+// the float32 operand; every weight fragment is multiplied by both planes.
+template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI, int DUAL>
 __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, int MT, int NT) {
   constexpr int NW = WMW * WNW;
+  constexpr int NPL = DUAL ? 2 : 1;  // A planes
   constexpr int CH = BKB / 16;      // 16-byte chunks per tile row per stage
   constexpr int RPI = 1024 / BKB;   // tile rows per DMA instruction
   constexpr int KB = BKB / 2;       // bf16 elements per tile row per stage
   constexpr int WM = BM / WMW, WN = BN / WNW;
   constexpr int FM = WM / 16, FN = WN / 16;
-  constexpr int A_INS = BM / RPI / NW, B_INS = BN / RPI / NW;
-  static_assert(A_INS * RPI * NW == BM && B_INS * RPI * NW == BN, "tile rows must split evenly over waves");
+  constexpr int A_INS = NPL * BM / RPI / NW, B_INS = BN / RPI / NW;
+  static_assert(A_INS * RPI * NW == NPL * BM && B_INS * RPI * NW == BN, "tile rows must split evenly over waves");
   static_assert(KB % 32 == 0, "stage depth must be a multiple of the MFMA k");
-  constexpr int STAGE_BYTES = (BM + BN) * BKB;
+  constexpr int A_ROWS = NPL * BM;   // stage rows of A: [0, BM) hi (or the only plane), [BM, 2BM) lo
+  constexpr int STAGE_BYTES = (A_ROWS + BN) * BKB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   int mt, nt;
@@ -111,9 +115,10 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
   const int lrow = lane / CH, lslot = lane % CH;
 #pragma unroll
   for (int j = 0; j < A_INS; ++j) {
-    const int r = (wave + NW * j) * RPI + lrow;
-    const int gm = min(m0 + r, a.M - 1);
-    asrc[j] = (const bf16_t*)a.A + (int64_t)gm * a.lda + swz<CH>(r, lslot) * 8;
+    const int r = (wave + NW * j) * RPI + lrow;   // stage row
+    const int plane = r >= BM ? 1 : 0;
+    const int gm = min(m0 + r - plane * BM, a.M - 1);
+    asrc[j] = (const bf16_t*)a.A + (plane ? a.lo_off : 0) + (int64_t)gm * a.lda + swz<CH>(r, lslot) * 8;
   }
 #pragma unroll
   for (int j = 0; j < B_INS; ++j) {
@@ -130,7 +135,7 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
 #pragma unroll
     for (int j = 0; j < B_INS; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(bsrc[j] + k0),
-                                       (lds_void_t*)(sb + BM * BKB + (wave + NW * j) * 1024), 16, 0, 0);
+                                       (lds_void_t*)(sb + A_ROWS * BKB + (wave + NW * j) * 1024), 16, 0, 0);
   };
 
   f32x4_t acc[FM][FN];
@@ -150,7 +155,7 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     __builtin_amdgcn_s_barrier();
     if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const unsigned char* sa = smem + (kt % STAGES) * STAGE_BYTES;
-    const unsigned char* sb = sa + BM * BKB;
+    const unsigned char* sb = sa + A_ROWS * BKB;
 #pragma unroll
     for (int ks = 0; ks < KB / 32; ++ks) {
       const int c = ks * 4 + lc;
@@ -161,12 +166,15 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
         bfr[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
       }
 #pragma unroll
-      for (int mi = 0; mi < FM; ++mi) {
-        const int r = wm * WM + mi * 16 + lr;
-        const bf16x8_t afr = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
+      for (int pl = 0; pl < NPL; ++pl) {
 #pragma unroll
-        for (int ni = 0; ni < FN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[ni], acc[mi][ni], 0, 0, 0);
+        for (int mi = 0; mi < FM; ++mi) {
+          const int r = pl * BM + wm * WM + mi * 16 + lr;
+          const bf16x8_t afr = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
+#pragma unroll
+          for (int ni = 0; ni < FN; ++ni)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[ni], acc[mi][ni], 0, 0, 0);
+        }
       }
     }
   }
@@ -183,6 +191,13 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
         for (int ni = 0; ni < FN / 2; ++ni) {
           const int f = nt * (BN / 2) + wn * (WN / 2) + ni * 16 + lr;
           if (f < a.N) C[f] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+        }
+      } else if constexpr (EPI == EPI_STORE_BF16) {
+        bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) {
+          const int col = nt * BN + wn * WN + ni * 16 + lr;
+          if (col < a.N) C[col] = f2bf(acc[mi][ni][r]);
         }
       } else {
         float* C = (float*)a.C + (int64_t)row * a.ldc;
@@ -421,12 +436,12 @@ hipError_t run_f32(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI>
+template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI, int DUAL = 0>
 hipError_t run_pipe(const GemmArgs& a, hipStream_t st) {
   const int MT = (a.M + BM - 1) / BM;
   const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
-  constexpr int lds = STAGES * (BM + BN) * BKB;
-  auto kern = gemm_pipe_kernel<BM, BN, WMW, WNW, STAGES, BKB, EPI>;
+  constexpr int lds = STAGES * ((DUAL ? 2 : 1) * BM + BN) * BKB;
+  auto kern = gemm_pipe_kernel<BM, BN, WMW, WNW, STAGES, BKB, EPI, DUAL>;
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (attr != hipSuccess) return attr;
@@ -455,8 +470,14 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     switch (epi) {
       case EPI_STORE_F32: return run_f32<EPI_STORE_F32>(a, st);
       case EPI_ADD_F32: return run_f32<EPI_ADD_F32>(a, st);
-      default: return run_f32<EPI_SWIGLU>(a, st);
+      case EPI_SWIGLU: return run_f32<EPI_SWIGLU>(a, st);
+      default: return hipErrorInvalidValue;
     }
+  }
+  if (amode == A_BF16_DUAL) {
+    if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 128, EPI_STORE_F32, 1>(a, st);
+    if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
+    return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }
   const bool small = a.M <= 512;
   if (amode == A_F32SPLIT) {
@@ -464,6 +485,7 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
                  : run_mfma<128, 128, EPI_STORE_F32, A_F32SPLIT>(a, st);
   }
   switch (epi) {
+    case EPI_STORE_BF16: return run_bf16<EPI_STORE_BF16>(a, st);
     case EPI_STORE_F32: return run_bf16<EPI_STORE_F32>(a, st);
     case EPI_ADD_F32: return run_bf16<EPI_ADD_F32>(a, st);
     default: return run_bf16<EPI_SWIGLU>(a, st);

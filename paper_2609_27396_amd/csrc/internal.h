@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "common.h"
+
 namespace dpara {
 
 // Per-phase tracing: when enabled (dpara_profile_enable), records a HIP event pair on `st`
@@ -19,11 +21,13 @@ struct Phase {
 // ---------------------------------------------------------------- GEMM
 // C[M, N] (op)= A[M, K] . B[N, K]^T with B given in up to three row segments
 // (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2).
-enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3 };
 // A_BF16: A is bf16.  A_F32SPLIT: A is float32 and is applied as hi + lo bf16 parts
 // (two MFMA passes), which keeps ~16 significant bits of A.  A_F32: float32 FMA kernel
 // (the float32 model path; B is then float32 too).
-enum GemmAMode { A_BF16 = 0, A_F32SPLIT = 1, A_F32 = 2 };
+// A_BF16_DUAL: A given as two bf16 planes hi (at A) and lo (at A + lo_off elements) with
+// hi + lo = the float32 operand to ~16 significant bits; both planes meet every weight tile.
+enum GemmAMode { A_BF16 = 0, A_F32SPLIT = 1, A_F32 = 2, A_BF16_DUAL = 3 };
 
 struct GemmArgs {
   const void* A;
@@ -35,6 +39,7 @@ struct GemmArgs {
   int M, N, K;
   void* C;
   int64_t ldc;
+  int64_t lo_off;  // A_BF16_DUAL only
   // EPI_SWIGLU: B0 = gate [N, K], B1 = up [N, K], C = bf16/f32 [M, N] of silu(g) * u,
   // where N is the FFN width.
 };
@@ -87,9 +92,10 @@ hipError_t launch_clear_status(int* status, hipStream_t st);
 hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits,
                          const int* spine, int* accept_len, int* bonus, int* target_argmax,
                          uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st);
+// G (fp32, optional copy G_out) and its bf16 hi/lo split planes Ghi, Glo = Ghi + M*H.
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
-                                const int* accept_len, float* G, float* G_out, int* status,
-                                hipStream_t st);
+                                const int* accept_len, float* G, float* G_out, bf16_t* Ghi,
+                                int* status, hipStream_t st);
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits,
                           const void* E, const void* W, const int* bonus, int* drafts,
                           int* next_spine, float* margins, uint64_t* part, int n_chunks,

@@ -68,23 +68,35 @@ __global__ __launch_bounds__(64) void verify_finalize(int gamma, int V, int n_ch
 }
 
 __global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const float* reps, const int* accept_len,
-                                                     float* G, float* G_out, int* status) {
+                                                     float* G, float* G_out, bf16_t* Ghi, int64_t lo_off,
+                                                     int* status) {
   const int i = blockIdx.x, b = blockIdx.y;
   int r = accept_len[b];
   if (r < 0 || r > gamma) {
     if (threadIdx.x == 0) raise_status(status, 4);
     r = r < 0 ? 0 : gamma;
   }
+  const int64_t row = (int64_t)b * gamma + i;
   const float4* src = (const float4*)(reps + (((int64_t)b * (gamma + 1) + r) * gamma + i) * H);
-  float4* dst = (float4*)(G + ((int64_t)b * gamma + i) * H);
-  float4* dst2 = G_out ? (float4*)(G_out + ((int64_t)b * gamma + i) * H) : nullptr;
+  float4* dst = (float4*)(G + row * H);
+  float4* dst2 = G_out ? (float4*)(G_out + row * H) : nullptr;
+  bf16_t* hi = Ghi + row * H;
+  bf16_t* lo = hi + lo_off;
   for (int k = threadIdx.x; k < H / 4; k += 256) {
     const float4 v = src[k];
     dst[k] = v;
     if (dst2) dst2[k] = v;
+    const float x[4] = {v.x, v.y, v.z, v.w};
+    bf16_t h[4], l[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      h[j] = f2bf(x[j]);
+      l[j] = f2bf(x[j] - bf2f(h[j]));
+    }
+    *(uint2*)(hi + 4 * k) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+    *(uint2*)(lo + 4 * k) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
   }
 }
-
 
 // Merge (key1, second-best value) pairs.
 __device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1, float ov2) {
@@ -250,10 +262,10 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
 }
 
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, const int* accept_len, float* G,
-                                float* G_out, int* status, hipStream_t st) {
+                                float* G_out, bf16_t* Ghi, int* status, hipStream_t st) {
   Phase ph("gather", st);
-  hipLaunchKernelGGL(gather_branch, dim3(gamma, B), dim3(256), 0, st, gamma, H, reps, accept_len, G, G_out,
-                     status);
+  hipLaunchKernelGGL(gather_branch, dim3(gamma, B), dim3(256), 0, st, gamma, H, reps, accept_len, G, G_out, Ghi,
+                     (int64_t)B * gamma * H, status);
   return hipGetLastError();
 }
 

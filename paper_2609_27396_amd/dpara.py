@@ -23,7 +23,8 @@ STATUS_TOKEN_RANGE, STATUS_CTX_FULL, STATUS_VERDICT_RANGE, STATUS_COUNT_RANGE = 
 
 EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boundaries",
            "dpara_verify_greedy", "dpara_select_and_head", "dpara_clear_status",
-           "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read")
+           "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
+           "dpara_target_workspace_bytes", "dpara_target_forward")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -55,6 +56,11 @@ class DparaWeights(ctypes.Structure):
                 ("layers", ctypes.POINTER(DparaLayerWeights))]
 
 
+class DparaTargetWeights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
+                ("layers", ctypes.POINTER(DparaLayerWeights))]
+
+
 class DparaCtx(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("ctx_len", ctypes.c_void_p),
                 ("batch_cap", ctypes.c_int32), ("ctx_cap", ctypes.c_int32)]
@@ -80,13 +86,17 @@ def lib():
         L.dpara_select_and_head.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP, VP, VP,
                                             SZ, VP]
         L.dpara_clear_status.argtypes = [VP, VP]
+        L.dpara_target_workspace_bytes.argtypes = [P(DparaConfig), I32, I32]
+        L.dpara_target_workspace_bytes.restype = SZ
+        L.dpara_target_forward.argtypes = [P(DparaConfig), P(DparaTargetWeights), P(DparaCtx), I32, VP, VP, I32,
+                                           VP, SZ, VP]
         L.dpara_last_error.restype = ctypes.c_char_p
         L.dpara_version.restype = I32
         L.dpara_profile_enable.argtypes = [I32]
         L.dpara_profile_read.argtypes = [ctypes.c_char_p, P(ctypes.c_double), P(ctypes.c_int64)]
         for name in ("dpara_ctx_append", "dpara_backbone_all_boundaries", "dpara_verify_greedy",
                      "dpara_select_and_head", "dpara_clear_status", "dpara_profile_enable",
-                     "dpara_profile_read"):
+                     "dpara_profile_read", "dpara_target_forward"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -125,6 +135,15 @@ def dpara_select_and_head(cfg, w, batch, reps, accept_len, bonus, gathered, draf
                           ws_bytes, stream):
     _check(lib().dpara_select_and_head(_ref(cfg), _ref(w), batch, reps, accept_len, bonus, gathered, drafts,
                                        next_spine, margins, ws, ws_bytes, stream))
+
+
+def dpara_target_workspace_bytes(cfg: DparaConfig, batch: int, ctx_cap: int) -> int:
+    return int(lib().dpara_target_workspace_bytes(ctypes.byref(cfg), batch, ctx_cap))
+
+
+def dpara_target_forward(cfg, w, ctx, batch, block, logits, logits_dtype, ws, ws_bytes, stream):
+    _check(lib().dpara_target_forward(_ref(cfg), _ref(w), _ref(ctx), batch, block, logits, logits_dtype, ws,
+                                      ws_bytes, stream))
 
 
 def dpara_clear_status(ws, stream):
@@ -204,6 +223,49 @@ class DeviceDrafter:
         return torch.bfloat16 if self.shape.dtype == "bf16" else torch.float32
 
 
+class DeviceTarget:
+    """Target weights resident in HBM (from host arrays, or generated on device when
+    `weights` is None: timing-only)."""
+
+    def __init__(self, shape, weights: dict | None, device="cuda", seed: int = 100):
+        import torch
+        from . import synth
+        self.shape = shape
+        self.cfg = make_config(shape)
+        self.cfg.ar_rank = 64
+        bf = torch.bfloat16
+        H, hd, F, V = shape.hidden, shape.head_dim, shape.ffn, shape.vocab
+        nq, nkv = shape.n_q_heads, shape.n_kv_heads
+        self.t = {}
+        if weights is not None:
+            for name, arr in weights.items():
+                base = name.split(".")[-1]
+                is_gain = base in ("attn_norm", "mlp_norm", "q_norm", "k_norm", "final_norm")
+                self.t[name] = torch.from_numpy(np.ascontiguousarray(arr)).to(
+                    device=device, dtype=torch.float32 if is_gain else bf)
+        else:
+            shapes = {"embed": (V, H), "lm_head": (V, H)}
+            for l in range(shape.n_layers):
+                shapes.update({f"L{l}.wq": (nq * hd, H), f"L{l}.wk": (nkv * hd, H), f"L{l}.wv": (nkv * hd, H),
+                               f"L{l}.wo": (H, nq * hd), f"L{l}.w_gate": (F, H), f"L{l}.w_up": (F, H),
+                               f"L{l}.w_down": (H, F)})
+            for i, (name, shp) in enumerate(sorted(shapes.items())):
+                self.t[name] = synth.device_normal_(torch.empty(shp, dtype=bf, device=device), seed * 1000 + i, 0.02)
+            ones = lambda n: torch.ones(n, dtype=torch.float32, device=device)
+            self.t["final_norm"] = ones(H)
+            for l in range(shape.n_layers):
+                for g, n in (("attn_norm", H), ("mlp_norm", H), ("q_norm", hd), ("k_norm", hd)):
+                    self.t[f"L{l}.{g}"] = ones(n)
+        self._layers = (DparaLayerWeights * shape.n_layers)()
+        for l in range(shape.n_layers):
+            for f in ("attn_norm", "wq", "wk", "wv", "q_norm", "k_norm", "wo", "mlp_norm", "w_gate", "w_up",
+                      "w_down"):
+                setattr(self._layers[l], f, _ptr(self.t[f"L{l}.{f}"]))
+        self.w = DparaTargetWeights(embed=_ptr(self.t["embed"]), lm_head=_ptr(self.t["lm_head"]),
+                                    final_norm=_ptr(self.t["final_norm"]),
+                                    layers=ctypes.cast(self._layers, ctypes.POINTER(DparaLayerWeights)))
+
+
 class DeviceContext:
     """Per-layer context K/V cache (K [L,B,n_kv,cap,hd], V transposed [L,B,n_kv,hd,cap]) + lengths."""
 
@@ -222,9 +284,9 @@ class DeviceContext:
 
 
 class Workspace:
-    def __init__(self, cfg: DparaConfig, batch: int, ctx_cap: int, device="cuda"):
+    def __init__(self, cfg: DparaConfig, batch: int, ctx_cap: int, device="cuda", target: bool = False):
         import torch
-        self.nbytes = dpara_workspace_bytes(cfg, batch, ctx_cap)
+        self.nbytes = (dpara_target_workspace_bytes if target else dpara_workspace_bytes)(cfg, batch, ctx_cap)
         if self.nbytes == 0:
             raise DparaError(DPARA_E_INVALID, "invalid configuration for workspace sizing")
         self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
@@ -262,3 +324,11 @@ def select_and_head(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts,
     dpara_select_and_head(d.cfg, d.w, int(accept_len.shape[0]), _ptr(reps), _ptr(accept_len), _ptr(bonus),
                           _ptr(gathered), _ptr(drafts), _ptr(next_spine), _ptr(margins), ws.ptr, ws.nbytes,
                           _stream(stream))
+
+
+def target_forward(t: DeviceTarget, ctx: DeviceContext, block, logits, ws: Workspace, stream=None):
+    """block [B, gamma+1] int32, logits [B, gamma+1, V] (bf16 or float32) on device."""
+    import torch
+    ldt = DPARA_BF16 if logits.dtype == torch.bfloat16 else DPARA_F32
+    dpara_target_forward(t.cfg, t.w, ctx.c, int(block.shape[0]), _ptr(block), _ptr(logits), ldt, ws.ptr,
+                         ws.nbytes, _stream(stream))

@@ -81,3 +81,15 @@ class DeviceRound:
     def status(self) -> int:
         torch.cuda.synchronize()
         return self.ws.status()
+
+
+def upload_cache(ctx, k, v, ctx_lens, dtype):
+    """Write host K/V (k[l][b], v[l][b]: [n_b, n_kv, hd]) into a DeviceContext and set ctx_len."""
+    for l in range(len(k)):
+        for b, n in enumerate(ctx_lens):
+            n = int(n)
+            if n == 0:
+                continue
+            ctx.k[l, b, :, :n, :] = torch.from_numpy(k[l][b]).to(dtype=dtype).permute(1, 0, 2).cuda()
+            ctx.v[l, b, :, :, :n] = torch.from_numpy(v[l][b]).to(dtype=dtype).permute(1, 2, 0).cuda()
+    ctx.ctx_len[:len(ctx_lens)] = torch.tensor(np.asarray(ctx_lens, np.int32)).cuda()

@@ -72,6 +72,9 @@ TINY = DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=
                     vocab=1024, gamma=4, ar_rank=256, qk_norm=False, dtype="f32")
 QWEN3_8B = DrafterShape(n_layers=5, hidden=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
                         ffn=12288, vocab=151936, gamma=16, ar_rank=256, qk_norm=True, dtype="bf16")
+# The 36-layer Qwen3-8B-shaped target used for the single-GPU full round (timing only).
+QWEN3_8B_TARGET = DrafterShape(n_layers=36, hidden=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                               ffn=12288, vocab=151936, gamma=16, ar_rank=256, qk_norm=True, dtype="bf16")
 QWEN3_14B = DrafterShape(n_layers=5, hidden=5120, n_q_heads=40, n_kv_heads=8, head_dim=128,
                          ffn=17408, vocab=151936, gamma=16, ar_rank=256, qk_norm=True, dtype="bf16")
 
@@ -87,6 +90,10 @@ WORKLOADS = {
                              p_reject=0.2,
                              description="Qwen3-8B-shaped drafter, gamma=16, batch 16, ragged "
                                          "contexts U[512,4096]"),
+    "full_round": Workload("full_round", QWEN3_8B, batch=16, ctx_min=2048, ctx_max=2048, p_reject=0.2,
+                           description="full round on one GPU: 36-layer Qwen3-8B-shaped random target "
+                                       "verifying gamma=16 blocks at batch 16, contexts 2048, with the "
+                                       "5-layer drafter's backbone on a concurrent stream"),
     "qwen3_14b_b8": Workload("qwen3_14b_b8", QWEN3_14B, batch=8, ctx_min=8192, ctx_max=8192,
                              p_reject=0.2,
                              description="Qwen3-14B-shaped 5-layer bf16 drafter, gamma=16, "
@@ -192,6 +199,48 @@ def make_weights(s: DrafterShape, seed: int = 0, **kw) -> dict:
     specs = weight_specs(s, **kw)
     arrs = normal_tensors([(tid, shp, std, mean, rb) for _, tid, shp, std, mean, rb in specs], seed)
     return {name: a for (name, *_), a in zip(specs, arrs)}
+
+
+def make_target_weights(s: DrafterShape, seed: int = 100, **kw) -> dict:
+    """A random target of the same layer structure: drafter-style layer weights, token
+    embedding, final norm and an untied LM head `lm_head` [V, H] (N(0, weight_std))."""
+    w = make_weights(s, seed=seed, **kw)
+    for k in ("mask_emb", "ar_E", "ar_W"):
+        w.pop(k)
+    std = kw.get("weight_std", 0.02)
+    (lm,) = normal_tensors([(6, (s.vocab, s.hidden), std, 0.0, s.dtype == "bf16")], seed)
+    w["lm_head"] = lm
+    return w
+
+
+def make_target_cache(s: DrafterShape, ctx_lens, seed: int = 101):
+    """The target's own per-layer context K/V: k[l][b], v[l][b] of shape [n_b, n_kv, hd],
+    N(0, 1) (bf16-valued in bf16 mode)."""
+    bf = s.dtype == "bf16"
+    specs, keys = [], []
+    for l in range(s.n_layers):
+        for b, n in enumerate(ctx_lens):
+            for kind in (0, 1):
+                specs.append((5000 + 64 * l + 2 * b + kind, (int(n), s.n_kv_heads, s.head_dim), 1.0, 0.0, bf))
+                keys.append((l, b, kind))
+    arrs = normal_tensors(specs, seed)
+    k = [[None] * len(ctx_lens) for _ in range(s.n_layers)]
+    v = [[None] * len(ctx_lens) for _ in range(s.n_layers)]
+    for (l, b, kind), a in zip(keys, arrs):
+        (k if kind == 0 else v)[l][b] = a
+    return k, v
+
+
+def device_normal_(t, seed: int, std: float = 1.0):
+    """Fill a device tensor in place with seeded N(0, std) draws (device generator; used for
+    the large timing-only target, which has no oracle)."""
+    import torch
+    g = torch.Generator(device=t.device)
+    g.manual_seed(int(seed))
+    tmp = torch.empty(t.shape, dtype=torch.float32, device=t.device)
+    tmp.normal_(0.0, std, generator=g)
+    t.copy_(tmp)
+    return t
 
 
 # ----------------------------------------------------------------------------

@@ -262,3 +262,82 @@ def test_full_size_qwen3_8b_b16():
     ri = synth.make_round(wl)
     samples = [(b, [int(ri.accept_planted[b])]) for b in (0, 7, 15)]
     _full_size("qwen3_8b_b16", samples)
+
+
+# ----------------------------------------------------------------------------- target verification forward
+TARGET_SMALL = synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=512,
+                                  vocab=3001, gamma=5, ar_rank=64, qk_norm=True, dtype="bf16")
+
+
+def _target_setup(ctx_lens, cap=256, seed=7):
+    from paper_2609_27396_amd import dpara as D
+    from paper_2609_27396_amd.harness import upload_cache
+    s = TARGET_SMALL
+    w = synth.make_target_weights(s, seed=seed, gain_jitter=0.1)
+    k, v = synth.make_target_cache(s, ctx_lens, seed=seed + 1)
+    block = np.random.default_rng(seed).integers(0, s.vocab, (len(ctx_lens), s.gamma + 1)).astype(np.int32)
+    t = D.DeviceTarget(s, w)
+    ctx = D.DeviceContext(s, len(ctx_lens), cap)
+    upload_cache(ctx, k, v, ctx_lens, torch.bfloat16)
+    ws = D.Workspace(t.cfg, len(ctx_lens), cap, target=True)
+    return s, w, k, v, block, t, ctx, ws
+
+
+def test_target_forward_parity():
+    from paper_2609_27396_amd import dpara as D
+    ctx_lens = [0, 50, 200]
+    _say("case target forward: 2 layers, 256 wide, block 6, contexts", ctx_lens)
+    s, w, k, v, block, t, ctx, ws = _target_setup(ctx_lens)
+    blk = torch.from_numpy(block).cuda()
+    lf = torch.empty((len(ctx_lens), s.gamma + 1, s.vocab), dtype=torch.float32, device="cuda")
+    lb = torch.empty_like(lf, dtype=torch.bfloat16)
+    D.target_forward(t, ctx, blk, lf, ws)
+    D.target_forward(t, ctx, blk, lb, ws)
+    torch.cuda.synchronize()
+    errs, skipped = [], 0
+    for b, n in enumerate(ctx_lens):
+        ref = O.target_forward(s, w, [k[l][b] for l in range(s.n_layers)], [v[l][b] for l in range(s.n_layers)],
+                               block[b], "bf16")
+        got = lf[b].cpu().numpy()
+        errs.append(np.abs(got - ref))
+        for j in range(s.gamma + 1):
+            y, m = O.argmax_margin(ref[j])
+            if m > MARGIN:
+                assert int(np.argmax(got[j])) == y
+            else:
+                skipped += 1
+    d = np.concatenate([e.ravel() for e in errs])
+    _say(f"target logits |gpu-oracle| max {d.max():.3e} median {np.median(d):.2e}, argmax rows skipped {skipped}")
+    assert d.max() <= TOL["bf16"]
+    # bf16 logits are the float32 logits rounded once
+    np.testing.assert_allclose(lb.float().cpu().numpy(), lf.cpu().numpy(), rtol=2 ** -8, atol=0)
+
+
+def test_backbone_and_target_on_concurrent_streams():
+    """The drafter backbone and the target forward on two streams at once give the same bits as run alone."""
+    from paper_2609_27396_amd import dpara as D
+    DeviceRound = _harness()
+    shape, _ = SMALL_CASES["h256_hd128_g5"]
+    wl = synth.Workload("cc", shape, batch=3, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=13)
+    wd = synth.make_weights(shape, seed=14)
+    ri = synth.make_round(wl, ctx_lens=[40, 0, 170])
+    dr = DeviceRound(shape, wd, ri)
+    s, w, k, v, block, t, ctx, ws = _target_setup([10, 120, 33], seed=21)
+    blk = torch.from_numpy(block).cuda()
+    l1 = torch.empty((3, s.gamma + 1, s.vocab), dtype=torch.bfloat16, device="cuda")
+    l2 = torch.empty_like(l1)
+    dr.backbone()
+    D.target_forward(t, ctx, blk, l1, ws)
+    torch.cuda.synchronize()
+    reps1 = dr.reps.clone()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for _ in range(3):
+        dr.reps.zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            dr.backbone(stream=s1)
+        with torch.cuda.stream(s2):
+            D.target_forward(t, ctx, blk, l2, ws, stream=s2)
+        torch.cuda.synchronize()
+        assert torch.equal(reps1, dr.reps)
+        assert torch.equal(l1, l2)

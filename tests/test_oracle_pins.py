@@ -397,3 +397,39 @@ def test_round_invariants():
     assert out["next_spine"][0] == out["bonus"]
     assert out["n_ctx_next"] == ri.ctx_lens[0] + out["r"] + 1
     assert out["reps"].shape == (wl.shape.gamma + 1, wl.shape.gamma, wl.shape.hidden)
+
+
+# ----------------------------------------------------------------------------
+# target verification forward vs the transformers Qwen3 causal LM
+# ----------------------------------------------------------------------------
+def test_target_forward_matches_hf_causal_lm_with_cache():
+    from transformers import Qwen3Config, Qwen3ForCausalLM
+    s = synth.shrink(SMALL, n_layers=2, vocab=113)
+    w = synth.make_weights(s, seed=61, gain_jitter=0.1)
+    w["lm_head"] = (_rng(62).standard_normal((s.vocab, s.hidden)) * 0.05).astype(np.float32)
+    cfg = Qwen3Config(hidden_size=s.hidden, intermediate_size=s.ffn, num_attention_heads=s.n_q_heads,
+                      num_key_value_heads=s.n_kv_heads, head_dim=s.head_dim, rms_norm_eps=s.rms_eps,
+                      rope_theta=s.rope_base, num_hidden_layers=s.n_layers, vocab_size=s.vocab,
+                      tie_word_embeddings=False)
+    cfg._attn_implementation = "eager"
+    model = Qwen3ForCausalLM(cfg).double().eval()
+    sd = {"model.embed_tokens.weight": w["embed"], "model.norm.weight": w["final_norm"], "lm_head.weight": w["lm_head"]}
+    names = {"self_attn.q_proj": "wq", "self_attn.k_proj": "wk", "self_attn.v_proj": "wv",
+             "self_attn.o_proj": "wo", "self_attn.q_norm": "q_norm", "self_attn.k_norm": "k_norm",
+             "mlp.gate_proj": "w_gate", "mlp.up_proj": "w_up", "mlp.down_proj": "w_down",
+             "input_layernorm": "attn_norm", "post_attention_layernorm": "mlp_norm"}
+    for l in range(s.n_layers):
+        for hf, ours in names.items():
+            sd[f"model.layers.{l}.{hf}.weight"] = w[f"L{l}.{ours}"]
+    model.load_state_dict({k: torch.from_numpy(np.asarray(v, np.float64)) for k, v in sd.items()})
+    r = _rng(63)
+    prefix = r.integers(0, s.vocab, 9)
+    block = r.integers(0, s.vocab, s.gamma + 1)
+    with torch.no_grad():
+        full = model(torch.from_numpy(np.concatenate([prefix, block]))[None], use_cache=False).logits[0]
+        out = model(torch.from_numpy(prefix)[None], use_cache=True)
+        cache = out.past_key_values
+        ks = [cache.layers[l].keys[0].permute(1, 0, 2).numpy() for l in range(s.n_layers)]
+        vs = [cache.layers[l].values[0].permute(1, 0, 2).numpy() for l in range(s.n_layers)]
+    got = O.target_forward(s, w, ks, vs, block, "exact")
+    np.testing.assert_allclose(got, full[len(prefix):].numpy(), rtol=2e-5, atol=2e-5)
