@@ -39,6 +39,20 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Block-wide sum for any block of NW waves.  `red` must hold NW floats.
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) t += red[i];
+  return t;
+}
+
 // Block-wide sum for blockDim.x == 256 (4 waves).  `red` must hold 4 floats.
 __device__ __forceinline__ float block_sum256(float v, float* red) {
   v = wave_sum(v);

@@ -108,8 +108,9 @@ int check_ctx(const dpara_ctx_t* x, int batch) {
 // Workspace layout (byte offsets), shared by all calls.
 struct Plan {
   int B, R, M, S, chunk, CH, esz;
+  int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   int v_chunk, v_chunks, h_chunk, h_chunks;
-  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, rope, vpart, G, Gsplit, logits, hpart, counters, F, KV32;
+  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, counters, F, KV32;
   size_t total;
 };
 
@@ -141,6 +142,10 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.v_chunks = (c->vocab + p.v_chunk - 1) / p.v_chunk;
   p.h_chunk = 256;
   p.h_chunks = (c->vocab + p.h_chunk - 1) / p.h_chunk;
+  const int amode = c->dtype == DPARA_BF16 ? A_BF16 : A_F32;
+  p.s_qkv = gemm_splits(amode, EPI_STORE_F32, p.M, (nq + 2 * nkv) * hd, H);
+  p.s_o = gemm_splits(amode, EPI_STORE_F32, p.M, H, nq * hd);
+  p.s_down = gemm_splits(amode, EPI_STORE_F32, p.M, H, c->ffn);
   const size_t M = p.M;
   size_t off = 256;  // status header
   auto take = [&](size_t bytes) {
@@ -150,7 +155,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   };
   p.X = take(M * H * 4);
   p.A = take(M * H * p.esz);
-  p.QKV = take(M * (size_t)(nq + 2 * nkv) * hd * 4);
+  p.QKV = take((size_t)p.s_qkv * M * (nq + 2 * nkv) * hd * 4);
   p.Q = take(M * (size_t)nq * hd * p.esz);
   p.Kb = take(M * (size_t)nkv * hd * p.esz);
   p.Vb = take(M * (size_t)nkv * hd * p.esz);
@@ -158,6 +163,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.ML = take((size_t)B * nq * p.R * p.S * 2 * 4);
   p.O = take(M * (size_t)nq * hd * p.esz);
   p.Hmid = take(M * (size_t)c->ffn * p.esz);
+  p.P = take((size_t)(p.s_o > p.s_down ? p.s_o : p.s_down) * M * H * 4);  // O / down partial planes
   p.rope = take((size_t)B * (2 * c->gamma + 1) * (hd / 2) * 8);
   p.vpart = take((size_t)B * (c->gamma + 1) * p.v_chunks * 8);
   p.G = take((size_t)B * c->gamma * H * 4);
@@ -166,7 +172,9 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.hpart = take((size_t)2 * B * p.h_chunks * 16);  // two step-parity slots
   p.counters = take((size_t)B * 4);
   p.F = take((size_t)B * p.CH * H * p.esz);
-  p.KV32 = take((size_t)B * p.CH * 2 * nkv * hd * 4);
+  // append K|V planes: split only when the append GEMM has at most 320 rows (16 planes max)
+  const size_t kv_rows = (size_t)B * p.CH > 16 * 320 ? (size_t)B * p.CH : 16 * 320;
+  p.KV32 = take(kv_rows * 2 * nkv * hd * 4);
   p.total = off;
   return p;
 }
@@ -241,7 +249,7 @@ namespace {
 // Leaves the residual stream in ws[p.X].
 int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, const void* embed,
                 const void* mask_emb, const dpara_ctx_t* ctx, int32_t batch, const int32_t* tokens,
-                int spine_only, const Plan& p, void* ws, hipStream_t st) {
+                int spine_only, const Plan& p, void* ws, hipStream_t st, int* pending) {
   const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q_heads, nkv = cfg->n_kv_heads;
   const int g = cfg->gamma, R = p.R, M = p.M, F = cfg->ffn;
   const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
@@ -256,11 +264,16 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
   HIP_TRY(launch_rope_table(batch, 2 * g + 1, hd, cfg->rope_base, ctx->ctx_len, 0, at<float2>(ws, p.rope), st),
           "rope_table");
   }
+  float* P = at<float>(ws, p.P);
+  int pend = 0;  // split-K planes of the last O / down projection not yet added into X
   for (int l = 0; l < cfg->n_layers; ++l) {
     const dpara_layer_weights_t& Lw = layers[l];
     {
     Phase ph("rmsnorm", st);
-    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.attn_norm, cfg->rms_eps, at<void>(ws, p.A), st), "attn_norm");
+    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, P, pend, (int64_t)M * H, 1, Lw.attn_norm, cfg->rms_eps,
+                           at<void>(ws, p.A), st),
+            "attn_norm");
+    pend = 0;
     }
     GemmArgs q{};
     q.A = at<void>(ws, p.A);
@@ -275,6 +288,7 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     q.K = H;
     q.C = at<void>(ws, p.QKV);
     q.ldc = q.N;
+    q.splits = p.s_qkv;
     {
     Phase ph("qkv_gemm", st);
     HIP_TRY(launch_gemm(amode, EPI_STORE_F32, q, st), "qkv gemm");
@@ -282,7 +296,7 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     {
     Phase ph("qk_norm_rope", st);
     HIP_TRY(launch_qk_norm_rope(dt, batch, R, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
-                                Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
+                                p.s_qkv, Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
                                 at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
             "qk_norm_rope");
     }
@@ -315,15 +329,18 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     o.M = M;
     o.N = H;
     o.K = nq * hd;
-    o.C = X;
+    o.C = P;
     o.ldc = H;
+    o.splits = p.s_o;
     {
     Phase ph("o_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, o, st), "o-proj gemm");
+    HIP_TRY(launch_gemm(amode, EPI_STORE_F32, o, st), "o-proj gemm");
     }
     {
     Phase ph("rmsnorm", st);
-    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, Lw.mlp_norm, cfg->rms_eps, at<void>(ws, p.A), st), "mlp_norm");
+    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, P, p.s_o, (int64_t)M * H, 1, Lw.mlp_norm, cfg->rms_eps,
+                           at<void>(ws, p.A), st),
+            "mlp_norm");
     }
     GemmArgs gu{};
     gu.A = at<void>(ws, p.A);
@@ -349,13 +366,16 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     dn.M = M;
     dn.N = H;
     dn.K = F;
-    dn.C = X;
+    dn.C = P;
     dn.ldc = H;
+    dn.splits = p.s_down;
     {
     Phase ph("down_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_ADD_F32, dn, st), "down gemm");
+    HIP_TRY(launch_gemm(amode, EPI_STORE_F32, dn, st), "down gemm");
     }
+    pend = p.s_down;
   }
+  *pending = pend;
   return DPARA_OK;
 }
 
@@ -451,6 +471,7 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
       g.K = H;
       g.C = at<void>(ws, p.KV32);
       g.ldc = g.N;
+      g.splits = gemm_splits(dt == DPARA_BF16 ? A_BF16 : A_F32, EPI_STORE_F32, g.M, g.N, g.K);
       {
         Phase ph("append_gemm", st);
         HIP_TRY(launch_gemm(dt == DPARA_BF16 ? A_BF16 : A_F32, EPI_STORE_F32, g, st), "append kv gemm");
@@ -459,7 +480,7 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
       char* vc = (char*)ctx->v + l * layer_elems * esz;
       Phase ph("append_store", st);
       HIP_TRY(launch_kv_store(dt, batch, CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps, cfg->rope_base,
-                              at<float>(ws, p.KV32), w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
+                              at<float>(ws, p.KV32), g.splits, w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
                               vc, status, st),
               "kv_store");
     }
@@ -482,13 +503,15 @@ int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights
   if ((rc = check_ws(p, ws, ws_bytes))) return rc;
   if ((rc = check_device())) return rc;
   hipStream_t st = (hipStream_t)stream;
-  if ((rc = run_decoder(cfg, w->layers, w->embed, w->mask_emb, ctx, batch, spine, 0, p, ws, st))) return rc;
-  // reps[b][r][i-1] = final norm of mask rows: input row (m / nmask) * R + (g + 1 + m % nmask)
+  int pend = 0;
+  if ((rc = run_decoder(cfg, w->layers, w->embed, w->mask_emb, ctx, batch, spine, 0, p, ws, st, &pend))) return rc;
+  // reps[b][r][i-1] = final norm of mask rows: input row (m / nmask) * R + (g + 1 + m % nmask), with the
+  // last down projection's split-K planes added
   const int g = cfg->gamma, R = p.R, H = cfg->hidden;
   const int nmask = R - g - 1;
   Phase ph("final_norm", st);
-  HIP_TRY(launch_rmsnorm(0, batch * nmask, H, at<float>(ws, p.X), nmask, (int64_t)R * H, g + 1, w->final_norm,
-                         cfg->rms_eps, reps, st),
+  HIP_TRY(launch_rmsnorm(0, batch * nmask, H, at<float>(ws, p.X), nmask, (int64_t)R * H, g + 1, at<float>(ws, p.P),
+                         pend, (int64_t)p.M * H, 0, w->final_norm, cfg->rms_eps, reps, st),
           "final_norm");
   return DPARA_OK;
 }
@@ -530,12 +553,13 @@ int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t
   if ((rc = check_ws(p, ws, ws_bytes))) return rc;
   if ((rc = check_device())) return rc;
   hipStream_t st = (hipStream_t)stream;
-  if ((rc = run_decoder(&c, w->layers, w->embed, w->embed, ctx, batch, block, 1, p, ws, st))) return rc;
+  int pend = 0;
+  if ((rc = run_decoder(&c, w->layers, w->embed, w->embed, ctx, batch, block, 1, p, ws, st, &pend))) return rc;
   const int H = c.hidden, M = p.M;
   {
     Phase ph("final_norm", st);
-    HIP_TRY(launch_rmsnorm(DPARA_BF16, M, H, at<float>(ws, p.X), M, 0, 0, w->final_norm, c.rms_eps,
-                           at<void>(ws, p.A), st),
+    HIP_TRY(launch_rmsnorm(DPARA_BF16, M, H, at<float>(ws, p.X), M, 0, 0, at<float>(ws, p.P), pend, (int64_t)M * H,
+                           0, w->final_norm, c.rms_eps, at<void>(ws, p.A), st),
             "target final norm");
   }
   GemmArgs lm{};

@@ -34,27 +34,49 @@ __global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, in
   for (int i = threadIdx.x; i < H; i += 256) dst[i] = ld_f(src + i);
 }
 
+// One block (16 waves) per output row.  x = X row + the S pending split-K partial planes of
+// that row (summed in plane order); optionally x is written back into X; y = x / rms(x) * g.
+constexpr int kNormThreads = 1024;
 template <typename TO>
-__global__ __launch_bounds__(256) void rmsnorm_rows(int H, const float* X, int grp, int64_t in_stride,
-                                                    int in_off, const float* g, float eps, TO* Y) {
-  __shared__ float red[4];
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, int grp, int64_t in_stride,
+                                                             int in_off, const float* P, int S, int64_t pstride,
+                                                             int write_back, const float* g, float eps, TO* Y) {
+  __shared__ float red[kNormThreads / 64];
   const int m = blockIdx.x;
-  const float* x = X + (int64_t)(m / grp) * in_stride + (int64_t)(in_off + m % grp) * H;
+  const int64_t roff = (int64_t)(m / grp) * in_stride + (int64_t)(in_off + m % grp) * H;
+  float* x = X + roff;
+  float4 v[2];  // H <= 8192: up to 2 float4 per thread
   float ss = 0.f;
-  for (int i = threadIdx.x * 4; i < H; i += 1024) {
-    const float4 v = *(const float4*)(x + i);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int i = (threadIdx.x + kNormThreads * t) * 4;
+    if (i < H) {
+      float4 a = *(const float4*)(x + i);
+      for (int sp = 0; sp < S; ++sp) {
+        const float4 b = *(const float4*)(P + sp * pstride + roff + i);
+        a.x += b.x;
+        a.y += b.y;
+        a.z += b.z;
+        a.w += b.w;
+      }
+      if (write_back && S > 0) *(float4*)(x + i) = a;
+      v[t] = a;
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+    }
   }
-  ss = block_sum256(ss, red);
+  ss = block_sum<kNormThreads / 64>(ss, red);
   const float r = 1.0f / sqrtf(ss / (float)H + eps);
   TO* y = Y + (int64_t)m * H;
-  for (int i = threadIdx.x * 4; i < H; i += 1024) {
-    const float4 v = *(const float4*)(x + i);
-    const float4 gg = *(const float4*)(g + i);
-    st_f(y + i + 0, v.x * r * gg.x);
-    st_f(y + i + 1, v.y * r * gg.y);
-    st_f(y + i + 2, v.z * r * gg.z);
-    st_f(y + i + 3, v.w * r * gg.w);
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int i = (threadIdx.x + kNormThreads * t) * 4;
+    if (i < H) {
+      const float4 gg = *(const float4*)(g + i);
+      st_f(y + i + 0, v[t].x * r * gg.x);
+      st_f(y + i + 1, v[t].y * r * gg.y);
+      st_f(y + i + 2, v[t].z * r * gg.z);
+      st_f(y + i + 3, v[t].w * r * gg.w);
+    }
   }
 }
 
@@ -70,25 +92,34 @@ __global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx
   table[((int64_t)b * n_pos + i) * half + p] = make_float2(c, s);
 }
 
-// One block per row; waves loop over head slots (q heads, k heads, v heads).
+// Grid (head-slot groups of 4, rows): one wave per (row, head slot); the slots are the q heads,
+// then the k heads, then the v heads of the fused QKV row, summed over the S split-K planes.
 template <typename T>
 __global__ __launch_bounds__(256) void qk_norm_rope(int R, int gamma, int n_q, int n_kv, int hd, int qk_norm,
-                                                    float eps, const float* QKV, const float* qn,
+                                                    float eps, const float* QKV, int S, int64_t pstride,
+                                                    const float* qn,
                                                     const float* kn, const float2* table, T* Q, T* Kb,
                                                     T* Vb) {
-  const int m = blockIdx.x;
+  const int m = blockIdx.y;
   const int b = m / R, row = m % R;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = hd / 2, grp = n_q / n_kv;
   const int n_slots = n_q + 2 * n_kv;
   const float* src = QKV + (int64_t)m * n_slots * hd;
   const float2* cs = table + ((int64_t)b * (2 * gamma + 1) + row_pos_offset(row, gamma)) * half;
-  for (int slot = wave; slot < n_slots; slot += 4) {
+  {
+    const int slot = blockIdx.x * 4 + wave;  // one wave per head slot (q heads, k heads, v heads)
+    if (slot >= n_slots) return;
     const float* x = src + slot * hd;
     if (slot < n_q + n_kv) {
       const bool isq = slot < n_q;
       const bool act = lane < half;
-      float x1 = act ? x[lane] : 0.f, x2 = act ? x[lane + half] : 0.f;
+      float x1 = 0.f, x2 = 0.f;
+      if (act)
+        for (int sp = 0; sp < S; ++sp) {
+          x1 += x[sp * pstride + lane];
+          x2 += x[sp * pstride + lane + half];
+        }
       if (qk_norm) {
         const float ss = wave_sum(x1 * x1 + x2 * x2);
         const float r = 1.0f / sqrtf(ss / (float)hd + eps);
@@ -116,7 +147,11 @@ __global__ __launch_bounds__(256) void qk_norm_rope(int R, int gamma, int n_q, i
     } else {
       const int kvh = slot - n_q - n_kv;
       T* dst = Vb + ((int64_t)(b * n_kv + kvh) * R + row) * hd;
-      for (int d = lane; d < hd; d += 64) st_f(dst + d, x[d]);
+      for (int d = lane; d < hd; d += 64) {
+        float acc = 0.f;
+        for (int sp = 0; sp < S; ++sp) acc += x[sp * pstride + d];
+        st_f(dst + d, acc);
+      }
     }
   }
 }
@@ -140,10 +175,11 @@ __device__ __forceinline__ int clamp_count(int n, int n_max) { return n < 0 ? 0 
 // [pos][hd], V to the transposed cache [hd][pos].
 template <typename T>
 __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n_kv, int hd, int qk_norm, float eps,
-                                                double base, const float* KV, const float* kn,
+                                                double base, const float* KV, int S, int64_t pstride,
+                                                const float* kn,
                                                 const int* n_new, const int* ctx_len, int cap, T* Kc,
                                                 T* Vc) {
-  const int m = blockIdx.x, b = m / CH, i = m % CH;
+  const int m = blockIdx.y, b = m / CH, i = m % CH;
   const int c = c0 + i;
   if (c >= clamp_count(n_new[b], n_max)) return;
   const int pos = max(ctx_len[b], 0) + c;
@@ -151,10 +187,17 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = hd / 2;
   const float* src = KV + (int64_t)m * 2 * n_kv * hd;
-  for (int kvh = wave; kvh < n_kv; kvh += 4) {
+  {
+    const int kvh = blockIdx.x * 4 + wave;  // one wave per (row, kv head)
+    if (kvh >= n_kv) return;
     const float* x = src + kvh * hd;
     const bool act = lane < half;
-    float x1 = act ? x[lane] : 0.f, x2 = act ? x[lane + half] : 0.f;
+    float x1 = 0.f, x2 = 0.f;
+    if (act)
+      for (int sp = 0; sp < S; ++sp) {
+        x1 += x[sp * pstride + lane];
+        x2 += x[sp * pstride + lane + half];
+      }
     if (qk_norm) {
       const float ss = wave_sum(x1 * x1 + x2 * x2);
       const float r = 1.0f / sqrtf(ss / (float)hd + eps);
@@ -172,7 +215,11 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
       st_f(kd + lane + half, x2 * cc + x1 * ss);
     }
     const float* xv = src + (n_kv + kvh) * hd;
-    for (int d = lane; d < hd; d += 64) st_f(Vc + (kvb * hd + d) * cap + pos, xv[d]);
+    for (int d = lane; d < hd; d += 64) {
+      float acc = 0.f;
+      for (int sp = 0; sp < S; ++sp) acc += xv[sp * pstride + d];
+      st_f(Vc + (kvb * hd + d) * cap + pos, acc);
+    }
   }
 }
 
@@ -207,15 +254,17 @@ hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(int out_dtype, int rows, int H, const float* X, int grp, int64_t in_stride,
-                          int in_off, const float* g, float eps, void* Y, hipStream_t st) {
+hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int64_t in_stride, int in_off,
+                          const float* P, int S, int64_t pstride, int write_back, const float* g, float eps,
+                          void* Y, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
+  if (H > 8 * kNormThreads || H % 4) return hipErrorInvalidValue;
   if (out_dtype == 1)
-    hipLaunchKernelGGL(rmsnorm_rows<bf16_t>, dim3(rows), dim3(256), 0, st, H, X, grp, in_stride, in_off, g,
-                       eps, (bf16_t*)Y);
+    hipLaunchKernelGGL(rmsnorm_rows<bf16_t>, dim3(rows), dim3(kNormThreads), 0, st, H, X, grp, in_stride, in_off, P, S,
+                       pstride, write_back, g, eps, (bf16_t*)Y);
   else
-    hipLaunchKernelGGL(rmsnorm_rows<float>, dim3(rows), dim3(256), 0, st, H, X, grp, in_stride, in_off, g,
-                       eps, (float*)Y);
+    hipLaunchKernelGGL(rmsnorm_rows<float>, dim3(rows), dim3(kNormThreads), 0, st, H, X, grp, in_stride, in_off, P, S,
+                       pstride, write_back, g, eps, (float*)Y);
   return hipGetLastError();
 }
 
@@ -229,15 +278,16 @@ hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ct
 }
 
 hipError_t launch_qk_norm_rope(int dtype, int B, int R, int gamma, int n_q, int n_kv, int hd, int qk_norm,
-                               float eps, const float* QKV, const float* qn, const float* kn,
+                               float eps, const float* QKV, int S, const float* qn, const float* kn,
                                const float2* table, void* Q, void* Kb, void* Vb, hipStream_t st) {
-  dim3 grid(B * R);
+  dim3 grid((n_q + 2 * n_kv + 3) / 4, B * R);
+  const int64_t pstride = (int64_t)B * R * (n_q + 2 * n_kv) * hd;
   if (dtype == 1)
     hipLaunchKernelGGL(qk_norm_rope<bf16_t>, grid, dim3(256), 0, st, R, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
-                       qn, kn, table, (bf16_t*)Q, (bf16_t*)Kb, (bf16_t*)Vb);
+                       S, pstride, qn, kn, table, (bf16_t*)Q, (bf16_t*)Kb, (bf16_t*)Vb);
   else
     hipLaunchKernelGGL(qk_norm_rope<float>, grid, dim3(256), 0, st, R, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
-                       qn, kn, table, (float*)Q, (float*)Kb, (float*)Vb);
+                       S, pstride, qn, kn, table, (float*)Q, (float*)Kb, (float*)Vb);
   return hipGetLastError();
 }
 
@@ -253,15 +303,17 @@ hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int 
 }
 
 hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd, int qk_norm,
-                           float eps, float base, const float* KV, const float* kn, const int* n_new,
+                           float eps, float base, const float* KV, int S, const float* kn, const int* n_new,
                            const int* ctx_len, int cap, void* Kc, void* Vc, int* status, hipStream_t st) {
   (void)status;
+  const int64_t pstride = (int64_t)B * CH * 2 * n_kv * hd;
+  const dim3 grid((n_kv + 3) / 4, B * CH);
   if (dtype == 1)
-    hipLaunchKernelGGL(kv_store<bf16_t>, dim3(B * CH), dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
-                       (double)base, KV, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc);
+    hipLaunchKernelGGL(kv_store<bf16_t>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
+                       (double)base, KV, S, pstride, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc);
   else
-    hipLaunchKernelGGL(kv_store<float>, dim3(B * CH), dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
-                       (double)base, KV, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc);
+    hipLaunchKernelGGL(kv_store<float>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
+                       (double)base, KV, S, pstride, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc);
   return hipGetLastError();
 }
 

@@ -102,8 +102,13 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
   constexpr int STAGE_BYTES = (A_ROWS + BN) * BKB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
+  // Split-K: the S splits of one output tile are consecutive logical workgroups; split s
+  // covers K range [s*K/S, (s+1)*K/S) and stores into plane s of C.
+  const int S = a.splits;
   int mt, nt;
-  tile_of(blockIdx.x, MT, NT, mt, nt);
+  tile_of(blockIdx.x / S, MT, NT, mt, nt);
+  const int split = blockIdx.x % S;
+  const int Ks = a.K / S, kbeg = split * Ks;
   const int m0 = mt * BM;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WNW, wn = wave % WNW;
@@ -118,13 +123,13 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     const int r = (wave + NW * j) * RPI + lrow;   // stage row
     const int plane = r >= BM ? 1 : 0;
     const int gm = min(m0 + r - plane * BM, a.M - 1);
-    asrc[j] = (const bf16_t*)a.A + (plane ? a.lo_off : 0) + (int64_t)gm * a.lda + swz<CH>(r, lslot) * 8;
+    asrc[j] = (const bf16_t*)a.A + (plane ? a.lo_off : 0) + (int64_t)gm * a.lda + kbeg + swz<CH>(r, lslot) * 8;
   }
 #pragma unroll
   for (int j = 0; j < B_INS; ++j) {
     const int r = (wave + NW * j) * RPI + lrow;
     bool ok;
-    bsrc[j] = b_row<bf16_t, BN, EPI>(a, nt, r, ok) + swz<CH>(r, lslot) * 8;
+    bsrc[j] = b_row<bf16_t, BN, EPI>(a, nt, r, ok) + kbeg + swz<CH>(r, lslot) * 8;
   }
   auto issue = [&](int kt, int stage) {
     unsigned char* sb = smem + stage * STAGE_BYTES;
@@ -144,7 +149,7 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = a.K / KB;
+  const int KT = Ks / KB;
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < KT) issue(st, st);
@@ -200,7 +205,7 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
           if (col < a.N) C[col] = f2bf(acc[mi][ni][r]);
         }
       } else {
-        float* C = (float*)a.C + (int64_t)row * a.ldc;
+        float* C = (float*)a.C + ((int64_t)split * a.M + row) * a.ldc;
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni) {
           const int col = nt * BN + wn * WN + ni * 16 + lr;
@@ -441,31 +446,46 @@ hipError_t run_pipe(const GemmArgs& a, hipStream_t st) {
   const int MT = (a.M + BM - 1) / BM;
   const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
   constexpr int lds = STAGES * ((DUAL ? 2 : 1) * BM + BN) * BKB;
+  static_assert(lds <= 163840, "LDS ring exceeds 160 KB");
   auto kern = gemm_pipe_kernel<BM, BN, WMW, WNW, STAGES, BKB, EPI, DUAL>;
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(kern, dim3(MT * NT), dim3(64 * WMW * WNW), lds, st, a, MT, NT);
+  // planes are float32 [S][M][ldc]: only the float32 store epilogue may split K
+  if (a.splits < 1 || (a.splits > 1 && EPI != EPI_STORE_F32) || a.K % (a.splits * (BKB / 2)) != 0)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kern, dim3(MT * NT * a.splits), dim3(64 * WMW * WNW), lds, st, a, MT, NT);
   return hipGetLastError();
 }
 
-// Tile choice for the bf16 projections (measured on MI355X, Qwen3-8B-sized N/K):
-//  M <= 512 : weight streaming; 32x128 tiles, 4-deep ring (QKV, O, down), and a full-M
-//             320x128 tile with 8 waves for the SwiGLU GEMM when M <= 320;
+// Tile choice for the bf16 projections (measured on MI355X at Qwen3-8B N/K):
+//  M <= 320 : weight streaming.  One 320-row tile covers every row, so each weight tile is
+//             read once; 8 waves (80x64 each), a 2-deep ring of 64-wide K steps.  The
+//             fp32-store GEMMs (QKV, O, down, append) split K so that about 256 workgroups
+//             run; their consumers add the S partial planes (gemm_splits).
 //  M <= 1024: 64x128 tiles, 3-deep ring;
-//  larger   : 256x256 tiles, 8 waves (128x64 per wave), 2-deep ring of 64-wide K steps.
+//  larger   : 256x256 tiles, 8 waves (128x64 per wave), 2-deep ring.
 template <int EPI>
 hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
   if (a.M > 1024) return run_pipe<256, 256, 2, 4, 2, 128, EPI>(a, st);
-  if (a.M > 512) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
-  if (EPI == EPI_SWIGLU && a.M > 64 && a.M <= 320) return run_pipe<320, 128, 4, 2, 2, 128, EPI>(a, st);
-  return run_pipe<32, 128, 1, 4, 4, 128, EPI>(a, st);
+  if (a.M > 320) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
+  return run_pipe<320, 128, 4, 2, 2, 128, EPI>(a, st);
 }
 
 }  // namespace
 
+int gemm_splits(int amode, int epi, int M, int N, int K) {
+  if (amode != A_BF16 || epi != EPI_STORE_F32 || M > 320) return 1;
+  const int NT = (N + 127) / 128;
+  int S = 1;
+  while (S < 16 && NT * S * 2 <= 256 && K % (64 * S * 2) == 0 && K / (S * 2) >= 256) S *= 2;
+  return S;
+}
+
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.splits < 1) return hipErrorInvalidValue;
+  if (a.splits > 1 && amode != A_BF16) return hipErrorInvalidValue;
   if (amode == A_F32) {
     switch (epi) {
       case EPI_STORE_F32: return run_f32<EPI_STORE_F32>(a, st);

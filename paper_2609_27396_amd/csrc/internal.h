@@ -40,11 +40,15 @@ struct GemmArgs {
   void* C;
   int64_t ldc;
   int64_t lo_off;  // A_BF16_DUAL only
+  int splits = 1;  // split-K: S >= 1 fp32 planes of C (plane stride M*ldc); EPI_STORE_F32 only
   // EPI_SWIGLU: B0 = gate [N, K], B1 = up [N, K], C = bf16/f32 [M, N] of silu(g) * u,
   // where N is the FFN width.
 };
 
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st);
+// Split-K factor launch_gemm uses for a bf16 fp32-store GEMM of this shape (1 = no split).
+// The consumer of C sums the S planes in order 0..S-1.
+int gemm_splits(int amode, int epi, int M, int N, int K);
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
@@ -68,20 +72,24 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st);
 hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V,
                                 const int* spine, const void* embed, const void* mask_emb,
                                 float* X, int* status, hipStream_t st);
-// Y[m] = rmsnorm(X[in_row(m)]) * g, in_row(m) = (m / grp) * in_stride + in_off + m % grp
-hipError_t launch_rmsnorm(int out_dtype, int rows, int H, const float* X, int grp,
-                          int64_t in_stride, int in_off, const float* g, float eps, void* Y,
-                          hipStream_t st);
+// Y[m] = rmsnorm(x) * g with x = X[in_row(m)] + sum_{s<S} P[s][in_row(m)] (P planes share
+// X's layout, plane stride pstride floats), in_row(m) = (m / grp) * in_stride + in_off + m % grp.
+// write_back: also store x into X (folds the pending partial sums into the residual stream).
+hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int64_t in_stride,
+                          int in_off, const float* P, int S, int64_t pstride, int write_back,
+                          const float* g, float eps, void* Y, hipStream_t st);
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len,
                              int pos_off, float2* table, hipStream_t st);
+// QKV: S fp32 planes [S][B*R][(n_q+2n_kv)*hd], summed in order.
 hipError_t launch_qk_norm_rope(int dtype, int B, int R, int gamma, int n_q, int n_kv, int hd,
-                               int qk_norm, float eps, const float* QKV, const float* qn,
+                               int qk_norm, float eps, const float* QKV, int S, const float* qn,
                                const float* kn, const float2* table, void* Q, void* Kb,
                                void* Vb, hipStream_t st);
 hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int H,
                                const void* feats, void* F, hipStream_t st);
+// KV: S fp32 planes [S][B*CH][2*n_kv*hd], summed in order.
 hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd,
-                           int qk_norm, float eps, float base, const float* KV,
+                           int qk_norm, float eps, float base, const float* KV, int S,
                            const float* kn, const int* n_new, const int* ctx_len, int cap,
                            void* Kc, void* Vc, int* status, hipStream_t st);
 hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, int* ctx_len,
