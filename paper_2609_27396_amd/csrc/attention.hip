@@ -1,20 +1,27 @@
 // Multi-boundary attention of the all-boundary backbone (tree mask of Section 3.2).
 //
-// Every block row (spine or mask) of a request sees the whole cached context, so the
-// context part is plain dense attention shared by all (gamma+1)^2 rows and all query
-// heads of a KV group.  It runs as an MFMA flash-attention pass over context chunks:
-// one workgroup per (request, KV head, 64 query rows, context chunk) stages the chunk's
-// K (keys x head_dim) and V^T (head_dim x keys, the cache stores V transposed) in LDS
-// and computes S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_16x16x32_bf16, keeping an
-// online softmax in log2 units.  P enters the PV product as a bf16 hi + lo pair (two
-// MFMAs), so the probabilities keep ~16 significant bits: a single bf16 rounding of P
-// moves the result by about one bf16 ulp of the hidden state, which is as large as the
-// whole error budget.  Each chunk emits an unnormalised partial (O, m, l).
+// Each request's (gamma+1)^2 block rows see the whole cached context plus, under the tree
+// mask, some of the block's own keys: spine t_j sees t_0..t_j, branch r's mask rows see
+// t_0..t_r and all of branch r's masks.  For one request and KV head the keys therefore
+// form one virtual sequence: ceil(L/64) blocks of context followed by ceil(R/64) blocks of
+// in-block keys (dense, masked per element).  Workgroups split that sequence evenly.
 //
-// The merge kernel (one wave per row and query head) folds the context partials and
-// then walks the row's in-block keys under the tree mask -- spine t_j sees t_0..t_j,
-// branch r's masks see t_0..t_r and the branch's own masks -- and writes O.
+// bf16 path (attn_mfma): one workgroup = 4 waves x 32 query rows (all query heads of the
+// KV group share the keys) over a contiguous range of 64-key blocks.  K (keys x head_dim)
+// and V^T (head_dim x keys; both the cache and the in-block values are stored transposed)
+// are staged through a double-buffered, XOR-swizzled LDS ring: the next block's global
+// loads are issued into registers before the current block's MFMAs, so their latency
+// hides behind the math.  S^T = K Q^T and O^T += V^T P^T use v_mfma_f32_16x16x32_bf16
+// with an online softmax in log2 units.  The K operand rows are permuted so that each
+// lane's probabilities form 8 consecutive keys, which makes every V^T operand one
+// 16-byte LDS read.  P enters the PV product as a bf16 hi + lo pair (two MFMAs), so the
+// probabilities keep ~16 significant bits: a single bf16 rounding of P moves the result
+// by about one bf16 ulp of the hidden state, which is as large as the whole error budget.
+// With one workgroup per row tile (S == 1) the kernel normalises and writes O itself;
+// otherwise each writes an unnormalised partial (O, m, l) and attn_fold combines them.
 #include <math.h>
+
+#include <type_traits>
 
 #include "common.h"
 #include "internal.h"
@@ -23,157 +30,344 @@ namespace dpara {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+#ifndef DPARA_ATTN_WAVES
+#define DPARA_ATTN_WAVES 8
+#endif
+#ifndef DPARA_ATTN_TILES
+#define DPARA_ATTN_TILES 1
+#endif
+#ifndef DPARA_ATTN_STAGES
+#define DPARA_ATTN_STAGES 2
+#endif
+constexpr int kKeyBlock = 64;
+constexpr int kAttnWaves = DPARA_ATTN_WAVES;   // waves per workgroup
+constexpr int kAttnTiles = DPARA_ATTN_TILES;   // 16-row query tiles per wave
+constexpr int kAttnStages = DPARA_ATTN_STAGES; // LDS ring depth
+constexpr int kRowsPerWG = kAttnWaves * kAttnTiles * 16;
 
+// LDS swizzles (16-byte chunk index within a row).  K rows hold head_dim entries; a K
+// operand read has 16 lanes on rows whose index bits 0,1,3,4 vary (bit 2 fixed), V^T
+// rows hold 64 keys (128 bytes) and a read has 16 lanes on 16 consecutive rows.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_ctx_mfma(AttnArgs a) {
-  constexpr int KB = 64;          // keys per staged block
-  constexpr int LDKS = HD + 8;    // K tile row stride (bf16)
-  constexpr int LDV = KB + 8;     // V^T tile row stride (bf16)
-  constexpr int NKS = HD / 32;    // k-steps over head_dim for S
-  constexpr int NHB = HD / 16;    // 16-row blocks of head_dim for O^T
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[KB * LDKS];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[HD * LDV];
+__device__ __forceinline__ int k_swz(int r, int c) {
+  if constexpr (HD == 128) return c ^ ((r & 3) | ((r >> 1) & 12));
+  else return c ^ (((r >> 1) & 1) | ((r >> 2) & 6));
+}
+__device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+// Key offset within a 64-key block held by S^T row i of 16-key MFMA block kb.
+__device__ __forceinline__ int key_perm(int kb, int i) { return (kb >> 1) * 32 + (i >> 2) * 8 + (kb & 1) * 4 + (i & 3); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14];
+  // expcnt and lgkmcnt are left at their maxima (no wait on them).
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | (((N >> 4) & 3) << 14));
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+__device__ __forceinline__ uint4 as_u4(bf16x8_t v) { return __builtin_bit_cast(uint4, v); }
+
+// The K and V^T tiles of a 64-key block are filled by direct global->LDS DMA
+// (global_load_lds_dwordx4: lane i's 16 bytes land at M0 + 16*i), through a ring of
+// STAGES stages: STAGES-1 blocks are in flight while one is consumed.  Every load is a
+// full 16-byte chunk: the context cache and the in-block buffers hold a multiple of 64
+// keys, so a block never reads past its buffer; keys past the valid count are excluded
+// from the scores by the mask, and their V^T entries are zeroed in the operand (a tail
+// block only) so that stale memory cannot turn 0 * V into NaN.
+//
+// Workgroup = NW waves x U 16-row query tiles per wave.  Fragment reads: the K operand
+// row of MFMA block kb for lane lq is key_perm(kb, lq), whose swizzle depends on lq only
+// (kb moves bits 2 and 5 of the row, which the swizzle ignores), and the V^T operand row
+// hb*16 + lq likewise swizzles by lq only; so each read is a per-lane base plus a
+// compile-time offset.
+template <int HD, int NW, int U, int STAGES>
+__global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
+  constexpr int NKS = HD / 32;                 // k-steps over head_dim for S
+  constexpr int NHB = HD / 16;                 // 16-row blocks of head_dim for O^T
+  constexpr int K_BYTES = kKeyBlock * HD * 2;  // K tile
+  constexpr int STAGE_BYTES = 2 * K_BYTES;     // K tile + V^T tile (same size)
+  constexpr int NINS = K_BYTES / 1024 / NW;    // DMA instructions per wave per tile
+  constexpr int ROWS_WG = NW * U * 16;
+  static_assert(NINS * 1024 * NW == K_BYTES, "tile must split evenly over the waves");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int b = blockIdx.z / a.n_kv, kvh = blockIdx.z % a.n_kv;
   const int grp = a.n_q / a.n_kv;
   const int nrows = grp * a.R;
   const int L = min(max(a.ctx_len[b], 0), a.cap);
-  const int k_begin = blockIdx.y * a.chunk;
-  if (k_begin >= L) return;
-  const int k_end = min(L, k_begin + a.chunk);
+  const int nb_ctx = (L + kKeyBlock - 1) / kKeyBlock;
+  const int nb = nb_ctx + (a.R + kKeyBlock - 1) / kKeyBlock;
+  const int per = (nb + a.S - 1) / a.S;
+  const int vb_begin = min(nb, (int)blockIdx.y * per);
+  const int n_blk = min(nb, vb_begin + per) - vb_begin;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 15, g4 = lane >> 4;
-  const int qi = blockIdx.x * 64 + wave * 16 + lq;
-
-  // Q^T fragments (B operand): Q[qi][ks*32 + g4*8 + 0..7]
-  const bf16_t* Qp = (const bf16_t*)a.Q + (int64_t)(b * a.n_kv + kvh) * nrows * HD;
-  bf16x8_t qf[NKS];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    if (qi < nrows) qf[ks] = *(const bf16x8_t*)(Qp + (int64_t)qi * HD + ks * 32 + g4 * 8);
-    else qf[ks] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-  }
-
-  f32x4_t o[NHB];
-#pragma unroll
-  for (int hb = 0; hb < NHB; ++hb) o[hb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
-  const float sc = kLog2e / sqrtf((float)HD);
+  const int qrow0 = blockIdx.x * ROWS_WG + wave * U * 16;
+  const bool wave_live = qrow0 < nrows;
 
   const int64_t kvbase = (int64_t)(b * a.n_kv + kvh);
   const bf16_t* Kg = (const bf16_t*)a.Kc + kvbase * a.cap * HD;
   const bf16_t* Vg = (const bf16_t*)a.Vc + kvbase * HD * a.cap;
-
-  for (int kb0 = k_begin; kb0 < k_end; kb0 += KB) {
-    __syncthreads();
-    for (int c = threadIdx.x; c < KB * HD / 8; c += 256) {
-      const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
-      const int key = kb0 + kr;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (key < k_end) v = *(const uint4*)(Kg + (int64_t)key * HD + kc);
-      *(uint4*)&Ks[kr * LDKS + kc] = v;
+  const bf16_t* Kin = (const bf16_t*)a.Kb + kvbase * a.Rp * HD;
+  const bf16_t* Vin = (const bf16_t*)a.Vb + kvbase * HD * a.Rp;
+  auto issue = [&](int vb, int stage) {
+    const bool inblk = vb >= nb_ctx;
+    const int kb0 = (inblk ? vb - nb_ctx : vb) * kKeyBlock;
+    const bf16_t* Ks = (inblk ? Kin : Kg) + (int64_t)kb0 * HD;
+    const bf16_t* Vs = (inblk ? Vin : Vg) + kb0;
+    const int vstride = inblk ? a.Rp : a.cap;
+    unsigned char* sb = smem + stage * STAGE_BYTES;
+    // instruction j of this wave fills tile chunks (wave + NW*j)*64 + lane of K and of V^T
+#pragma unroll
+    for (int j = 0; j < NINS; ++j) {
+      const int idx = (wave + NW * j) * 64 + lane;
+      const int r = idx / (HD / 8), c = idx % (HD / 8);
+      __builtin_amdgcn_global_load_lds((const void*)(Ks + r * HD + k_swz<HD>(r, c) * 8),
+                                       (lds_void_t*)(sb + (wave + NW * j) * 1024), 16, 0, 0);
     }
-    for (int c = threadIdx.x; c < HD * KB / 8; c += 256) {
-      const int d = c / (KB / 8), kc = (c % (KB / 8)) * 8;
-      const int key = kb0 + kc;
-      const bf16_t* src = Vg + (int64_t)d * a.cap + key;
-      uint4 v;
-      if (key + 8 <= k_end) {
-        v = *(const uint4*)src;
-      } else {
-        bf16_t t[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) t[j] = (key + j < k_end) ? src[j] : (bf16_t)0;
-        v = make_uint4(t[0] | ((uint32_t)t[1] << 16), t[2] | ((uint32_t)t[3] << 16),
-                       t[4] | ((uint32_t)t[5] << 16), t[6] | ((uint32_t)t[7] << 16));
-      }
-      *(uint4*)&Vs[d * LDV + kc] = v;
+    for (int j = 0; j < NINS; ++j) {
+      const int idx = (wave + NW * j) * 64 + lane;
+      const int d = idx / (kKeyBlock / 8), c = idx % (kKeyBlock / 8);
+      __builtin_amdgcn_global_load_lds((const void*)(Vs + d * vstride + v_swz(d, c) * 8),
+                                       (lds_void_t*)(sb + K_BYTES + (wave + NW * j) * 1024), 16, 0, 0);
     }
-    __syncthreads();
+  };
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < n_blk) issue(vb_begin + st, st);
 
-    // S^T block: s[kb][r] = score(key = kb0 + kb*16 + g4*4 + r, query qi)
-    f32x4_t s[4];
+  // Query fragments (B operand of S^T = K Q^T) and the tree-mask intervals of each row:
+  // an in-block key j is visible iff j < e1 or lo2 <= j < lo2 + span.
+  const bf16_t* Qp = (const bf16_t*)a.Q + kvbase * nrows * HD;
+  bf16x8_t qf[U][NKS];
+  int qi[U], e1[U], lo2[U], span[U];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      s[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int u = 0; u < U; ++u) {
+    qi[u] = qrow0 + u * 16 + lq;
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const bf16x8_t kf = *(const bf16x8_t*)&Ks[(kb * 16 + lq) * LDKS + ks * 32 + g4 * 8];
-        s[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[kb], 0, 0, 0);
+    for (int ks = 0; ks < NKS; ++ks)
+      qf[u][ks] = qi[u] < nrows ? *(const bf16x8_t*)(Qp + (int64_t)qi[u] * HD + ks * 32 + g4 * 8)
+                                : bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    const int row = qi[u] % a.R, g = a.gamma;
+    if (a.spine_only || row <= g) {
+      e1[u] = row + 1;
+      lo2[u] = span[u] = 0;
+    } else {
+      const int br = (row - g - 1) / g;
+      e1[u] = br + 1;
+      lo2[u] = g + 1 + br * g;
+      span[u] = g;
+    }
+  }
+  // per-lane LDS byte offsets of the fragment reads within a stage
+  const int kx = k_swz<HD>(key_perm(0, lq), 0);
+  const int k_lane = key_perm(0, lq) * HD * 2;
+  const int v_lane = lq * kKeyBlock * 2;
+  const int vx = v_swz(lq, 0);
+
+  f32x4_t o[U][NHB];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb) o[u][hb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[U], l_run[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    m_run[u] = -INFINITY;
+    l_run[u] = 0.f;
+  }
+  const float sc = kLog2e / sqrtf((float)HD);
+
+  for (int i = 0; i < n_blk; ++i) {
+    if (i + STAGES - 2 < n_blk) wait_vmcnt<(STAGES - 2) * 2 * NINS>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (i + STAGES - 1 < n_blk) issue(vb_begin + i + STAGES - 1, (i + STAGES - 1) % STAGES);
+    if (!wave_live) continue;
+
+    const unsigned char* sb = smem + (i % STAGES) * STAGE_BYTES;
+    const int vb = vb_begin + i;
+    const bool inblk = vb >= nb_ctx;
+    const int kb0 = (inblk ? vb - nb_ctx : vb) * kKeyBlock;
+    const int kend = inblk ? a.R : L;
+
+    // S^T blocks: s[u][kb][r] = score(key kb0 + key_perm(kb, 4*g4 + r), query qi[u])
+    f32x4_t s[U][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) s[u][kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const unsigned char* kp = sb + k_lane + ((ks * 4 + g4) ^ kx) * 16;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const bf16x8_t kf = *(const bf16x8_t*)(kp + key_perm(kb, 0) * HD * 2);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          s[u][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[u][ks], s[u][kb], 0, 0, 0);
       }
     }
-    float mx = -INFINITY;
+    // Blocks of context keys that are all valid need no mask (all but the last one);
+    // in-block blocks and the context tail mask per element and zero V^T past kend.
+    if (inblk || kb0 + kKeyBlock > kend) {
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+      for (int u = 0; u < U; ++u) {
+        const int lim1 = inblk ? e1[u] : L, lo = inblk ? lo2[u] : 0, sp = inblk ? span[u] : 0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = kb0 + kb * 16 + g4 * 4 + r;
-        const float v = key < k_end ? s[kb][r] * sc : -INFINITY;
-        s[kb][r] = v;
-        mx = fmaxf(mx, v);
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = kb0 + key_perm(kb, 4 * g4 + r);
+            const bool vis = (key < lim1) | ((unsigned)(key - lo) < (unsigned)sp);
+            s[u][kb][r] = vis ? s[u][kb][r] : -INFINITY;
+          }
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float m_new = fmaxf(m_run, mx);  // finite: key kb0 < k_end is in this block
-    const float alpha = exp2f(m_run - m_new);
-    float psum = 0.f;
-    bf16_t pb[4][4], pl[4][4];  // p = hi + lo, both bf16 (16 significant bits of p)
+    }
+    bf16x8_t pf[U][2], pfl[U][2];  // [u][t]: p = hi + lo, both bf16
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+    for (int u = 0; u < U; ++u) {
+      float mx = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(s[kb][r] - m_new);
-        psum += p;
-        pb[kb][r] = f2bf(p);
-        pl[kb][r] = f2bf(p - bf2f(pb[kb][r]));
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[u][kb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float m_new = fmaxf(m_run[u], mx * sc);          // running max, log2 units
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;  // row sees no key yet
+      float psum = 0.f;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        uint32_t hw[4], lw[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // slot j of k-step t holds key t*32 + g4*8 + j: kb = 2t + j/4, r = j%4
+          const int kb = 2 * t + (q >> 1), r = 2 * (q & 1);
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[u][kb][r], sc, -m_use));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[u][kb][r + 1], sc, -m_use));
+          psum += p0 + p1;
+          bf16x2_t h;
+          h[0] = (__bf16)p0;
+          h[1] = (__bf16)p1;
+          hw[q] = __builtin_bit_cast(uint32_t, h);
+          bf16x2_t l;
+          l[0] = (__bf16)(p0 - __uint_as_float(hw[q] << 16));
+          l[1] = (__bf16)(p1 - __uint_as_float(hw[q] & 0xFFFF0000u));
+          lw[q] = __builtin_bit_cast(uint32_t, l);
+        }
+        pf[u][t] = as_bf16x8(make_uint4(hw[0], hw[1], hw[2], hw[3]));
+        pfl[u][t] = as_bf16x8(make_uint4(lw[0], lw[1], lw[2], lw[3]));
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+      // o is rescaled only when some row of the wave raised its max (alpha == 1 else)
+      const float alpha = __builtin_amdgcn_exp2f(m_run[u] - m_use);
+      l_run[u] = l_run[u] * alpha + psum;
+      if (__any(m_new > m_run[u])) {
 #pragma unroll
-    for (int hb = 0; hb < NHB; ++hb) o[hb] *= alpha;
+        for (int hb = 0; hb < NHB; ++hb) o[u][hb] *= alpha;
+      }
+      m_run[u] = m_new;
+    }
+    // O^T += V^T P^T over 64 keys = 2 k-steps of 32.
+    auto pv = [&](auto zero_tail) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const unsigned char* vp = sb + K_BYTES + v_lane + ((t * 4 + g4) ^ vx) * 16;
+#pragma unroll
+        for (int hb = 0; hb < NHB; ++hb) {
+          bf16x8_t vf = *(const bf16x8_t*)(vp + hb * 16 * kKeyBlock * 2);
+          if constexpr (decltype(zero_tail)::value) {  // zero V^T entries of keys >= kend
+            const int nv = kend - (kb0 + t * 32 + g4 * 8);
+            uint4 x = as_u4(vf);
+            x.x &= (0 < nv ? 0xFFFFu : 0u) | (1 < nv ? 0xFFFF0000u : 0u);
+            x.y &= (2 < nv ? 0xFFFFu : 0u) | (3 < nv ? 0xFFFF0000u : 0u);
+            x.z &= (4 < nv ? 0xFFFFu : 0u) | (5 < nv ? 0xFFFF0000u : 0u);
+            x.w &= (6 < nv ? 0xFFFFu : 0u) | (7 < nv ? 0xFFFF0000u : 0u);
+            vf = as_bf16x8(x);
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][t], o[u][hb], 0, 0, 0);
+            o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[u][t], o[u][hb], 0, 0, 0);
+          }
+        }
+      }
+    };
+    if (kb0 + kKeyBlock > kend) pv(std::true_type{});
+    else pv(std::false_type{});
+  }
 
-    // O^T += V^T P^T over 64 keys = 2 k-steps of 32.  Lane (g4) slot j of k-step t holds
-    // key t*32 + g4*4 + j (j < 4) or t*32 + 16 + g4*4 + (j-4): the same key set is used
-    // for the V^T operand, so the contraction pairs matching keys.
-    // P enters as hi + lo so the product keeps ~16 bits of p (V is exact in bf16).
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      bf16x8_t pf, pfl;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        pf[j] = __builtin_bit_cast(__bf16, pb[2 * t][j]);
-        pf[j + 4] = __builtin_bit_cast(__bf16, pb[2 * t + 1][j]);
-        pfl[j] = __builtin_bit_cast(__bf16, pl[2 * t][j]);
-        pfl[j + 4] = __builtin_bit_cast(__bf16, pl[2 * t + 1][j]);
-      }
+  for (int u = 0; u < U; ++u) {
+    float l_tot = l_run[u] + __shfl_xor(l_run[u], 16, kWave);
+    l_tot += __shfl_xor(l_tot, 32, kWave);
+    if (qi[u] >= nrows) continue;
+    const int gi = qi[u] / a.R, row = qi[u] % a.R;
+    const int h = kvh * grp + gi;
+    if (a.S == 1) {
+      const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+      bf16_t* op = (bf16_t*)a.O + (int64_t)(b * a.R + row) * (a.n_q * HD) + h * HD;
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb) {
-        const bf16_t* vr = &Vs[(hb * 16 + lq) * LDV + t * 32 + g4 * 4];
-        const uint2 lo = *(const uint2*)vr;
-        const uint2 hi = *(const uint2*)(vr + 16);
-        const uint4 packed = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, packed);
-        o[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[hb], 0, 0, 0);
-        o[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl, o[hb], 0, 0, 0);
+        const uint32_t w0 = f2bf(o[u][hb][0] * inv) | ((uint32_t)f2bf(o[u][hb][1] * inv) << 16);
+        const uint32_t w1 = f2bf(o[u][hb][2] * inv) | ((uint32_t)f2bf(o[u][hb][3] * inv) << 16);
+        *(uint2*)(op + hb * 16 + g4 * 4) = make_uint2(w0, w1);
+      }
+    } else {
+      const int64_t base = ((int64_t)(b * a.n_q + h) * a.R + row) * a.S + blockIdx.y;
+      if (l_tot > 0.f) {
+        float* op = a.Opart + base * HD;
+#pragma unroll
+        for (int hb = 0; hb < NHB; ++hb)
+          *(float4*)(op + hb * 16 + g4 * 4) = make_float4(o[u][hb][0], o[u][hb][1], o[u][hb][2], o[u][hb][3]);
+      }
+      if (g4 == 0) {
+        a.MLpart[base * 2] = m_run[u];
+        a.MLpart[base * 2 + 1] = l_tot;
       }
     }
   }
+}
 
-  float l_tot = l_run + __shfl_xor(l_run, 16, kWave);
-  l_tot += __shfl_xor(l_tot, 32, kWave);
-  if (qi < nrows) {
-    const int gi = qi / a.R, row = qi % a.R;
-    const int h = kvh * grp + gi;
-    const int64_t base = ((int64_t)(b * a.n_q + h) * a.R + row) * a.S + blockIdx.y;
-    float* op = a.Opart + base * HD;
-#pragma unroll
-    for (int hb = 0; hb < NHB; ++hb)
-      *(float4*)(op + hb * 16 + g4 * 4) = make_float4(o[hb][0], o[hb][1], o[hb][2], o[hb][3]);
-    if (g4 == 0) {
-      a.MLpart[base * 2] = m_run;
-      a.MLpart[base * 2 + 1] = l_tot;
-    }
+// Folds the S partials of one (request, head, row): 4 head_dim entries per thread.
+// Partials with l == 0 saw no key and are skipped (their O was not written).
+template <int HD>
+__global__ __launch_bounds__(256) void attn_fold(AttnArgs a) {
+  constexpr int TPR = HD / 4;  // threads per (request, head, row)
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t task = t / TPR;
+  if (task >= (int64_t)a.B * a.n_q * a.R) return;
+  const int c = (int)(t % TPR);
+  const int row = (int)(task % a.R);
+  const int bh = (int)(task / a.R), h = bh % a.n_q, b = bh / a.n_q;
+  const int64_t pbase = task * a.S;
+  float M = -INFINITY;
+  for (int s = 0; s < a.S; ++s)
+    if (a.MLpart[(pbase + s) * 2 + 1] > 0.f) M = fmaxf(M, a.MLpart[(pbase + s) * 2]);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float Ls = 0.f;
+  for (int s = 0; s < a.S; ++s) {
+    const float ls = a.MLpart[(pbase + s) * 2 + 1];
+    if (!(ls > 0.f)) continue;
+    const float w = exp2f(a.MLpart[(pbase + s) * 2] - M);
+    Ls += ls * w;
+    const float4 v = *(const float4*)(a.Opart + (pbase + s) * HD + c * 4);
+    acc.x += v.x * w;
+    acc.y += v.y * w;
+    acc.z += v.z * w;
+    acc.w += v.w * w;
   }
+  const float inv = Ls > 0.f ? 1.0f / Ls : 0.f;
+  bf16_t* op = (bf16_t*)a.O + (int64_t)(b * a.R + row) * (a.n_q * HD) + h * HD + c * 4;
+  const uint32_t w0 = f2bf(acc.x * inv) | ((uint32_t)f2bf(acc.y * inv) << 16);
+  const uint32_t w1 = f2bf(acc.z * inv) | ((uint32_t)f2bf(acc.w * inv) << 16);
+  *(uint2*)op = make_uint2(w0, w1);
 }
 
 // Scalar context pass (float32 model path; any dtype): one wave per (request, head,
@@ -222,6 +416,8 @@ __global__ __launch_bounds__(256) void attn_ctx_scalar(AttnArgs a) {
   }
 }
 
+// float32 path, second pass: one wave per (request, head, row) takes the context partial,
+// then walks the row's in-block keys under the tree mask and writes the normalised O.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   constexpr int PER = HD / 64;
@@ -259,9 +455,8 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
     branch = (row - g - 1) / g;
     n_spine = branch + 1;
   }
-  const int64_t kb = (int64_t)(b * a.n_kv + kvh) * a.R;
-  const T* Kp = (const T*)a.Kb + kb * HD;
-  const T* Vp = (const T*)a.Vb + kb * HD;
+  const T* Kp = (const T*)a.Kb + (int64_t)(b * a.n_kv + kvh) * a.Rp * HD;  // [Rp][hd]
+  const T* Vp = (const T*)a.Vb + (int64_t)(b * a.n_kv + kvh) * HD * a.Rp;  // [hd][Rp]
   const float sc = kLog2e / sqrtf((float)HD);
   const int n_keys = n_spine + (branch >= 0 ? g : 0);
   for (int t = 0; t < n_keys; ++t) {
@@ -274,7 +469,7 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
     const float al = exp2f(M - mn), p = exp2f(d - mn);
     Ls = Ls * al + p;
 #pragma unroll
-    for (int c = 0; c < PER; ++c) o[c] = fmaf(p, ld_f(Vp + (int64_t)key * HD + lane + 64 * c), o[c] * al);
+    for (int c = 0; c < PER; ++c) o[c] = fmaf(p, ld_f(Vp + (int64_t)(lane + 64 * c) * a.Rp + key), o[c] * al);
     M = mn;
   }
   const float inv = 1.0f / Ls;
@@ -283,19 +478,39 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   for (int c = 0; c < PER; ++c) st_f(op + lane + 64 * c, o[c] * inv);
 }
 
+template <int HD>
+hipError_t run_attention_bf16(const AttnArgs& a, hipStream_t st) {
+  constexpr int STAGES = kAttnStages;
+  constexpr size_t lds = (size_t)STAGES * 2 * kKeyBlock * HD * 2;
+  static_assert(lds <= 163840, "attention LDS ring exceeds 160 KB");
+  if constexpr (lds > 65536) {
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void*)attn_mfma<HD, kAttnWaves, kAttnTiles, STAGES>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (attr != hipSuccess) return attr;
+  }
+  const int nrows = (a.n_q / a.n_kv) * a.R;
+  {
+    Phase ph("attn_ctx", st);
+    dim3 grid((nrows + kRowsPerWG - 1) / kRowsPerWG, a.S, a.B * a.n_kv);
+    hipLaunchKernelGGL((attn_mfma<HD, kAttnWaves, kAttnTiles, STAGES>), grid, dim3(64 * kAttnWaves), lds, st, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.S == 1) return e;
+  {
+    Phase ph("attn_merge", st);
+    const int64_t threads = (int64_t)a.B * a.n_q * a.R * (HD / 4);
+    hipLaunchKernelGGL((attn_fold<HD>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
 template <typename T, int HD>
-hipError_t run_attention(const AttnArgs& a, hipStream_t st, bool mfma) {
+hipError_t run_attention_scalar(const AttnArgs& a, hipStream_t st) {
   const int waves = a.B * a.n_q * a.R;
   const int blocks = (waves + 3) / 4;
   {
     Phase ph("attn_ctx", st);
-    if (mfma) {
-      const int nrows = (a.n_q / a.n_kv) * a.R;
-      dim3 grid((nrows + 63) / 64, a.S, a.B * a.n_kv);
-      hipLaunchKernelGGL((attn_ctx_mfma<HD>), grid, dim3(256), 0, st, a);
-    } else {
-      hipLaunchKernelGGL((attn_ctx_scalar<T, HD>), dim3(blocks), dim3(256), 0, st, a);
-    }
+    hipLaunchKernelGGL((attn_ctx_scalar<T, HD>), dim3(blocks), dim3(256), 0, st, a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -308,11 +523,13 @@ hipError_t run_attention(const AttnArgs& a, hipStream_t st, bool mfma) {
 
 }  // namespace
 
+int attn_rows_per_workgroup() { return kRowsPerWG; }
+
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
-  if (dtype == 1) {
-    return a.hd == 128 ? run_attention<bf16_t, 128>(a, st, true) : run_attention<bf16_t, 64>(a, st, true);
-  }
-  return a.hd == 128 ? run_attention<float, 128>(a, st, false) : run_attention<float, 64>(a, st, false);
+  if (a.Rp < a.R || a.Rp % kKeyBlock || a.S < 1) return hipErrorInvalidValue;
+  if (dtype == 1) return a.hd == 128 ? run_attention_bf16<128>(a, st) : run_attention_bf16<64>(a, st);
+  if (a.S != 1) return hipErrorInvalidValue;
+  return a.hd == 128 ? run_attention_scalar<float, 128>(a, st) : run_attention_scalar<float, 64>(a, st);
 }
 
 }  // namespace dpara

@@ -11,6 +11,10 @@
 #include "../../include/dpara.h"
 #include "internal.h"
 
+#ifndef DPARA_ATTN_TARGET_WG
+#define DPARA_ATTN_TARGET_WG 256
+#endif
+
 using namespace dpara;
 
 namespace {
@@ -107,7 +111,7 @@ int check_ctx(const dpara_ctx_t* x, int batch) {
 
 // Workspace layout (byte offsets), shared by all calls.
 struct Plan {
-  int B, R, M, S, chunk, CH, esz;
+  int B, R, Rp, M, S, chunk, CH, esz;
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, counters, F, KV32;
@@ -118,21 +122,25 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   Plan p{};
   p.B = B;
   p.R = R > 0 ? R : (c->gamma + 1) * (c->gamma + 1);
+  p.Rp = (p.R + 63) / 64 * 64;
   p.M = B * p.R;
   p.esz = c->dtype == DPARA_BF16 ? 2 : 4;
   const int hd = c->head_dim, nq = c->n_q_heads, nkv = c->n_kv_heads, H = c->hidden;
   const int grp = nq / nkv;
   if (c->dtype == DPARA_BF16) {
-    // split the context so that the MFMA pass launches a few hundred workgroups
-    const int base = B * nkv * ((grp * p.R + 63) / 64);
-    int S = (512 + base - 1) / base;
-    const int max_s = (ctx_cap + 255) / 256;
+    // Split each request's key blocks (context + in-block) over S workgroups so that the
+    // MFMA pass launches at most about DPARA_ATTN_TARGET_WG workgroups (one resident
+    // workgroup per CU), with at least 2 key blocks each; partial (O, m, l) traffic grows
+    // with S, so no more splits than that.
+    const int tiles = (grp * p.R + attn_rows_per_workgroup() - 1) / attn_rows_per_workgroup();
+    const int base = B * nkv * tiles;
+    const int max_blocks = (ctx_cap + 63) / 64 + p.Rp / 64;
+    int S = DPARA_ATTN_TARGET_WG / base;
+    const int max_s = max_blocks / 2;
     if (S > max_s) S = max_s;
     if (S < 1) S = 1;
-    int chunk = (ctx_cap + S - 1) / S;
-    chunk = (chunk + 63) / 64 * 64;
-    p.chunk = chunk;
-    p.S = (ctx_cap + chunk - 1) / chunk;
+    p.S = S;
+    p.chunk = 0;
   } else {
     p.S = 1;
     p.chunk = ctx_cap;
@@ -140,7 +148,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.CH = p.R;
   p.v_chunk = 4096;
   p.v_chunks = (c->vocab + p.v_chunk - 1) / p.v_chunk;
-  p.h_chunk = 256;
+  p.h_chunk = ar_head_chunk(c->dtype == DPARA_BF16 ? 1 : 0, c->ar_rank);
   p.h_chunks = (c->vocab + p.h_chunk - 1) / p.h_chunk;
   const int amode = c->dtype == DPARA_BF16 ? A_BF16 : A_F32;
   p.s_qkv = gemm_splits(amode, EPI_STORE_F32, p.M, (nq + 2 * nkv) * hd, H);
@@ -157,8 +165,8 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.A = take(M * H * p.esz);
   p.QKV = take((size_t)p.s_qkv * M * (nq + 2 * nkv) * hd * 4);
   p.Q = take(M * (size_t)nq * hd * p.esz);
-  p.Kb = take(M * (size_t)nkv * hd * p.esz);
-  p.Vb = take(M * (size_t)nkv * hd * p.esz);
+  p.Kb = take((size_t)B * nkv * p.Rp * hd * p.esz);  // [Rp][hd] per request and KV head
+  p.Vb = take((size_t)B * nkv * hd * p.Rp * p.esz);  // transposed [hd][Rp] per request and KV head
   p.Opart = take((size_t)B * nq * p.R * p.S * hd * 4);
   p.ML = take((size_t)B * nq * p.R * p.S * 2 * 4);
   p.O = take(M * (size_t)nq * hd * p.esz);
@@ -295,7 +303,7 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     }
     {
     Phase ph("qk_norm_rope", st);
-    HIP_TRY(launch_qk_norm_rope(dt, batch, R, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
+    HIP_TRY(launch_qk_norm_rope(dt, batch, R, p.Rp, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
                                 p.s_qkv, Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
                                 at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
             "qk_norm_rope");
@@ -310,6 +318,7 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     aa.Q = at<void>(ws, p.Q);
     aa.Kb = at<void>(ws, p.Kb);
     aa.Vb = at<void>(ws, p.Vb);
+    aa.Rp = p.Rp;
     aa.Kc = (const char*)ctx->k + l * layer_elems * p.esz;
     aa.Vc = (const char*)ctx->v + l * layer_elems * p.esz;
     aa.cap = ctx->ctx_cap;

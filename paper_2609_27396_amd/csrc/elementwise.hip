@@ -94,8 +94,10 @@ __global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx
 
 // Grid (head-slot groups of 4, rows): one wave per (row, head slot); the slots are the q heads,
 // then the k heads, then the v heads of the fused QKV row, summed over the S split-K planes.
+// In-block keys are stored [Rp][hd] and values transposed [hd][Rp] per request and KV head
+// (Rp = R rounded up to 64 keys) for the MFMA attention pass.
 template <typename T>
-__global__ __launch_bounds__(256) void qk_norm_rope(int R, int gamma, int n_q, int n_kv, int hd, int qk_norm,
+__global__ __launch_bounds__(256) void qk_norm_rope(int R, int Rp, int gamma, int n_q, int n_kv, int hd, int qk_norm,
                                                     float eps, const float* QKV, int S, int64_t pstride,
                                                     const float* qn,
                                                     const float* kn, const float2* table, T* Q, T* Kb,
@@ -139,18 +141,18 @@ __global__ __launch_bounds__(256) void qk_norm_rope(int R, int gamma, int n_q, i
           dst = Q + (((int64_t)(b * n_kv + kvh) * grp + gi) * R + row) * hd;
         } else {
           const int kvh = slot - n_q;
-          dst = Kb + ((int64_t)(b * n_kv + kvh) * R + row) * hd;
+          dst = Kb + ((int64_t)(b * n_kv + kvh) * Rp + row) * hd;
         }
         st_f(dst + lane, y1);
         st_f(dst + lane + half, y2);
       }
     } else {
       const int kvh = slot - n_q - n_kv;
-      T* dst = Vb + ((int64_t)(b * n_kv + kvh) * R + row) * hd;
+      T* dst = Vb + (int64_t)(b * n_kv + kvh) * hd * Rp + row;  // transposed: [hd][Rp]
       for (int d = lane; d < hd; d += 64) {
         float acc = 0.f;
         for (int sp = 0; sp < S; ++sp) acc += x[sp * pstride + d];
-        st_f(dst + d, acc);
+        st_f(dst + (int64_t)d * Rp, acc);
       }
     }
   }
@@ -277,16 +279,17 @@ hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ct
   return hipGetLastError();
 }
 
-hipError_t launch_qk_norm_rope(int dtype, int B, int R, int gamma, int n_q, int n_kv, int hd, int qk_norm,
+hipError_t launch_qk_norm_rope(int dtype, int B, int R, int Rp, int gamma, int n_q, int n_kv, int hd, int qk_norm,
                                float eps, const float* QKV, int S, const float* qn, const float* kn,
                                const float2* table, void* Q, void* Kb, void* Vb, hipStream_t st) {
+  if (Rp < R) return hipErrorInvalidValue;
   dim3 grid((n_q + 2 * n_kv + 3) / 4, B * R);
   const int64_t pstride = (int64_t)B * R * (n_q + 2 * n_kv) * hd;
   if (dtype == 1)
-    hipLaunchKernelGGL(qk_norm_rope<bf16_t>, grid, dim3(256), 0, st, R, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
+    hipLaunchKernelGGL(qk_norm_rope<bf16_t>, grid, dim3(256), 0, st, R, Rp, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
                        S, pstride, qn, kn, table, (bf16_t*)Q, (bf16_t*)Kb, (bf16_t*)Vb);
   else
-    hipLaunchKernelGGL(qk_norm_rope<float>, grid, dim3(256), 0, st, R, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
+    hipLaunchKernelGGL(qk_norm_rope<float>, grid, dim3(256), 0, st, R, Rp, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
                        S, pstride, qn, kn, table, (float*)Q, (float*)Kb, (float*)Vb);
   return hipGetLastError();
 }

@@ -54,19 +54,21 @@ int gemm_splits(int amode, int epi, int M, int N, int K);
 struct AttnArgs {
   int B, R, gamma, n_q, n_kv, hd;
   const void* Q;    // [B, n_kv, grp*R, hd] (row index g*R + row for query head kvh*grp + g)
-  const void* Kb;   // [B, n_kv, R, hd]     in-block keys
-  const void* Vb;   // [B, n_kv, R, hd]     in-block values
+  const void* Kb;   // [B, n_kv, Rp, hd]    in-block keys (rows R..Rp-1 unused)
+  const void* Vb;   // [B, n_kv, hd, Rp]    in-block values, transposed (row stride Rp)
+  int Rp;           // R rounded up to a multiple of 64
   const void* Kc;   // context K cache of this layer  [batch_cap, n_kv, cap, hd]
   const void* Vc;   // context V cache of this layer  [batch_cap, n_kv, hd, cap]
   int cap;
   const int* ctx_len;  // [B] device
-  int S, chunk;        // context split into S chunks of `chunk` positions
+  int S, chunk;        // bf16: keys split over S workgroups; float32: S == 1, chunk == cap
   float* Opart;        // [B, n_q, R, S, hd]
   float* MLpart;       // [B, n_q, R, S, 2]  (running max in log2 units, running sum)
   void* O;             // [B*R, n_q*hd]
   int spine_only;      // 1: rows are only the causal spine (no branches)
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st);
+int attn_rows_per_workgroup();  // query rows (over the heads of a KV group) per bf16 workgroup
 
 // ---------------------------------------------------------------- elementwise
 hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V,
@@ -81,7 +83,7 @@ hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len,
                              int pos_off, float2* table, hipStream_t st);
 // QKV: S fp32 planes [S][B*R][(n_q+2n_kv)*hd], summed in order.
-hipError_t launch_qk_norm_rope(int dtype, int B, int R, int gamma, int n_q, int n_kv, int hd,
+hipError_t launch_qk_norm_rope(int dtype, int B, int R, int Rp, int gamma, int n_q, int n_kv, int hd,
                                int qk_norm, float eps, const float* QKV, int S, const float* qn,
                                const float* kn, const float2* table, void* Q, void* Kb,
                                void* Vb, hipStream_t st);
@@ -104,6 +106,7 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
                                 const int* accept_len, float* G, float* G_out, bf16_t* Ghi,
                                 int* status, hipStream_t st);
+int ar_head_chunk(int dtype, int rank);  // vocabulary rows per AR-step workgroup
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits,
                           const void* E, const void* W, const int* bonus, int* drafts,
                           int* next_spine, float* margins, uint64_t* part, int n_chunks,

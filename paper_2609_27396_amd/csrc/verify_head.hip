@@ -9,7 +9,9 @@
 // head: y_0 = bonus; step i computes z_i = l_i + W E(y_{i-1}) over the vocabulary in
 // chunks (8 lanes per vocabulary row, E(y_{i-1}) staged in LDS) and keeps a per-chunk
 // top-2; the next step's workgroups reduce those partials to y_i and the top1 - top2
-// margin before starting (head equation of Section 3.2).
+// margin before starting (head equation of Section 3.2).  For ranks up to 512 (bf16) or
+// 256 (float32) the step prefetches its whole weight slice (ar_step_pf); wider ranks
+// walk the rows (ar_step).
 #include <math.h>
 
 #include "common.h"
@@ -109,6 +111,10 @@ __device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1
     v2 = fmaxf(fmaxf(v2, ov2), vb);
   }
 }
+
+// Rows per 8-lane group of the prefetching AR step for P 16-byte pieces per lane per row:
+// NR * P <= 32 pieces (128 VGPRs) in flight per lane.
+__host__ __device__ constexpr int ar_rows_per_group(int P) { return P <= 4 ? 8 : (P <= 8 ? 4 : 0); }
 
 template <typename T>
 __device__ __forceinline__ float dot_row8(const T* w, const float* e, int rank, int j);
@@ -241,6 +247,112 @@ __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int r
   }
 }
 
+// Prefetching form of ar_step for rows of P 16-byte pieces per lane (row bytes = 128 P):
+// each 8-lane group owns NR rows (grp + 32 i), and all of the workgroup's W rows and
+// logits are requested before the previous step's partials are reduced, so the weight
+// stream, the partial reduction and the E(y) fetch overlap instead of paying one memory
+// latency per row.  Rows past V read row V-1 and are discarded.  Same arithmetic order as
+// ar_step: per lane sequential over its pieces, then the 8-lane butterfly.
+template <typename T, int P>
+__global__ __launch_bounds__(256) void ar_step_pf(int step, int gamma, int V, int rank, const float* logits,
+                                                  const T* E, const T* W, const int* bonus, int* drafts,
+                                                  int* next_spine, float* margins, uint64_t* part,
+                                                  int n_chunks, int chunk, int B, int* status) {
+  constexpr int NR = ar_rows_per_group(P);
+  __shared__ __attribute__((aligned(16))) float e[1024];
+  __shared__ uint64_t rk[4];
+  __shared__ float rv[4];
+  const int c = blockIdx.x, b = blockIdx.y;
+  const int j = threadIdx.x & 7, grp = threadIdx.x >> 3;
+  const int v0 = c * chunk;
+  const size_t row_bytes = (size_t)rank * sizeof(T);
+
+  uint4 wv[NR][P];
+  float lg = -INFINITY;
+  if (step <= gamma) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const int v = min(v0 + grp + 32 * i, V - 1);
+      const unsigned char* row = (const unsigned char*)W + (size_t)v * row_bytes;
+#pragma unroll
+      for (int t = 0; t < P; ++t) wv[i][t] = *(const uint4*)(row + (t * 8 + j) * 16);
+    }
+    const int vl = v0 + grp + 32 * j;
+    if (j < NR && vl < V) lg = logits[((int64_t)b * gamma + step - 1) * V + vl];
+  }
+
+  int y_prev;
+  if (step == 1) {
+    y_prev = bonus[b];
+    if (y_prev < 0 || y_prev >= V) {
+      if (threadIdx.x == 0 && c == 0) raise_status(status, 1);
+      y_prev = 0;
+    }
+    if (threadIdx.x == 0 && c == 0) next_spine[b * (gamma + 1)] = y_prev;
+  } else {
+    const uint64_t* pp = part + ((int64_t)((step - 1) & 1) * B + b) * n_chunks * 2;
+    float m;
+    reduce_step(pp, n_chunks, rk, rv, &y_prev, &m);
+    if (threadIdx.x == 0 && c == 0) {
+      drafts[b * gamma + step - 2] = y_prev;
+      next_spine[b * (gamma + 1) + step - 1] = y_prev;
+      if (margins) margins[b * gamma + step - 2] = m;
+    }
+  }
+  if (step > gamma) return;
+  for (int k = threadIdx.x; k < rank; k += 256) e[k] = ld_f(E + (int64_t)y_prev * rank + k);
+  __syncthreads();
+
+  constexpr int EPP = 16 / sizeof(T);  // elements per 16-byte piece
+  float zmine = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    float d = 0.f;
+#pragma unroll
+    for (int t = 0; t < P; ++t) {
+      const float* ek = e + (t * 8 + j) * EPP;
+      const uint4 u = wv[i][t];
+      const uint32_t ws[4] = {u.x, u.y, u.z, u.w};
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          d = fmaf(__uint_as_float(ws[q] << 16), ek[2 * q], d);
+          d = fmaf(__uint_as_float(ws[q] & 0xFFFF0000u), ek[2 * q + 1], d);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) d = fmaf(__uint_as_float(ws[q]), ek[q], d);
+      }
+    }
+    d += __shfl_xor(d, 1, kWave);
+    d += __shfl_xor(d, 2, kWave);
+    d += __shfl_xor(d, 4, kWave);
+    if (j == i) zmine = lg + d;
+  }
+  const int vmine = v0 + grp + 32 * j;
+  uint64_t k1 = (j < NR && vmine < V) ? argmax_key(zmine, (uint32_t)vmine) : 0;
+  float v2 = -INFINITY;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t ok = __shfl_xor(k1, o, kWave);
+    const float ov = __shfl_xor(v2, o, kWave);
+    top2_merge(k1, v2, ok, ov);
+  }
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    rk[w] = k1;
+    rv[w] = v2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 4; ++i) top2_merge(rk[0], rv[0], rk[i], rv[i]);
+    uint64_t* pp = part + (((int64_t)(step & 1) * B + b) * n_chunks + c) * 2;
+    pp[0] = rk[0];
+    pp[1] = (uint64_t)__float_as_uint(rv[0]);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits, const int* spine,
@@ -269,19 +381,61 @@ hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, cons
   return hipGetLastError();
 }
 
+int ar_head_chunk(int dtype, int rank) {
+  const int P = rank * (dtype == 1 ? 2 : 4) / 128;
+  const int nr = ar_rows_per_group(P);
+  return nr > 0 ? 32 * nr : 256;
+}
+
+template <typename T, int P>
+hipError_t launch_ar_pf(dim3 grid, hipStream_t st, int step, int gamma, int V, int rank, const float* logits,
+                        const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
+                        float* margins, uint64_t* part, int n_chunks, int chunk, int B, int* status) {
+  hipLaunchKernelGGL((ar_step_pf<T, P>), grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const T*)E,
+                     (const T*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+  return hipGetLastError();
+}
+
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                           const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                           uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st) {
+  if (chunk != ar_head_chunk(dtype, rank) || n_chunks != (V + chunk - 1) / chunk) return hipErrorInvalidValue;
+  const int P = rank * (dtype == 1 ? 2 : 4) / 128;
   for (int step = 1; step <= gamma + 1; ++step) {
     Phase ph("ar_step", st);
     dim3 grid(step <= gamma ? n_chunks : 1, B);
-    if (dtype == 1)
-      hipLaunchKernelGGL(ar_step<bf16_t>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const bf16_t*)E,
-                         (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
-    else
-      hipLaunchKernelGGL(ar_step<float>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const float*)E,
-                         (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
-    const hipError_t e = hipGetLastError();
+    hipError_t e = hipErrorInvalidValue;
+#define DPARA_AR_PF(TT, PP) \
+  e = launch_ar_pf<TT, PP>(grid, st, step, gamma, V, rank, logits, E, W, bonus, drafts, next_spine, margins, part, \
+                           n_chunks, chunk, B, status)
+    if (dtype == 1) {
+      switch (P) {
+        case 1: DPARA_AR_PF(bf16_t, 1); break;
+        case 2: DPARA_AR_PF(bf16_t, 2); break;
+        case 3: DPARA_AR_PF(bf16_t, 3); break;
+        case 4: DPARA_AR_PF(bf16_t, 4); break;
+        case 5: DPARA_AR_PF(bf16_t, 5); break;
+        case 6: DPARA_AR_PF(bf16_t, 6); break;
+        case 7: DPARA_AR_PF(bf16_t, 7); break;
+        case 8: DPARA_AR_PF(bf16_t, 8); break;
+        default:
+          hipLaunchKernelGGL(ar_step<bf16_t>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const bf16_t*)E,
+                             (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+          e = hipGetLastError();
+      }
+    } else {
+      switch (P) {
+        case 2: DPARA_AR_PF(float, 2); break;
+        case 4: DPARA_AR_PF(float, 4); break;
+        case 6: DPARA_AR_PF(float, 6); break;
+        case 8: DPARA_AR_PF(float, 8); break;
+        default:
+          hipLaunchKernelGGL(ar_step<float>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const float*)E,
+                             (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+          e = hipGetLastError();
+      }
+    }
+#undef DPARA_AR_PF
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -8,11 +8,14 @@ teacher-forced (the oracle's step i is fed the GPU's y_{i-1}).
 Deep bf16 drafters (5 layers at 4096/5120 width): float32 accumulation alone
 (instead of the oracle's float64) flips a fraction of the bf16 roundings and the
 flips compound with depth.  Running the oracle's own GEMMs and attention in
-float32 moves it by up to 3.7e-2 max-abs from itself at the Qwen3-8B shape
-(99.99th percentile 2.9e-2, median 5e-3), while one full-width layer stays at
-1.1e-2.  So single-layer and small configurations keep the 2e-2 bar and the
-5-layer configurations are held to that measured float32 envelope:
-max-abs <= 5e-2, 99.99th percentile <= 3e-2, median <= 1e-2.
+float32 moves it from itself, at the Qwen3-8B shape, by up to 3.7e-2 max-abs on
+request 0 of the batch-1 round (99.99th percentile 2.9e-2, median 5e-3) and by
+3.4e-2 max-abs on the sampled rows of the batch-16 round (99.99th percentile
+2.8e-2, median 4.8e-3), while one full-width layer stays at 1.1e-2.  Any other
+float32 summation order lands in that envelope only statistically, so the
+5-layer configurations are held to it with a 25% margin: max-abs <= 5e-2,
+99.99th percentile <= 3.5e-2, median <= 1e-2; single-layer and small
+configurations keep the 2e-2 bar.
 """
 import sys
 
@@ -27,7 +30,7 @@ from paper_2609_27396_amd import synth  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-5, "bf16": 2e-2}
-DEEP = {"max": 5e-2, "q9999": 3e-2, "median": 1e-2}
+DEEP = {"max": 5e-2, "q9999": 3.5e-2, "median": 1e-2}
 MARGIN = 1e-2
 
 
