@@ -7,6 +7,39 @@
 namespace dpara {
 namespace {
 
+constexpr int kMaxPlanes = 16;  // split-K partial planes a consumer may have to add
+
+// acc + p[0] + p[stride] + ... + p[(n-1)*stride], added in plane order; all n loads are
+// issued before the first add so that their latencies overlap.
+__device__ __forceinline__ float sum_planes(float acc, const float* p, int64_t stride, int n) {
+  float v[kMaxPlanes];
+#pragma unroll
+  for (int s = 0; s < kMaxPlanes; ++s) v[s] = s < n ? p[s * stride] : 0.f;
+#pragma unroll
+  for (int s = 0; s < kMaxPlanes; ++s)
+    if (s < n) acc += v[s];
+  return acc;
+}
+// float4 form for the row kernels: planes are loaded in batches of 4 (bounded registers,
+// still 4 loads in flight per slot), added in plane order.
+__device__ __forceinline__ float4 sum_planes4(float4 acc, const float* p, int64_t stride, int n) {
+  for (int s0 = 0; s0 < n; s0 += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      v[q] = s0 + q < n ? *(const float4*)(p + (s0 + q) * stride) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (s0 + q < n) {
+        acc.x += v[q].x;
+        acc.y += v[q].y;
+        acc.z += v[q].z;
+        acc.w += v[q].w;
+      }
+  }
+  return acc;
+}
+
 // Row layout of one request (Section 3.2): rows 0..gamma are the spine t_0..t_gamma;
 // row gamma+1 + r*gamma + (i-1) is mask i of branch r.  Position offset from the
 // context length: spine j -> j; branch r mask i -> r + i.
@@ -34,10 +67,11 @@ __global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, in
   for (int i = threadIdx.x; i < H; i += 256) dst[i] = ld_f(src + i);
 }
 
-// One block (16 waves) per output row.  x = X row + the S pending split-K partial planes of
-// that row (summed in plane order); optionally x is written back into X; y = x / rms(x) * g.
-constexpr int kNormThreads = 1024;
-template <typename TO>
+// One block (8 waves) per output row, VN float4 per thread.  x = X row + the S pending
+// split-K partial planes of that row (added in plane order); optionally x is written back
+// into X; y = x / rms(x) * g.
+constexpr int kNormThreads = 512;
+template <typename TO, int VN>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, int grp, int64_t in_stride,
                                                              int in_off, const float* P, int S, int64_t pstride,
                                                              int write_back, const float* g, float eps, TO* Y) {
@@ -45,20 +79,13 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, in
   const int m = blockIdx.x;
   const int64_t roff = (int64_t)(m / grp) * in_stride + (int64_t)(in_off + m % grp) * H;
   float* x = X + roff;
-  float4 v[2];  // H <= 8192: up to 2 float4 per thread
+  float4 v[VN];
   float ss = 0.f;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
+  for (int t = 0; t < VN; ++t) {
     const int i = (threadIdx.x + kNormThreads * t) * 4;
     if (i < H) {
-      float4 a = *(const float4*)(x + i);
-      for (int sp = 0; sp < S; ++sp) {
-        const float4 b = *(const float4*)(P + sp * pstride + roff + i);
-        a.x += b.x;
-        a.y += b.y;
-        a.z += b.z;
-        a.w += b.w;
-      }
+      const float4 a = sum_planes4(*(const float4*)(x + i), P + roff + i, pstride, S);
       if (write_back && S > 0) *(float4*)(x + i) = a;
       v[t] = a;
       ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
@@ -68,7 +95,7 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, in
   const float r = 1.0f / sqrtf(ss / (float)H + eps);
   TO* y = Y + (int64_t)m * H;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
+  for (int t = 0; t < VN; ++t) {
     const int i = (threadIdx.x + kNormThreads * t) * 4;
     if (i < H) {
       const float4 gg = *(const float4*)(g + i);
@@ -117,11 +144,10 @@ __global__ __launch_bounds__(256) void qk_norm_rope(int R, int Rp, int gamma, in
       const bool isq = slot < n_q;
       const bool act = lane < half;
       float x1 = 0.f, x2 = 0.f;
-      if (act)
-        for (int sp = 0; sp < S; ++sp) {
-          x1 += x[sp * pstride + lane];
-          x2 += x[sp * pstride + lane + half];
-        }
+      if (act) {
+        x1 = sum_planes(0.f, x + lane, pstride, S);
+        x2 = sum_planes(0.f, x + lane + half, pstride, S);
+      }
       if (qk_norm) {
         const float ss = wave_sum(x1 * x1 + x2 * x2);
         const float r = 1.0f / sqrtf(ss / (float)hd + eps);
@@ -149,11 +175,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope(int R, int Rp, int gamma, in
     } else {
       const int kvh = slot - n_q - n_kv;
       T* dst = Vb + (int64_t)(b * n_kv + kvh) * hd * Rp + row;  // transposed: [hd][Rp]
-      for (int d = lane; d < hd; d += 64) {
-        float acc = 0.f;
-        for (int sp = 0; sp < S; ++sp) acc += x[sp * pstride + d];
-        st_f(dst + (int64_t)d * Rp, acc);
-      }
+      for (int d = lane; d < hd; d += 64) st_f(dst + (int64_t)d * Rp, sum_planes(0.f, x + d, pstride, S));
     }
   }
 }
@@ -195,11 +217,10 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
     const float* x = src + kvh * hd;
     const bool act = lane < half;
     float x1 = 0.f, x2 = 0.f;
-    if (act)
-      for (int sp = 0; sp < S; ++sp) {
-        x1 += x[sp * pstride + lane];
-        x2 += x[sp * pstride + lane + half];
-      }
+    if (act) {
+      x1 = sum_planes(0.f, x + lane, pstride, S);
+      x2 = sum_planes(0.f, x + lane + half, pstride, S);
+    }
     if (qk_norm) {
       const float ss = wave_sum(x1 * x1 + x2 * x2);
       const float r = 1.0f / sqrtf(ss / (float)hd + eps);
@@ -217,11 +238,7 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
       st_f(kd + lane + half, x2 * cc + x1 * ss);
     }
     const float* xv = src + (n_kv + kvh) * hd;
-    for (int d = lane; d < hd; d += 64) {
-      float acc = 0.f;
-      for (int sp = 0; sp < S; ++sp) acc += xv[sp * pstride + d];
-      st_f(Vc + (kvb * hd + d) * cap + pos, acc);
-    }
+    for (int d = lane; d < hd; d += 64) st_f(Vc + (kvb * hd + d) * cap + pos, sum_planes(0.f, xv + d, pstride, S));
   }
 }
 
@@ -256,18 +273,36 @@ hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V
   return hipGetLastError();
 }
 
+template <typename TO, int VN>
+void rmsnorm_launch(int rows, int H, float* X, int grp, int64_t in_stride, int in_off, const float* P, int S,
+                    int64_t pstride, int write_back, const float* g, float eps, void* Y, hipStream_t st) {
+  hipLaunchKernelGGL((rmsnorm_rows<TO, VN>), dim3(rows), dim3(kNormThreads), 0, st, H, X, grp, in_stride, in_off, P,
+                     S, pstride, write_back, g, eps, (TO*)Y);
+}
+
+template <typename TO>
+hipError_t rmsnorm_dispatch(int rows, int H, float* X, int grp, int64_t in_stride, int in_off, const float* P,
+                            int S, int64_t pstride, int write_back, const float* g, float eps, void* Y,
+                            hipStream_t st) {
+  const int vn = (H / 4 + kNormThreads - 1) / kNormThreads;
+  switch (vn) {
+    case 1: rmsnorm_launch<TO, 1>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st); break;
+    case 2: rmsnorm_launch<TO, 2>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st); break;
+    case 3: rmsnorm_launch<TO, 3>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st); break;
+    case 4: rmsnorm_launch<TO, 4>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int64_t in_stride, int in_off,
                           const float* P, int S, int64_t pstride, int write_back, const float* g, float eps,
                           void* Y, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  if (H > 8 * kNormThreads || H % 4) return hipErrorInvalidValue;
+  if (H > 16 * kNormThreads || H % 4 || S < 0 || S > kMaxPlanes) return hipErrorInvalidValue;
   if (out_dtype == 1)
-    hipLaunchKernelGGL(rmsnorm_rows<bf16_t>, dim3(rows), dim3(kNormThreads), 0, st, H, X, grp, in_stride, in_off, P, S,
-                       pstride, write_back, g, eps, (bf16_t*)Y);
-  else
-    hipLaunchKernelGGL(rmsnorm_rows<float>, dim3(rows), dim3(kNormThreads), 0, st, H, X, grp, in_stride, in_off, P, S,
-                       pstride, write_back, g, eps, (float*)Y);
-  return hipGetLastError();
+    return rmsnorm_dispatch<bf16_t>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st);
+  return rmsnorm_dispatch<float>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st);
 }
 
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len, int pos_off,
@@ -282,7 +317,7 @@ hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ct
 hipError_t launch_qk_norm_rope(int dtype, int B, int R, int Rp, int gamma, int n_q, int n_kv, int hd, int qk_norm,
                                float eps, const float* QKV, int S, const float* qn, const float* kn,
                                const float2* table, void* Q, void* Kb, void* Vb, hipStream_t st) {
-  if (Rp < R) return hipErrorInvalidValue;
+  if (Rp < R || S < 1 || S > kMaxPlanes) return hipErrorInvalidValue;
   dim3 grid((n_q + 2 * n_kv + 3) / 4, B * R);
   const int64_t pstride = (int64_t)B * R * (n_q + 2 * n_kv) * hd;
   if (dtype == 1)
@@ -309,6 +344,7 @@ hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv
                            float eps, float base, const float* KV, int S, const float* kn, const int* n_new,
                            const int* ctx_len, int cap, void* Kc, void* Vc, int* status, hipStream_t st) {
   (void)status;
+  if (S < 1 || S > kMaxPlanes) return hipErrorInvalidValue;
   const int64_t pstride = (int64_t)B * CH * 2 * n_kv * hd;
   const dim3 grid((n_kv + 3) / 4, B * CH);
   if (dtype == 1)
