@@ -114,7 +114,7 @@ struct Plan {
   int B, R, Rp, M, S, chunk, CH, esz;
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   int v_chunk, v_chunks, h_chunk, h_chunks;
-  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, counters, F, KV32;
+  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, F, KV32, rope_app;
   size_t total;
 };
 
@@ -178,11 +178,11 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.Gsplit = take((size_t)2 * B * c->gamma * H * 2);  // bf16 hi and lo planes of G
   p.logits = take((size_t)B * c->gamma * c->vocab * 4);
   p.hpart = take((size_t)2 * B * p.h_chunks * 16);  // two step-parity slots
-  p.counters = take((size_t)B * 4);
   p.F = take((size_t)B * p.CH * H * p.esz);
   // append K|V planes: split only when the append GEMM has at most 320 rows (16 planes max)
   const size_t kv_rows = (size_t)B * p.CH > 16 * 320 ? (size_t)B * p.CH : 16 * 320;
   p.KV32 = take(kv_rows * 2 * nkv * hd * 4);
+  p.rope_app = take((size_t)B * p.CH * (hd / 2) * 8);  // (cos, sin) of the appended rows' positions
   p.total = off;
   return p;
 }
@@ -466,6 +466,8 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
   const int CH = n_max < p.CH ? n_max : p.CH;  // rows per request per chunk
   for (int c0 = 0; c0 < n_max; c0 += CH) {
     HIP_TRY(launch_gather_feats(dt, batch, CH, c0, n_max, H, feats, at<void>(ws, p.F), st), "gather_feats");
+    HIP_TRY(launch_rope_table(batch, CH, hd, cfg->rope_base, ctx->ctx_len, c0, at<float2>(ws, p.rope_app), st),
+            "rope_table");
     for (int l = 0; l < cfg->n_layers; ++l) {
       GemmArgs g{};
       g.A = at<void>(ws, p.F);
@@ -488,8 +490,8 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
       char* kc = (char*)ctx->k + l * layer_elems * esz;
       char* vc = (char*)ctx->v + l * layer_elems * esz;
       Phase ph("append_store", st);
-      HIP_TRY(launch_kv_store(dt, batch, CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps, cfg->rope_base,
-                              at<float>(ws, p.KV32), g.splits, w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
+      HIP_TRY(launch_kv_store(dt, batch, CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps,
+                              at<float2>(ws, p.rope_app), at<float>(ws, p.KV32), g.splits, w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
                               vc, status, st),
               "kv_store");
     }
@@ -623,7 +625,7 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   const Plan p = make_plan(cfg, batch, 64);
   if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
-  const size_t need = p.counters + up256((size_t)batch * 4);
+  const size_t need = p.hpart + up256((size_t)2 * batch * p.h_chunks * 16);
   if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
   if ((rc = check_device())) return rc;
 

@@ -64,7 +64,23 @@ __global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, in
     src = embed + (int64_t)t * H;
   }
   float* dst = X + ((int64_t)b * R + row) * H;
-  for (int i = threadIdx.x; i < H; i += 256) dst[i] = ld_f(src + i);
+  // 8 elements (one 16- or 32-byte chunk) per thread and iteration; H % 8 == 0
+#pragma unroll 2
+  for (int i = threadIdx.x * 8; i < H; i += 256 * 8) {
+    float4 lo, hi;
+    if constexpr (sizeof(T) == 2) {
+      const uint4 u = *(const uint4*)(src + i);
+      lo = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xFFFF0000u));
+      hi = make_float4(__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xFFFF0000u), __uint_as_float(u.w << 16),
+                       __uint_as_float(u.w & 0xFFFF0000u));
+    } else {
+      lo = *(const float4*)(src + i);
+      hi = *(const float4*)(src + i + 4);
+    }
+    *(float4*)(dst + i) = lo;
+    *(float4*)(dst + i + 4) = hi;
+  }
 }
 
 // One block (8 waves) per output row, VN float4 per thread.  x = X row + the S pending
@@ -115,7 +131,7 @@ __global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx
   if (idx >= n_pos * half) return;
   const int i = idx / half, p = idx % half;
   float c, s;
-  rope_cs(ctx_len[b] + pos_off + i, p, hd, base, &c, &s);
+  rope_cs(max(ctx_len[b], 0) + pos_off + i, p, hd, base, &c, &s);
   table[((int64_t)b * n_pos + i) * half + p] = make_float2(c, s);
 }
 
@@ -184,13 +200,16 @@ template <typename T>
 __global__ __launch_bounds__(256) void gather_feats(int CH, int c0, int n_max, int H, const T* feats, T* F) {
   const int m = blockIdx.x, b = m / CH, i = m % CH;
   const int c = c0 + i;
-  T* dst = F + (int64_t)m * H;
+  // 16-byte chunks; H * sizeof(T) % 16 == 0
+  uint4* dst = (uint4*)(F + (int64_t)m * H);
+  const int nch = H * (int)sizeof(T) / 16;
   if (c >= n_max) {
-    for (int k = threadIdx.x; k < H; k += 256) dst[k] = (T)0;
+    for (int k = threadIdx.x; k < nch; k += 256) dst[k] = make_uint4(0, 0, 0, 0);
     return;
   }
-  const T* src = feats + ((int64_t)b * n_max + c) * H;
-  for (int k = threadIdx.x; k < H; k += 256) dst[k] = src[k];
+  const uint4* src = (const uint4*)(feats + ((int64_t)b * n_max + c) * H);
+#pragma unroll 4
+  for (int k = threadIdx.x; k < nch; k += 256) dst[k] = src[k];
 }
 
 __device__ __forceinline__ int clamp_count(int n, int n_max) { return n < 0 ? 0 : (n > n_max ? n_max : n); }
@@ -199,7 +218,7 @@ __device__ __forceinline__ int clamp_count(int n, int n_max) { return n < 0 ? 0 
 // [pos][hd], V to the transposed cache [hd][pos].
 template <typename T>
 __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n_kv, int hd, int qk_norm, float eps,
-                                                double base, const float* KV, int S, int64_t pstride,
+                                                const float2* rope, const float* KV, int S, int64_t pstride,
                                                 const float* kn,
                                                 const int* n_new, const int* ctx_len, int cap, T* Kc,
                                                 T* Vc) {
@@ -231,11 +250,10 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
     }
     const int64_t kvb = (int64_t)(b * n_kv + kvh);
     if (act) {
-      float cc, ss;
-      rope_cs(pos, lane, hd, base, &cc, &ss);
+      const float2 cs = rope[(int64_t)m * half + lane];  // row m of this chunk, position pos
       T* kd = Kc + (kvb * cap + pos) * hd;
-      st_f(kd + lane, x1 * cc - x2 * ss);
-      st_f(kd + lane + half, x2 * cc + x1 * ss);
+      st_f(kd + lane, x1 * cs.x - x2 * cs.y);
+      st_f(kd + lane + half, x2 * cs.x + x1 * cs.y);
     }
     const float* xv = src + (n_kv + kvh) * hd;
     for (int d = lane; d < hd; d += 64) st_f(Vc + (kvb * hd + d) * cap + pos, sum_planes(0.f, xv + d, pstride, S));
@@ -341,7 +359,7 @@ hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int 
 }
 
 hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd, int qk_norm,
-                           float eps, float base, const float* KV, int S, const float* kn, const int* n_new,
+                           float eps, const float2* rope, const float* KV, int S, const float* kn, const int* n_new,
                            const int* ctx_len, int cap, void* Kc, void* Vc, int* status, hipStream_t st) {
   (void)status;
   if (S < 1 || S > kMaxPlanes) return hipErrorInvalidValue;
@@ -349,10 +367,10 @@ hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv
   const dim3 grid((n_kv + 3) / 4, B * CH);
   if (dtype == 1)
     hipLaunchKernelGGL(kv_store<bf16_t>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
-                       (double)base, KV, S, pstride, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc);
+                       rope, KV, S, pstride, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc);
   else
     hipLaunchKernelGGL(kv_store<float>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
-                       (double)base, KV, S, pstride, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc);
+                       rope, KV, S, pstride, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc);
   return hipGetLastError();
 }
 

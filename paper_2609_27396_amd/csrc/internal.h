@@ -90,8 +90,9 @@ hipError_t launch_qk_norm_rope(int dtype, int B, int R, int Rp, int gamma, int n
 hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int H,
                                const void* feats, void* F, hipStream_t st);
 // KV: S fp32 planes [S][B*CH][2*n_kv*hd], summed in order.
+// rope: [B*CH][hd/2] (cos, sin) of row m's position max(ctx_len[b], 0) + c0 + (m % CH).
 hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd,
-                           int qk_norm, float eps, float base, const float* KV, int S,
+                           int qk_norm, float eps, const float2* rope, const float* KV, int S,
                            const float* kn, const int* n_new, const int* ctx_len, int cap,
                            void* Kc, void* Vc, int* status, hipStream_t st);
 hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, int* ctx_len,

@@ -20,7 +20,9 @@
 namespace dpara {
 namespace {
 
-template <typename T>
+// VEC: rows are 16-byte aligned and the chunk is read in 16-byte pieces (8 bf16 or 4 float32
+// per load), several pieces in flight per thread; otherwise element by element.
+template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void verify_partial(const T* logits, int V, int chunk, int n_chunks,
                                                       uint64_t* part) {
   __shared__ uint64_t red[4];
@@ -28,9 +30,28 @@ __global__ __launch_bounds__(256) void verify_partial(const T* logits, int V, in
   const T* x = logits + (int64_t)rowid * V;
   const int v0 = c * chunk, v1 = min(V, v0 + chunk);
   uint64_t best = 0;
-  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const uint64_t k = argmax_key(ld_f(x + v), (uint32_t)v);
-    best = k > best ? k : best;
+  if constexpr (VEC) {
+    constexpr int EPP = 16 / sizeof(T);
+#pragma unroll 4
+    for (int v = v0 + threadIdx.x * EPP; v < v1; v += 256 * EPP) {
+      const uint4 u = *(const uint4*)(x + v);
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int q = 0; q < EPP; ++q) {
+        float f;
+        if constexpr (sizeof(T) == 2) f = __uint_as_float(q & 1 ? (w[q >> 1] & 0xFFFF0000u) : (w[q >> 1] << 16));
+        else f = __uint_as_float(w[q]);
+        if (v + q < v1) {
+          const uint64_t k = argmax_key(f, (uint32_t)(v + q));
+          best = k > best ? k : best;
+        }
+      }
+    }
+  } else {
+    for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+      const uint64_t k = argmax_key(ld_f(x + v), (uint32_t)v);
+      best = k > best ? k : best;
+    }
   }
   best = wave_max_u64(best);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = best;
@@ -360,12 +381,23 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
                          int chunk, int* status, hipStream_t st) {
   Phase ph("verify", st);
   dim3 grid(n_chunks, B * (gamma + 1));
-  if (logits_dtype == 1)
-    hipLaunchKernelGGL(verify_partial<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)logits, V, chunk, n_chunks,
-                       part);
-  else
-    hipLaunchKernelGGL(verify_partial<float>, grid, dim3(256), 0, st, (const float*)logits, V, chunk, n_chunks,
-                       part);
+  const size_t esz = logits_dtype == 1 ? 2 : 4;
+  const bool vec = ((uintptr_t)logits % 16 == 0) && ((size_t)V * esz % 16 == 0) && ((size_t)chunk * esz % 16 == 0);
+  if (logits_dtype == 1) {
+    if (vec)
+      hipLaunchKernelGGL((verify_partial<bf16_t, true>), grid, dim3(256), 0, st, (const bf16_t*)logits, V, chunk,
+                         n_chunks, part);
+    else
+      hipLaunchKernelGGL((verify_partial<bf16_t, false>), grid, dim3(256), 0, st, (const bf16_t*)logits, V, chunk,
+                         n_chunks, part);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((verify_partial<float, true>), grid, dim3(256), 0, st, (const float*)logits, V, chunk,
+                         n_chunks, part);
+    else
+      hipLaunchKernelGGL((verify_partial<float, false>), grid, dim3(256), 0, st, (const float*)logits, V, chunk,
+                         n_chunks, part);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(verify_finalize, dim3(B), dim3(64), 0, st, gamma, V, n_chunks, part, spine, accept_len,
