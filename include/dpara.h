@@ -56,7 +56,9 @@ enum {
   DPARA_STATUS_TOKEN_RANGE = 1,  /* a token id was outside [0, vocab) */
   DPARA_STATUS_CTX_FULL = 2,     /* an append would exceed ctx_cap; rows beyond it dropped */
   DPARA_STATUS_VERDICT_RANGE = 4, /* accept_len outside [0, gamma] */
-  DPARA_STATUS_COUNT_RANGE = 8    /* an append count n_new outside [0, n_max] (clamped) */
+  DPARA_STATUS_COUNT_RANGE = 8,   /* an append count n_new outside [0, n_max] (clamped) */
+  DPARA_STATUS_HEAD_TIMEOUT = 16  /* the single-launch AR head's workgroups were not all resident
+                                     together (e.g. the GPU was shared); its drafts are invalid */
 };
 
 /* Drafter shape.  Constraints: gamma in [1, 63]; head_dim in {64, 128};
@@ -168,7 +170,12 @@ int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* ta
  *         l_i = gathered_i . embed^T, z_i = l_i + ar_W ar_E[y_{i-1}], y_0 = bonus,
  *         y_i = argmax z_i (lowest index on ties).
  * next_spine: [batch, gamma+1] int32 (device): (bonus, y_1..y_gamma).
- * margins: [batch, gamma] float32 (device, may be NULL): top1 - top2 of z_i. */
+ * margins: [batch, gamma] float32 (device, may be NULL): top1 - top2 of z_i.
+ * bf16 drafters with ar_rank in {64, 128, 256, 512}, vocab <= 2^18 and batch <= 16 run the
+ * gamma head steps in one launch that needs all of its workgroups resident at once (one
+ * per CU); if the GPU is shared so that they cannot all run, the launch gives up after
+ * about 0.3 s per step and sets DPARA_STATUS_HEAD_TIMEOUT.  Other configurations launch
+ * one kernel per step. */
 int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
                           const float* reps, const int32_t* accept_len, const int32_t* bonus,
                           float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,

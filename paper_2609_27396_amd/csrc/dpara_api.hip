@@ -114,7 +114,8 @@ struct Plan {
   int B, R, Rp, M, S, chunk, CH, esz;
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   int v_chunk, v_chunks, h_chunk, h_chunks;
-  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, F, KV32, rope_app;
+  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, F, KV32, rope_app;
+  int ar_grid;  // persistent AR head grid (0: step kernels only)
   size_t total;
 };
 
@@ -178,6 +179,8 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.Gsplit = take((size_t)2 * B * c->gamma * H * 2);  // bf16 hi and lo planes of G
   p.logits = take((size_t)B * c->gamma * c->vocab * 4);
   p.hpart = take((size_t)2 * B * p.h_chunks * 16);  // two step-parity slots
+  p.ar_grid = (c->dtype == DPARA_BF16 && B <= 16) ? ar_persistent_grid(c->ar_rank, c->vocab) : 0;
+  p.arpart = take((size_t)2 * 16 * p.ar_grid * 16);  // persistent head: [2][16][grid] x 2 words
   p.F = take((size_t)B * p.CH * H * p.esz);
   // append K|V planes: split only when the append GEMM has at most 320 rows (16 planes max)
   const size_t kv_rows = (size_t)B * p.CH > 16 * 320 ? (size_t)B * p.CH : 16 * 320;
@@ -625,7 +628,7 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   const Plan p = make_plan(cfg, batch, 64);
   if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
-  const size_t need = p.hpart + up256((size_t)2 * batch * p.h_chunks * 16);
+  const size_t need = p.arpart + up256((size_t)2 * 16 * p.ar_grid * 16);
   if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
   if ((rc = check_device())) return rc;
 
@@ -634,7 +637,9 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   int* status = at<int>(ws, 0);
   float* G = at<float>(ws, p.G);
   bf16_t* Gs = at<bf16_t>(ws, p.Gsplit);
-  HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, G, gathered, Gs, status, st), "gather_branch");
+  HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, G, gathered, Gs, at<uint64_t>(ws, p.arpart),
+                               (int64_t)2 * 16 * p.ar_grid * 2, status, st),
+          "gather_branch");
   const bool bf = cfg->dtype == DPARA_BF16;
   GemmArgs lm{};
   lm.A = bf ? (const void*)Gs : (const void*)G;
@@ -653,7 +658,7 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   }
   HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
-                         status, st),
+                         p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status, st),
           "ar head");
   return DPARA_OK;
 }

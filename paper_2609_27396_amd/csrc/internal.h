@@ -104,13 +104,24 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
                          const int* spine, int* accept_len, int* bonus, int* target_argmax,
                          uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st);
 // G (fp32, optional copy G_out) and its bf16 hi/lo split planes Ghi, Glo = Ghi + M*H.
+// Also zeroes n_clear uint64 words at `clear` (the persistent AR head's step tags).
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
                                 const int* accept_len, float* G, float* G_out, bf16_t* Ghi,
-                                int* status, hipStream_t st);
+                                uint64_t* clear, int64_t n_clear, int* status, hipStream_t st);
 int ar_head_chunk(int dtype, int rank);  // vocabulary rows per AR-step workgroup
+// Persistent bf16 AR head: grid size for (rank, V), 0 if unsupported; the partial buffer is
+// [2][16][grid][2] uint64 and must hold zero tags when the launch starts.  Returns
+// hipErrorNotSupported (nothing launched) when the configuration or the device's occupancy
+// does not allow it.
+int ar_persistent_grid(int rank, int V);
+hipError_t launch_ar_head_persistent(int B, int gamma, int V, int rank, const float* logits, const void* E,
+                                     const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
+                                     uint64_t* part, int part_grid, int* status, hipStream_t st);
+// bf16 with ppart (zero tags, ppart_grid = ar_persistent_grid) runs the persistent head when
+// the device allows it; otherwise gamma+1 step kernels with partials in `part`.
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits,
                           const void* E, const void* W, const int* bonus, int* drafts,
                           int* next_spine, float* margins, uint64_t* part, int n_chunks,
-                          int chunk, int* status, hipStream_t st);
+                          int chunk, uint64_t* ppart, int ppart_grid, int* status, hipStream_t st);
 
 }  // namespace dpara

@@ -92,8 +92,10 @@ __global__ __launch_bounds__(64) void verify_finalize(int gamma, int V, int n_ch
 
 __global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const float* reps, const int* accept_len,
                                                      float* G, float* G_out, bf16_t* Ghi, int64_t lo_off,
-                                                     int* status) {
+                                                     uint64_t* clear, int64_t n_clear, int* status) {
   const int i = blockIdx.x, b = blockIdx.y;
+  for (int64_t k = ((int64_t)b * gridDim.x + i) * 256 + threadIdx.x; k < n_clear; k += (int64_t)gridDim.x * gridDim.y * 256)
+    clear[k] = 0;
   int r = accept_len[b];
   if (r < 0 || r > gamma) {
     if (threadIdx.x == 0) raise_status(status, 4);
@@ -406,10 +408,11 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
 }
 
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, const int* accept_len, float* G,
-                                float* G_out, bf16_t* Ghi, int* status, hipStream_t st) {
+                                float* G_out, bf16_t* Ghi, uint64_t* clear, int64_t n_clear, int* status,
+                                hipStream_t st) {
   Phase ph("gather", st);
   hipLaunchKernelGGL(gather_branch, dim3(gamma, B), dim3(256), 0, st, gamma, H, reps, accept_len, G, G_out, Ghi,
-                     (int64_t)B * gamma * H, status);
+                     (int64_t)B * gamma * H, clear, n_clear, status);
   return hipGetLastError();
 }
 
@@ -430,7 +433,13 @@ hipError_t launch_ar_pf(dim3 grid, hipStream_t st, int step, int gamma, int V, i
 
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                           const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                          uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st) {
+                          uint64_t* part, int n_chunks, int chunk, uint64_t* ppart, int ppart_grid, int* status,
+                          hipStream_t st) {
+  if (dtype == 1 && ppart && ppart_grid > 0) {
+    const hipError_t e = launch_ar_head_persistent(B, gamma, V, rank, logits, E, W, bonus, drafts, next_spine,
+                                                   margins, ppart, ppart_grid, status, st);
+    if (e != hipErrorNotSupported) return e;
+  }
   if (chunk != ar_head_chunk(dtype, rank) || n_chunks != (V + chunk - 1) / chunk) return hipErrorInvalidValue;
   const int P = rank * (dtype == 1 ? 2 : 4) / 128;
   for (int step = 1; step <= gamma + 1; ++step) {

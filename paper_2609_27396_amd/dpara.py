@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libdpara.so")
 
 DPARA_OK, DPARA_E_INVALID, DPARA_E_UNSUPPORTED, DPARA_E_WORKSPACE, DPARA_E_CAPACITY, DPARA_E_HIP = 0, -1, -2, -3, -4, -5
 DPARA_F32, DPARA_BF16 = 0, 1
-STATUS_TOKEN_RANGE, STATUS_CTX_FULL, STATUS_VERDICT_RANGE, STATUS_COUNT_RANGE = 1, 2, 4, 8
+STATUS_TOKEN_RANGE, STATUS_CTX_FULL, STATUS_VERDICT_RANGE, STATUS_COUNT_RANGE, STATUS_HEAD_TIMEOUT = 1, 2, 4, 8, 16
 
 EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boundaries",
            "dpara_verify_greedy", "dpara_select_and_head", "dpara_clear_status",
