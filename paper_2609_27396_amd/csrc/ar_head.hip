@@ -4,8 +4,8 @@
 // Each step computes z_i = l_i + W E(y_{i-1}) over the vocabulary and y_i = argmax z_i.
 // Reading the V x r matrix W from HBM at every step dominates the per-step kernels; here
 // every workgroup keeps its slice of W in registers for the whole launch, so W is read
-// once.  Workgroup = 4 waves (one per SIMD); wave w owns 16*NRB vocabulary rows as MFMA
-// B-operand fragments (up to 320 registers per lane, VGPRs and AGPRs).  Per step the workgroup stages E(y_{i-1}) of every request in LDS
+// once.  Workgroup = NW waves; wave w owns 16*NRB vocabulary rows as MFMA B-operand
+// fragments (640 rows per workgroup).  Per step the workgroup stages E(y_{i-1}) of every request in LDS
 // (A operand, up to 16 requests) and one v_mfma_f32_16x16x32_bf16 chain per 16-row block
 // gives W E for all requests at once.
 //
@@ -29,12 +29,10 @@
 namespace dpara {
 namespace {
 
-constexpr int kArpWaves = 4;        // one wave per SIMD: 512 registers per lane
 constexpr int kArpMaxB = 16;         // requests per launch (the MFMA's 16 rows)
 constexpr int kArpTagBits = 14;      // step tag in the low bits of the key word
 constexpr uint32_t kArpIdxMask = 0x3FFFFu;  // vocabulary index field: V <= 2^18
-constexpr int kArpTpr = 64 * kArpWaves / kArpMaxB;  // polling threads per request (16)
-constexpr int kArpPollPer = 16;      // partials per polling thread: grid <= kArpTpr * 16
+constexpr int kArpMaxGrid = 256;     // polling covers up to 16 partials per thread at 16 requests
 constexpr int kArpStatusTimeout = 16;
 
 // Key word: high 32 bits = order-preserving value bits, then (index complement, 18 bits),
@@ -73,49 +71,66 @@ __device__ __forceinline__ uint64_t load_dev(const uint64_t* p) {
 
 // part: [2 slots][kArpMaxB][G][2] uint64 (key word, value word).
 // Reduces step `s` (tags == s) for every request into ys/ms (LDS).  Returns false on timeout.
-// kArpTpr threads per request read its G partials in batches of 8.
-__device__ bool arp_poll(const uint64_t* part, int s, int B, int G, int V, uint32_t spin_limit, int* ys, float* ms) {
-  const int t = threadIdx.x, b = t / kArpTpr, j = t % kArpTpr;
+// The workgroup's threads are split evenly over the requests (tpr = 256 / bpad threads per
+// request, bpad = B rounded up to a power of two), each reading ceil(G / tpr) partials in
+// batches of 4, so a small batch polls all partials in one memory round trip.
+__device__ bool arp_poll(const uint64_t* part, int s, int B, int G, int V, uint32_t spin_limit, int* ys, float* ms,
+                         uint64_t* rkw, float* rvw) {
+  int bpad = 1;
+  while (bpad < B) bpad <<= 1;
+  const int tpr = (int)blockDim.x / bpad;
+  const int t = threadIdx.x, b = t / tpr, j = t % tpr;
+  const int per = (G + tpr - 1) / tpr;
   const uint64_t* slot = part + ((int64_t)(s & 1) * kArpMaxB + b) * G * 2;
   const uint32_t tag = (uint32_t)s & ((1u << kArpTagBits) - 1);
   uint64_t K1 = 0;
   float V2 = -INFINITY;
-  for (int q0 = 0; q0 < kArpPollPer; q0 += 8) {
-    if (kArpTpr * q0 >= G) break;  // uniform
+  for (int q0 = 0; q0 < per; q0 += 4) {  // uniform
     uint32_t it = 0;
     while (true) {
       bool ok = true;
-      uint64_t kw[8], vw[8];
+      uint64_t kw[4], vw[4];
       if (b < B) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int i = min(j + kArpTpr * (q0 + q), G - 1);
+        for (int q = 0; q < 4; ++q) {
+          const int i = min(j + tpr * (q0 + q), G - 1);
           vw[q] = load_dev(slot + 2 * i + 1);
           kw[q] = load_dev(slot + 2 * i);
         }
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-          if (j + kArpTpr * (q0 + q) < G)
+        for (int q = 0; q < 4; ++q)
+          if (j + tpr * (q0 + q) < G)
             ok = ok && ((uint32_t)kw[q] & ((1u << kArpTagBits) - 1)) == tag && (uint32_t)vw[q] == (uint32_t)s;
       }
       if (__syncthreads_and(ok)) {
         if (b < B) {
 #pragma unroll
-          for (int q = 0; q < 8; ++q)
-            if (j + kArpTpr * (q0 + q) < G)
+          for (int q = 0; q < 4; ++q)
+            if (j + tpr * (q0 + q) < G)
               arp_merge(K1, V2, kw[q] & ~(uint64_t)((1u << kArpTagBits) - 1), __uint_as_float((uint32_t)(vw[q] >> 32)));
         }
         break;
       }
       if (++it > spin_limit) return false;
-      __builtin_amdgcn_s_sleep(2);
+      __builtin_amdgcn_s_sleep(1);
     }
   }
-#pragma unroll
-  for (int o = 1; o < kArpTpr; o <<= 1) {
+  const int span = tpr < 64 ? tpr : 64;  // lanes of one request within a wave
+  for (int o = 1; o < span; o <<= 1) {
     const uint64_t ok1 = __shfl_xor(K1, o, kWave);
     const float ov = __shfl_xor(V2, o, kWave);
     arp_merge(K1, V2, ok1, ov);
+  }
+  if (tpr > 64) {  // a request spans several waves: combine their results
+    const int wave = t >> 6;
+    if ((t & 63) == 0) {
+      rkw[wave] = K1;
+      rvw[wave] = V2;
+    }
+    __syncthreads();
+    if (j == 0 && b < B) {
+      for (int w = 1; w < tpr / 64; ++w) arp_merge(K1, V2, rkw[wave + w], rvw[wave + w]);
+    }
   }
   if (b < B && j == 0) {
     ys[b] = min((int)arp_index(K1), V - 1);  // K1 is a real row key unless every z was NaN
@@ -126,8 +141,26 @@ __device__ bool arp_poll(const uint64_t* part, int s, int B, int G, int V, uint3
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int NKB, int NRB>
-__global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, int V, int B, const float* logits,
+// Branch-free top-2 tracking: (k1, v1) best key and its value, v2 second-best value.
+struct Top2 {
+  uint64_t k1;
+  float v1, v2;
+};
+__device__ __forceinline__ void top2_add(Top2& t, uint64_t k, float z) {
+  const bool better = k > t.k1;
+  t.v2 = fmaxf(t.v2, better ? t.v1 : z);
+  t.v1 = better ? z : t.v1;
+  t.k1 = better ? k : t.k1;
+}
+__device__ __forceinline__ void top2_join(Top2& t, const Top2& o) {
+  const bool better = o.k1 > t.k1;
+  t.v2 = fmaxf(fmaxf(t.v2, o.v2), better ? t.v1 : o.v1);
+  t.v1 = better ? o.v1 : t.v1;
+  t.k1 = better ? o.k1 : t.k1;
+}
+
+template <int NKB, int NRB, int NW>
+__global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, int B, const float* logits,
                                                                      const bf16_t* E, const bf16_t* W,
                                                                      const int* bonus, int* drafts,
                                                                      int* next_spine, float* margins,
@@ -135,20 +168,20 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
                                                                      uint32_t spin_limit) {
   constexpr int RANK = NKB * 32;
   constexpr int ROWS_WAVE = 16 * NRB;
-  constexpr int ROWS_WG = kArpWaves * ROWS_WAVE;
+  constexpr int ROWS_WG = NW * ROWS_WAVE;
   constexpr int LCH = ROWS_WG / 4;  // 16-byte logit chunks per request
   constexpr int ESTRIDE = RANK + 8;  // bf16 per staged E row (padding spreads LDS banks)
-  static_assert((kArpMaxB * LCH) % (64 * kArpWaves) == 0, "logit staging must split into whole DMA rounds");
+  static_assert((kArpMaxB * LCH) % (64 * NW) == 0, "logit staging must split into whole DMA rounds");
   __shared__ __attribute__((aligned(16))) bf16_t es[kArpMaxB * ESTRIDE];
   __shared__ __attribute__((aligned(16))) float lgs[kArpMaxB * ROWS_WG];  // this step's logits of the slice
   __shared__ int ys[kArpMaxB];
   __shared__ float ms[kArpMaxB];
-  __shared__ uint64_t rk[kArpWaves][kArpMaxB];
-  __shared__ float rv[kArpWaves][kArpMaxB];
+  __shared__ uint64_t rk[NW][kArpMaxB];
+  __shared__ float rv[NW][kArpMaxB];
   __shared__ int bail;
   const int G = gridDim.x, wg = blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lr = lane & 15, lg = lane >> 4;
-  const int vbase = (wg * kArpWaves + wave) * ROWS_WAVE;
+  const int vbase = (wg * NW + wave) * ROWS_WAVE;
 
   // W fragments: lane (lr, lg) holds W[vbase + rb*16 + lr][kb*32 + lg*8 .. +8].  Rows past
   // V read row V-1; their results are never used.
@@ -177,7 +210,7 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
     // this step's logits of the slice -> LDS by DMA (independent of y): LDS chunk c holds
     // request c / LCH, rows v0 + 4*(c % LCH) .. +3 (chunks past V re-read the last full
     // chunk of the row and are never used)
-    for (int c0 = 0; c0 < B * LCH; c0 += 64 * kArpWaves) {
+    for (int c0 = 0; c0 < B * LCH; c0 += 64 * NW) {
       const int c = c0 + wave * 64 + lane;
       const int b = min(c / LCH, B - 1);
       const int v = min(v0 + 4 * (c % LCH), V - 4);
@@ -185,7 +218,7 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
                                        (lds_void_t*)(lgs + 4 * (c0 + wave * 64)), 16, 0, 0);
     }
     if (s > 1) {
-      const bool okp = arp_poll(part, s - 1, B, G, V, spin_limit, ys, ms);
+      const bool okp = arp_poll(part, s - 1, B, G, V, spin_limit, ys, ms, &rk[0][0], &rv[0][0]);
       if (tid == 0) bail = !okp;
       __syncthreads();
       if (bail) {
@@ -201,7 +234,7 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
       __syncthreads();
     }
     // stage E(y) rows (16-byte pieces); rows of absent requests are zero
-    for (int c = tid; c < kArpMaxB * (RANK / 8); c += 64 * kArpWaves) {
+    for (int c = tid; c < kArpMaxB * (RANK / 8); c += 64 * NW) {
       const int b = c / (RANK / 8), k = (c % (RANK / 8)) * 8;
       uint4 u = make_uint4(0, 0, 0, 0);
       if (b < B) u = *(const uint4*)(E + (int64_t)ys[b] * RANK + k);
@@ -210,9 +243,12 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
     __builtin_amdgcn_s_waitcnt(0);  // this wave's logit DMA has landed
     __syncthreads();
 
-    // z = l + E W^T: C[request 4*lg + i][row lr] of each 16-row block
-    uint64_t k1[4] = {0, 0, 0, 0};
-    float v2[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    // z = l + E W^T: C[request 4*lg + i][row lr] of each 16-row block.  Only the first
+    // min(B, 4) requests of each lane group can exist (uniform loop bound).
+    const int IMAX = B < 4 ? B : 4;
+    Top2 t2[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t2[i] = Top2{0, -INFINITY, -INFINITY};
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
       f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -224,29 +260,36 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
       const int v = vbase + rb * 16 + lr;
       const int vl = wave * ROWS_WAVE + rb * 16 + lr;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (v < V && 4 * lg + i < B)
-          arp_merge(k1[i], v2[i], arp_key(lgs[(4 * lg + i) * ROWS_WG + vl] + acc[i], (uint32_t)v), -INFINITY);
+      for (int i = 0; i < 4; ++i) {
+        if (i >= IMAX) break;
+        const int b = 4 * lg + i;
+        const bool valid = v < V && b < B;
+        const float z = lgs[min(b, B - 1) * ROWS_WG + vl] + acc[i];
+        top2_add(t2[i], valid ? arp_key(z, (uint32_t)v) : 0ull, valid ? z : -INFINITY);
+      }
     }
     // reduce over the 16 rows of the lane group, then over the waves
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+      if (i >= IMAX) break;
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) {
-        const uint64_t ok1 = __shfl_xor(k1[i], o, kWave);
-        const float ov = __shfl_xor(v2[i], o, kWave);
-        arp_merge(k1[i], v2[i], ok1, ov);
+        Top2 ot;
+        ot.k1 = __shfl_xor(t2[i].k1, o, kWave);
+        ot.v1 = __shfl_xor(t2[i].v1, o, kWave);
+        ot.v2 = __shfl_xor(t2[i].v2, o, kWave);
+        top2_join(t2[i], ot);
       }
       if (lr == 0) {
-        rk[wave][4 * lg + i] = k1[i];
-        rv[wave][4 * lg + i] = v2[i];
+        rk[wave][4 * lg + i] = t2[i].k1;
+        rv[wave][4 * lg + i] = t2[i].v2;
       }
     }
     __syncthreads();
     if (tid < B) {
       uint64_t K = rk[0][tid];
       float V2 = rv[0][tid];
-      for (int w = 1; w < kArpWaves; ++w) arp_merge(K, V2, rk[w][tid], rv[w][tid]);
+      for (int w = 1; w < NW; ++w) arp_merge(K, V2, rk[w][tid], rv[w][tid]);
       uint64_t* e = part + (((int64_t)(s & 1) * kArpMaxB + tid) * G + wg) * 2;
       store_dev(e + 1, ((uint64_t)__float_as_uint(V2) << 32) | (uint32_t)s);
       store_dev(e, K | ((uint32_t)s & ((1u << kArpTagBits) - 1)));
@@ -254,7 +297,7 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
   }
   // y_gamma: only workgroup 0 needs it
   if (wg != 0) return;
-  const bool okp = arp_poll(part, gamma, B, G, V, spin_limit, ys, ms);
+  const bool okp = arp_poll(part, gamma, B, G, V, spin_limit, ys, ms, &rk[0][0], &rv[0][0]);
   if (!okp) {
     if (tid == 0) raise_status(status, kArpStatusTimeout);
     return;
@@ -267,23 +310,23 @@ __global__ __launch_bounds__(64 * kArpWaves) void ar_head_persistent(int gamma, 
   }
 }
 
-template <int NKB, int NRB>
+template <int NKB, int NRB, int NW>
 hipError_t arp_launch(int B, int gamma, int V, const float* logits, const void* E, const void* W, const int* bonus,
                       int* drafts, int* next_spine, float* margins, uint64_t* part, int part_grid, int* status,
                       hipStream_t st) {
-  constexpr int ROWS_WG = kArpWaves * 16 * NRB;
+  constexpr int ROWS_WG = NW * 16 * NRB;
   const int G = (V + ROWS_WG - 1) / ROWS_WG;
-  if (G > part_grid || G > kArpTpr * kArpPollPer) return hipErrorNotSupported;
+  if (G > part_grid || G > kArpMaxGrid) return hipErrorNotSupported;
   int dev = 0, cus = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e == hipSuccess)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ar_head_persistent<NKB, NRB>, 64 * kArpWaves, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ar_head_persistent<NKB, NRB, NW>, 64 * NW, 0);
   if (e != hipSuccess) return e;
   if (G > per_cu * cus) return hipErrorNotSupported;  // not co-resident: the caller falls back
   const uint32_t spin_limit = 1u << 17;  // polls of ~2 us: ~0.3 s before a workgroup gives up
   Phase ph("ar_step", st);
-  hipLaunchKernelGGL((ar_head_persistent<NKB, NRB>), dim3(G), dim3(64 * kArpWaves), 0, st, gamma, V, B, logits,
+  hipLaunchKernelGGL((ar_head_persistent<NKB, NRB, NW>), dim3(G), dim3(64 * NW), 0, st, gamma, V, B, logits,
                      (const bf16_t*)E, (const bf16_t*)W, bonus, drafts, next_spine, margins, part, status,
                      spin_limit);
   return hipGetLastError();
@@ -291,12 +334,12 @@ hipError_t arp_launch(int B, int gamma, int V, const float* logits, const void* 
 
 }  // namespace
 
-// 16-row blocks of W per wave: 10 (rank <= 256; up to 160 registers of W per lane) or 5
-// (rank 512, 320 registers), so a workgroup covers 640 or 320 vocabulary rows.
+// 8 waves x 5 16-row blocks (up to 160 registers of W per lane at rank 256, two waves per
+// SIMD): a workgroup covers 640 vocabulary rows.  Wider ranks do not fit one workgroup per
+// CU and use the step kernels.
 int ar_persistent_grid(int rank, int V) {
-  const int nrb = (rank == 64 || rank == 128 || rank == 256) ? 10 : rank == 512 ? 5 : 0;
-  if (nrb == 0) return 0;
-  const int rows = kArpWaves * 16 * nrb;
+  if (rank != 64 && rank != 128 && rank != 256) return 0;
+  const int rows = 640;
   return (V + rows - 1) / rows;
 }
 
@@ -307,10 +350,9 @@ hipError_t launch_ar_head_persistent(int B, int gamma, int V, int rank, const fl
       gamma >= (1 << kArpTagBits) || (uintptr_t)logits % 16)
     return hipErrorNotSupported;
   switch (rank) {
-    case 64: return arp_launch<2, 10>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
-    case 128: return arp_launch<4, 10>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
-    case 256: return arp_launch<8, 10>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
-    case 512: return arp_launch<16, 5>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
+    case 64: return arp_launch<2, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
+    case 128: return arp_launch<4, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
+    case 256: return arp_launch<8, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
     default: return hipErrorNotSupported;
   }
 }
