@@ -28,6 +28,7 @@ METRIC = "all-boundary backbone rounds/sec + head µs/round at b=1..16; % HBM/MF
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
+COPY_PROBE_BYTES = 256 << 20
 
 
 def log(*a):
@@ -195,6 +196,57 @@ def full_round(args, wl):
     print(json.dumps(out), flush=True)
 
 
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary (two rocprofv3 --pmc
+    passes, FETCH_SIZE and WRITE_SIZE, scaled on a plain copy of known size), or None when the
+    summary is missing or the kernel's source changed since the counters were taken."""
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    try:
+        with open(os.path.join(here, "profiles", "traffic_qwen3_8b_b1.md")) as f:
+            line = next(l for l in f if l.startswith("traffic-json: "))
+        rec = json.loads(line[len("traffic-json: "):])
+        with open(os.path.join(here, rec["source"]), "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, StopIteration, ValueError, KeyError):
+        return None
+    if rec.get("kernel") != kernel or rec.get("source_sha256") != digest:
+        return None
+    return float(rec["bytes_per_launch"])
+
+
+def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
+    """Select + AR head alone (gather, LM head over gamma rows, gamma AR steps) at several
+    batch sizes, on synthetic branch representations; microseconds per call."""
+    import torch
+    from paper_2609_27396_amd import dpara as D
+    g, H, V = shape.gamma, shape.hidden, shape.vocab
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1234)
+    out = {}
+    for B in batches:
+        ws = D.Workspace(dr.d.cfg, B, 64)
+        reps = torch.randn((B, g + 1, g, H), generator=gen, device="cuda", dtype=torch.float32)
+        acc = torch.randint(0, g + 1, (B,), generator=gen, device="cuda", dtype=torch.int32)
+        bon = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
+        drafts = torch.empty((B, g), dtype=torch.int32, device="cuda")
+        nspine = torch.empty((B, g + 1), dtype=torch.int32, device="cuda")
+        call = lambda: D.select_and_head(dr.d, reps, acc, bon, None, drafts, nspine, None, ws)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        assert ws.status() == 0, f"device status {ws.status()}"
+        out[str(B)] = 1000.0 * e0.elapsed_time(e1) / iters
+        del ws, reps
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +254,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_8b_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-head-sweep", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first run a plain 256 MiB device copy 3 times (known HBM bytes, to scale "
+                         "profiler traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); requests are independent, so several "
@@ -217,6 +273,13 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     shape = wl.shape
     log(f"[bench] workload {wl.name}: {wl.description}")
+    if args.copy_probe:
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if wl.name == "full_round":
         full_round(args, wl)
         return
@@ -283,8 +346,8 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": gf / g_avg_s / 1e12, "peak": peak_flops, "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
-    roof["kernel"] = "gemm_mfma_kernel (gate/up SwiGLU epilogue)"
+    roof["kernel"] = "gemm_pipe_kernel<320, 96, 4, 1, 2, 128, 2, 0>" if M <= 320 else "gemm_pipe_kernel (gate/up SwiGLU)"
+    roof["traffic"] = recorded_traffic(roof["kernel"]) if wl.name == "qwen3_8b_b1" else None
     roof["algorithmic_bytes_per_launch"] = gb
     roof["algorithmic_flops_per_launch"] = gf
     roof["avg_launch_us"] = g_avg_s * 1e6
@@ -310,6 +373,8 @@ def main():
         "append_us_per_round": 1000.0 * sum_ms(["append_gemm", "append_store"]),
         "phases": phases,
     }
+    if shape.dtype == "bf16" and not args.no_head_sweep:
+        out["head_us_by_batch"] = head_sweep(dr, shape)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(wl, weights, ri)

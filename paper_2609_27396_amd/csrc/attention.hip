@@ -55,6 +55,8 @@ __device__ __forceinline__ int k_swz(int r, int c) {
 }
 __device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
+__device__ __forceinline__ int grp_rows(const AttnArgs& a) { return (a.n_q / a.n_kv) * a.R; }
+
 // Key offset within a 64-key block held by S^T row i of 16-key MFMA block kb.
 __device__ __forceinline__ int key_perm(int kb, int i) { return (kb >> 1) * 32 + (i >> 2) * 8 + (kb & 1) * 4 + (i & 3); }
 
@@ -96,18 +98,26 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
   static_assert(NINS * 1024 * NW == K_BYTES, "tile must split evenly over the waves");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
-  const int b = blockIdx.z / a.n_kv, kvh = blockIdx.z % a.n_kv;
+  // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs, so physical id p
+  // maps to logical id lid with each XCD taking a contiguous range of lid; row tiles run
+  // fastest in lid, so the tiles that read the same key blocks share one XCD's L2.
+  const int n_tiles = (grp_rows(a) + ROWS_WG - 1) / ROWS_WG;
+  const int total = n_tiles * a.S * a.B * a.n_kv;
+  const int p = blockIdx.x, per_xcd = total >> 3;
+  const int lid = p < (per_xcd << 3) ? (p & 7) * per_xcd + (p >> 3) : p;
+  const int tile = lid % n_tiles, split = (lid / n_tiles) % a.S, bh = lid / (n_tiles * a.S);
+  const int b = bh / a.n_kv, kvh = bh % a.n_kv;
   const int grp = a.n_q / a.n_kv;
   const int nrows = grp * a.R;
   const int L = min(max(a.ctx_len[b], 0), a.cap);
   const int nb_ctx = (L + kKeyBlock - 1) / kKeyBlock;
   const int nb = nb_ctx + (a.R + kKeyBlock - 1) / kKeyBlock;
   const int per = (nb + a.S - 1) / a.S;
-  const int vb_begin = min(nb, (int)blockIdx.y * per);
+  const int vb_begin = min(nb, split * per);
   const int n_blk = min(nb, vb_begin + per) - vb_begin;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lq = lane & 15, g4 = lane >> 4;
-  const int qrow0 = blockIdx.x * ROWS_WG + wave * U * 16;
+  const int qrow0 = tile * ROWS_WG + wave * U * 16;
   const bool wave_live = qrow0 < nrows;
 
   const int64_t kvbase = (int64_t)(b * a.n_kv + kvh);
@@ -320,7 +330,7 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
         *(uint2*)(op + hb * 16 + g4 * 4) = make_uint2(w0, w1);
       }
     } else {
-      const int64_t base = ((int64_t)(b * a.n_q + h) * a.R + row) * a.S + blockIdx.y;
+      const int64_t base = ((int64_t)(b * a.n_q + h) * a.R + row) * a.S + split;
       if (l_tot > 0.f) {
         float* op = a.Opart + base * HD;
 #pragma unroll
@@ -491,8 +501,8 @@ hipError_t run_attention_bf16(const AttnArgs& a, hipStream_t st) {
   const int nrows = (a.n_q / a.n_kv) * a.R;
   {
     Phase ph("attn_ctx", st);
-    dim3 grid((nrows + kRowsPerWG - 1) / kRowsPerWG, a.S, a.B * a.n_kv);
-    hipLaunchKernelGGL((attn_mfma<HD, kAttnWaves, kAttnTiles, STAGES>), grid, dim3(64 * kAttnWaves), lds, st, a);
+    const int grid = (nrows + kRowsPerWG - 1) / kRowsPerWG * a.S * a.B * a.n_kv;
+    hipLaunchKernelGGL((attn_mfma<HD, kAttnWaves, kAttnTiles, STAGES>), dim3(grid), dim3(64 * kAttnWaves), lds, st, a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.S == 1) return e;

@@ -267,6 +267,15 @@ def test_full_size_qwen3_8b_b16():
     _full_size("qwen3_8b_b16", samples)
 
 
+def test_full_size_qwen3_14b_b8():
+    """Qwen3-14B-shaped drafter (hidden 5120, 40/8 heads, FFN 17408), batch 8 at context 8192:
+    the accepted branch of the first and last request against the oracle, head teacher-forced."""
+    wl = synth.WORKLOADS["qwen3_14b_b8"]
+    ri = synth.make_round(wl)
+    samples = [(b, [int(ri.accept_planted[b])]) for b in (0, wl.batch - 1)]
+    _full_size("qwen3_14b_b8", samples)
+
+
 # ----------------------------------------------------------------------------- target verification forward
 TARGET_SMALL = synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=512,
                                   vocab=3001, gamma=5, ar_rank=64, qk_norm=True, dtype="bf16")
