@@ -223,7 +223,7 @@ def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
     g, H, V = shape.gamma, shape.hidden, shape.vocab
     gen = torch.Generator(device="cuda")
     gen.manual_seed(1234)
-    out = {}
+    out, fallback = {}, {}
     for B in batches:
         ws = D.Workspace(dr.d.cfg, B, 64)
         reps = torch.randn((B, g + 1, g, H), generator=gen, device="cuda", dtype=torch.float32)
@@ -243,8 +243,9 @@ def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
         torch.cuda.synchronize()
         assert ws.status() == 0, f"device status {ws.status()}"
         out[str(B)] = 1000.0 * e0.elapsed_time(e1) / iters
+        fallback[str(B)] = ws.head_fallback()
         del ws, reps
-    return out
+    return out, fallback
 
 
 def main():
@@ -369,12 +370,13 @@ def main():
                      "hbm_frac": bb_bytes / bb_s / 1e9 / PEAK_HBM_GBS,
                      "mfma_frac": bb_flops / bb_s / 1e12 / peak_flops},
         "head_us_per_round": head_us,
+        "head_full_fallback": dr.head_fallback(),
         "verify_us_per_round": 1000.0 * sum_ms(["verify"]),
         "append_us_per_round": 1000.0 * sum_ms(["append_gemm", "append_store"]),
         "phases": phases,
     }
     if shape.dtype == "bf16" and not args.no_head_sweep:
-        out["head_us_by_batch"] = head_sweep(dr, shape)
+        out["head_us_by_batch"], out["head_full_fallback_by_batch"] = head_sweep(dr, shape)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(wl, weights, ri)

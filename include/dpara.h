@@ -171,11 +171,17 @@ int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* ta
  *         y_i = argmax z_i (lowest index on ties).
  * next_spine: [batch, gamma+1] int32 (device): (bonus, y_1..y_gamma).
  * margins: [batch, gamma] float32 (device, may be NULL): top1 - top2 of z_i.
- * bf16 drafters with ar_rank in {64, 128, 256, 512}, vocab <= 2^18 and batch <= 16 run the
- * gamma head steps in one launch that needs all of its workgroups resident at once (one
- * per CU); if the GPU is shared so that they cannot all run, the launch gives up after
- * about 0.3 s per step and sets DPARA_STATUS_HEAD_TIMEOUT.  Other configurations launch
- * one kernel per step. */
+ * With ar_rank in {64, 128, 256}, vocab >= 64 and gamma <= 63 the steps first run exactly
+ * over a few candidates per step: the 16 largest l_i and a bound from the largest
+ * remaining logit plus max_v |ar_W[v]| |ar_E[y_{i-1}]| (Cauchy-Schwarz), which proves the
+ * step's top two when both candidates exceed it.  If any step of any request is not
+ * proven, the int32 at byte offset 4 of `ws` is left nonzero (diagnostic; 0 otherwise) and
+ * the full head below recomputes every request; the results are the same either way.
+ * The full head: bf16 drafters with ar_rank in {64, 128, 256}, vocab <= 2^18 and
+ * batch <= 16 run the gamma head steps in one launch that needs all of its workgroups
+ * resident at once (one per CU); if the GPU is shared so that they cannot all run, the
+ * launch gives up after about 0.3 s per step and sets DPARA_STATUS_HEAD_TIMEOUT.  Other
+ * configurations launch one kernel per step. */
 int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
                           const float* reps, const int32_t* accept_len, const int32_t* bonus,
                           float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,

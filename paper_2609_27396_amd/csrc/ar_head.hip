@@ -139,8 +139,6 @@ __device__ bool arp_poll(const uint64_t* part, int s, int B, int G, int V, uint3
   return true;
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
 // Branch-free top-2 tracking: (k1, v1) best key and its value, v2 second-best value.
 struct Top2 {
   uint64_t k1;
@@ -165,7 +163,9 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
                                                                      const int* bonus, int* drafts,
                                                                      int* next_spine, float* margins,
                                                                      uint64_t* part, int* status,
-                                                                     uint32_t spin_limit) {
+                                                                     uint32_t spin_limit, const int* only_if) {
+  // Every workgroup reads the same flag, so all of them leave together.
+  if (only_if && *only_if == 0) return;
   constexpr int RANK = NKB * 32;
   constexpr int ROWS_WAVE = 16 * NRB;
   constexpr int ROWS_WG = NW * ROWS_WAVE;
@@ -313,7 +313,7 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
 template <int NKB, int NRB, int NW>
 hipError_t arp_launch(int B, int gamma, int V, const float* logits, const void* E, const void* W, const int* bonus,
                       int* drafts, int* next_spine, float* margins, uint64_t* part, int part_grid, int* status,
-                      hipStream_t st) {
+                      const int* only_if, hipStream_t st) {
   constexpr int ROWS_WG = NW * 16 * NRB;
   const int G = (V + ROWS_WG - 1) / ROWS_WG;
   if (G > part_grid || G > kArpMaxGrid) return hipErrorNotSupported;
@@ -328,7 +328,7 @@ hipError_t arp_launch(int B, int gamma, int V, const float* logits, const void* 
   Phase ph("ar_step", st);
   hipLaunchKernelGGL((ar_head_persistent<NKB, NRB, NW>), dim3(G), dim3(64 * NW), 0, st, gamma, V, B, logits,
                      (const bf16_t*)E, (const bf16_t*)W, bonus, drafts, next_spine, margins, part, status,
-                     spin_limit);
+                     spin_limit, only_if);
   return hipGetLastError();
 }
 
@@ -345,14 +345,14 @@ int ar_persistent_grid(int rank, int V) {
 
 hipError_t launch_ar_head_persistent(int B, int gamma, int V, int rank, const float* logits, const void* E,
                                      const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                                     uint64_t* part, int part_grid, int* status, hipStream_t st) {
+                                     uint64_t* part, int part_grid, int* status, const int* only_if, hipStream_t st) {
   if (B < 1 || B > kArpMaxB || V > (int)kArpIdxMask + 1 || V % 4 || V < 4 || gamma < 1 ||
       gamma >= (1 << kArpTagBits) || (uintptr_t)logits % 16)
     return hipErrorNotSupported;
   switch (rank) {
-    case 64: return arp_launch<2, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
-    case 128: return arp_launch<4, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
-    case 256: return arp_launch<8, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, st);
+    case 64: return arp_launch<2, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, only_if, st);
+    case 128: return arp_launch<4, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, only_if, st);
+    case 256: return arp_launch<8, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, only_if, st);
     default: return hipErrorNotSupported;
   }
 }

@@ -60,15 +60,6 @@ __device__ __forceinline__ int grp_rows(const AttnArgs& a) { return (a.n_q / a.n
 // Key offset within a 64-key block held by S^T row i of 16-key MFMA block kb.
 __device__ __forceinline__ int key_perm(int kb, int i) { return (kb >> 1) * 32 + (i >> 2) * 8 + (kb & 1) * 4 + (i & 3); }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14];
-  // expcnt and lgkmcnt are left at their maxima (no wait on them).
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | (((N >> 4) & 3) << 14));
-}
-
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -346,10 +337,13 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
 }
 
 // Folds the S partials of one (request, head, row): 4 head_dim entries per thread.
-// Partials with l == 0 saw no key and are skipped (their O was not written).
+// Partials with l == 0 saw no key and are skipped (their O was not written): every
+// partial is loaded up front, so the loads overlap, and an unwritten one is replaced by
+// zero with a select (never multiplied), so that stale memory cannot reach the result.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_fold(AttnArgs a) {
   constexpr int TPR = HD / 4;  // threads per (request, head, row)
+  constexpr int SMAX = kMaxAttnSplits;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t task = t / TPR;
   if (task >= (int64_t)a.B * a.n_q * a.R) return;
@@ -357,21 +351,30 @@ __global__ __launch_bounds__(256) void attn_fold(AttnArgs a) {
   const int row = (int)(task % a.R);
   const int bh = (int)(task / a.R), h = bh % a.n_q, b = bh / a.n_q;
   const int64_t pbase = task * a.S;
+  float2 ml[SMAX];
+  float4 v[SMAX];
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < a.S) {
+      ml[s] = *(const float2*)(a.MLpart + (pbase + s) * 2);
+      v[s] = *(const float4*)(a.Opart + (pbase + s) * HD + c * 4);
+    }
   float M = -INFINITY;
-  for (int s = 0; s < a.S; ++s)
-    if (a.MLpart[(pbase + s) * 2 + 1] > 0.f) M = fmaxf(M, a.MLpart[(pbase + s) * 2]);
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < a.S && ml[s].y > 0.f) M = fmaxf(M, ml[s].x);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float Ls = 0.f;
-  for (int s = 0; s < a.S; ++s) {
-    const float ls = a.MLpart[(pbase + s) * 2 + 1];
-    if (!(ls > 0.f)) continue;
-    const float w = exp2f(a.MLpart[(pbase + s) * 2] - M);
-    Ls += ls * w;
-    const float4 v = *(const float4*)(a.Opart + (pbase + s) * HD + c * 4);
-    acc.x += v.x * w;
-    acc.y += v.y * w;
-    acc.z += v.z * w;
-    acc.w += v.w * w;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    if (s >= a.S) continue;
+    const bool live = ml[s].y > 0.f;
+    const float w = live ? exp2f(ml[s].x - M) : 0.f;
+    Ls += live ? ml[s].y * w : 0.f;
+    acc.x += live ? v[s].x * w : 0.f;
+    acc.y += live ? v[s].y * w : 0.f;
+    acc.z += live ? v[s].z * w : 0.f;
+    acc.w += live ? v[s].w * w : 0.f;
   }
   const float inv = Ls > 0.f ? 1.0f / Ls : 0.f;
   bf16_t* op = (bf16_t*)a.O + (int64_t)(b * a.R + row) * (a.n_q * HD) + h * HD + c * 4;
@@ -536,7 +539,7 @@ hipError_t run_attention_scalar(const AttnArgs& a, hipStream_t st) {
 int attn_rows_per_workgroup() { return kRowsPerWG; }
 
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
-  if (a.Rp < a.R || a.Rp % kKeyBlock || a.S < 1) return hipErrorInvalidValue;
+  if (a.Rp < a.R || a.Rp % kKeyBlock || a.S < 1 || a.S > kMaxAttnSplits) return hipErrorInvalidValue;
   if (dtype == 1) return a.hd == 128 ? run_attention_bf16<128>(a, st) : run_attention_bf16<64>(a, st);
   if (a.S != 1) return hipErrorInvalidValue;
   return a.hd == 128 ? run_attention_scalar<float, 128>(a, st) : run_attention_scalar<float, 64>(a, st);

@@ -63,6 +63,46 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
+// Generic LDS pointer type of the direct global->LDS DMA builtin.
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Wait until at most N vector-memory loads (DMA included) of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14];
+  // expcnt and lgkmcnt are left at their maxima (no wait on them).
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | (((N >> 4) & 3) << 14));
+}
+
+// Cross-lane moves inside 16-lane rows by DPP (no LDS round trip): quad_perm xor 1 and
+// xor 2, then the half-row and row mirrors.  After the four steps every lane of a row
+// holds the row's reduction.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) { return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(v))); }
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  return ((uint64_t)dpp_u32<CTRL>((uint32_t)(v >> 32)) << 32) | dpp_u32<CTRL>((uint32_t)v);
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f<kDppXor1>(v);
+  v += dpp_f<kDppXor2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return v;
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return v;
+}
+
 // Orderable 64-bit key: larger value wins, and on equal values the LOWER index wins.
 __device__ __forceinline__ uint64_t argmax_key(float v, uint32_t idx) {
   uint32_t u = __float_as_uint(v);
@@ -82,6 +122,18 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     v = w > v ? w : v;
   }
   return v;
+}
+
+// Merge (key1, second-best value) pairs.
+__device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1, float ov2) {
+  const float va = k1 ? key_value(k1) : -INFINITY;
+  const float vb = ok1 ? key_value(ok1) : -INFINITY;
+  if (ok1 > k1) {
+    v2 = fmaxf(fmaxf(v2, ov2), va);
+    k1 = ok1;
+  } else {
+    v2 = fmaxf(fmaxf(v2, ov2), vb);
+  }
 }
 
 // Status word (int32 at byte offset 0 of the workspace).

@@ -114,7 +114,8 @@ struct Plan {
   int B, R, Rp, M, S, chunk, CH, esz;
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   int v_chunk, v_chunks, h_chunk, h_chunks;
-  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, F, KV32, rope_app;
+  size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
+      hflag, F, KV32, rope_app;
   int ar_grid;  // persistent AR head grid (0: step kernels only)
   size_t total;
 };
@@ -137,7 +138,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
     const int base = B * nkv * tiles;
     const int max_blocks = (ctx_cap + 63) / 64 + p.Rp / 64;
     int S = DPARA_ATTN_TARGET_WG / base;
-    const int max_s = max_blocks / 2;
+    const int max_s = min(max_blocks / 2, kMaxAttnSplits);
     if (S > max_s) S = max_s;
     if (S < 1) S = 1;
     p.S = S;
@@ -181,6 +182,9 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.hpart = take((size_t)2 * B * p.h_chunks * 16);  // two step-parity slots
   p.ar_grid = (c->dtype == DPARA_BF16 && B <= 16) ? ar_persistent_grid(c->ar_rank, c->vocab) : 0;
   p.arpart = take((size_t)2 * 16 * p.ar_grid * 16);  // persistent head: [2][16][grid] x 2 words
+  p.hcand = take(head_prune_cand_bytes(B * c->gamma, c->vocab));  // pruned head: candidate keys
+  p.hwpart = take((size_t)head_prune_wparts() * 4);                // pruned head: |W_v|^2 maxima
+  p.hflag = 4;  // pruned head: fallback flag, int32 in the header after the status word
   p.F = take((size_t)B * p.CH * H * p.esz);
   // append K|V planes: split only when the append GEMM has at most 320 rows (16 planes max)
   const size_t kv_rows = (size_t)B * p.CH > 16 * 320 ? (size_t)B * p.CH : 16 * 320;
@@ -628,7 +632,7 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   const Plan p = make_plan(cfg, batch, 64);
   if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
-  const size_t need = p.arpart + up256((size_t)2 * 16 * p.ar_grid * 16);
+  const size_t need = p.hwpart + up256((size_t)head_prune_wparts() * 4);
   if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
   if ((rc = check_device())) return rc;
 
@@ -656,9 +660,17 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
     Phase ph("lm_head", st);
     HIP_TRY(launch_gemm(bf ? A_BF16_DUAL : A_F32, EPI_STORE_F32, lm, st), "lm head gemm");
   }
+  // Exact bound-pruned steps first; the full head then runs only if some step could not be
+  // decided from the candidates (its kernels return at once otherwise).
+  int* hflag = at<int>(ws, p.hflag);
+  const hipError_t pe = launch_head_pruned(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits),
+                                           w->ar_E, w->ar_W, bonus, drafts, next_spine, margins,
+                                           at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart), hflag, status, st);
+  if (pe != hipSuccess && pe != hipErrorNotSupported) return hip_fail(pe, "pruned head");
   HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
-                         p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status, st),
+                         p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status,
+                         pe == hipSuccess ? hflag : nullptr, st),
           "ar head");
   return DPARA_OK;
 }

@@ -69,15 +69,6 @@ __device__ __forceinline__ int b_frag_row(int wn, int ni) {
 // counts outstanding DMA instructions), then one s_barrier makes every wave's part of that
 // stage visible; the refill of the ring slot freed by the previous iteration is issued
 // right after the barrier, so STAGES-1 stages are in flight while one is consumed.
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14];
-  // expcnt and lgkmcnt are left at their maxima (no wait on them).
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | (((N >> 4) & 3) << 14));
-}
-
 template <int CH>
 __device__ __forceinline__ int swz(int r, int c) {
   if (CH == 8) return c ^ (r & 7);

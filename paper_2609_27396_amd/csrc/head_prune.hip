@@ -1,0 +1,396 @@
+// Exact bound-pruned AR head.
+//
+// The head step y_i = argmax_v z_v with z_v = l_v + W_v . E(y_{i-1}) (head equation of
+// Section 3.2) needs the whole vocabulary only when the correction W_v . e can reorder the
+// logits far down the list.  By Cauchy-Schwarz every v has
+//     z_v <= l_v + max_u |W_u| |e|,
+// so if K candidates C hold the K largest logits and L is the largest logit outside C,
+// every v outside C has z_v <= L + max_u |W_u| |e|.  When the best and the second best z
+// over C both exceed that bound, they are the top two over the whole vocabulary: the
+// step's argmax and its top1 - top2 margin are exact, and the step costs K dot products of
+// length ar_rank instead of a sweep over all V rows of W.
+//
+//   logit_topk      per (row, vocabulary split): the kTopK largest logit keys and the
+//                   (kTopK+1)-th, in descending order.  The threshold is the (kTopK+1)-th
+//                   largest of the 256 per-thread maxima (at least kTopK+1 elements are at
+//                   or above it), found by rank counting in LDS; a second pass collects the
+//                   elements at or above it and ranks them the same way.
+//   w_rownorm_max   per-workgroup maxima of |W_v|^2 (16 lanes per row); the first
+//                   workgroup also clears the fallback flag.
+//   ar_pruned       one workgroup per request runs all gamma steps.  A 16-lane row per head
+//                   row merges the split lists (one list per lane, DPP row maxima) into the
+//                   global top kTopK and the bound, the (kTopK+1)-th key: every logit left
+//                   out of a split's list is at most that split's last key, which no more
+//                   than kTopK keys of the union exceed.  Per step, 16 lanes per candidate
+//                   take the dot product W_v . e over rank slices; the candidates of step
+//                   i+1 depend on the row only, so their W and E rows are fetched while step
+//                   i runs, and the winner's E row is already in registers when it ends.
+//
+// A row whose candidate collection overflows, or a step whose bound does not hold, sets
+// the fallback flag; the full head (launch_ar_head with only_if = flag) then recomputes
+// every request and overwrites these results.  Keys are the argmax keys of common.h
+// (larger value wins, the lower index on ties), as in the full head.
+#include <math.h>
+
+#include "common.h"
+#include "internal.h"
+
+namespace dpara {
+namespace {
+
+constexpr int kTopK = 16;         // candidates kept per row
+constexpr int kKeys = kTopK + 1;  // + the bound key
+constexpr int kCollect = 512;     // collection buffer of the second pass
+constexpr int kMaxGamma = 63;
+constexpr int kMaxSplits = 16;
+
+// EPL contiguous elements from p as float, in 16-byte (or 8-byte) pieces.
+template <typename T, int EPL>
+__device__ __forceinline__ void load_piece(const T* p, float (&r)[EPL]) {
+  constexpr int BYTES = EPL * (int)sizeof(T);
+  constexpr int PB = BYTES % 16 == 0 ? 16 : 8;
+  constexpr int EPW = 4 / (int)sizeof(T);  // elements per 32-bit word
+#pragma unroll
+  for (int q = 0; q < BYTES / PB; ++q) {
+    uint32_t w[PB / 4];
+    if constexpr (PB == 16) {
+      const uint4 u = ((const uint4*)p)[q];
+      w[0] = u.x;
+      w[1] = u.y;
+      w[2] = u.z;
+      w[3] = u.w;
+    } else {
+      const uint2 u = ((const uint2*)p)[q];
+      w[0] = u.x;
+      w[1] = u.y;
+    }
+#pragma unroll
+    for (int i = 0; i < PB / 4; ++i) {
+      if constexpr (EPW == 2) {
+        r[(q * (PB / 4) + i) * 2] = __uint_as_float(w[i] << 16);
+        r[(q * (PB / 4) + i) * 2 + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+      } else {
+        r[q * (PB / 4) + i] = __uint_as_float(w[i]);
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ uint64_t row16_max_u64(uint64_t k) {
+  uint64_t o = dpp_u64<kDppXor1>(k);
+  k = o > k ? o : k;
+  o = dpp_u64<kDppXor2>(k);
+  k = o > k ? o : k;
+  o = dpp_u64<kDppHalfMirror>(k);
+  k = o > k ? o : k;
+  o = dpp_u64<kDppMirror>(k);
+  return o > k ? o : k;
+}
+
+// Rows of V float32 logits; split sp covers [sp*per, min(V, (sp+1)*per)).  With V % 4 == 0
+// and per % 4 == 0 the scans read 16-byte pieces.
+template <typename F>
+__device__ __forceinline__ void scan_split(const float* x, int v0, int v1, bool vec, F&& fn) {
+  const int tid = threadIdx.x;
+  if (vec) {
+    // four 16-byte loads in flight per thread
+    const float4* x4 = (const float4*)x;
+    const int q1 = v1 >> 2;
+    for (int q = (v0 >> 2) + tid; q < q1; q += 1024) {
+      float4 f[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (q + 256 * u < q1) f[u] = x4[q + 256 * u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (q + 256 * u < q1) {
+          const int v = 4 * (q + 256 * u);
+          fn(f[u].x, v);
+          fn(f[u].y, v + 1);
+          fn(f[u].z, v + 2);
+          fn(f[u].w, v + 3);
+        }
+    }
+  } else {
+    for (int v = v0 + tid; v < v1; v += 1024) {
+      float f[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v + 256 * u < v1) f[u] = x[v + 256 * u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v + 256 * u < v1) fn(f[u], v + 256 * u);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void logit_topk(const float* logits, int V, int S, int per, uint64_t* out,
+                                                  int* flag) {
+  __shared__ __attribute__((aligned(16))) uint64_t tm[256];
+  __shared__ uint64_t buf[kCollect];
+  __shared__ uint64_t thr;
+  __shared__ int cnt;
+  const int row = blockIdx.y, sp = blockIdx.x, tid = threadIdx.x;
+  const int v0 = sp * per, v1 = min(V, v0 + per);
+  const bool vec = (V & 3) == 0 && (per & 3) == 0;
+  const float* x = logits + (int64_t)row * V;
+
+  uint64_t best = 0;
+  scan_split(x, v0, v1, vec, [&](float f, int v) {
+    const uint64_t k = argmax_key(f, (uint32_t)v);
+    best = k > best ? k : best;
+  });
+  tm[tid] = best;
+  if (tid == 0) {
+    cnt = 0;
+    thr = 0;
+  }
+  __syncthreads();
+  // rank of this thread's maximum among the 256 (keys are unique; empty threads hold 0)
+  int r = 0;
+  for (int j = 0; j < 256; j += 2) {
+    const uint4 u = *(const uint4*)&tm[j];
+    r += (((uint64_t)u.y << 32 | u.x) > best) + (((uint64_t)u.w << 32 | u.z) > best);
+  }
+  if (r == kTopK && best != 0) thr = best;
+  __syncthreads();
+  const uint64_t T = thr;
+  if (T != 0) {
+    scan_split(x, v0, v1, vec, [&](float f, int v) {
+      const uint64_t k = argmax_key(f, (uint32_t)v);
+      if (k >= T) {
+        const int pos = atomicAdd(&cnt, 1);
+        if (pos < kCollect) buf[pos] = k;
+      }
+    });
+  }
+  __syncthreads();
+  const int n = cnt;
+  if (T == 0 || n > kCollect) {
+    // not decidable here (a split of fewer than kKeys elements cannot occur: the launcher
+    // keeps at least 64 per split); the full head takes over
+    if (tid == 0) atomicOr(flag, 1);
+    return;
+  }
+  uint64_t* o = out + ((int64_t)row * S + sp) * kKeys;
+  for (int e = tid; e < n; e += 256) {
+    const uint64_t k = buf[e];
+    int rr = 0;
+    for (int j = 0; j < n; ++j) rr += buf[j] > k;
+    if (rr < kKeys) o[rr] = k;
+  }
+}
+
+template <typename T, int RANK>
+__global__ __launch_bounds__(256) void w_rownorm_max(const T* W, int V, float* partial, int* flag) {
+  constexpr int EPL = RANK / 16;
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0 && tid == 0) *flag = 0;
+  const int per = (V + gridDim.x - 1) / gridDim.x;
+  const int v0 = blockIdx.x * per, v1 = min(V, v0 + per);
+  const int sub = tid & 15, grp = tid >> 4;  // a 16-lane row reads one W row
+  float mx = 0.f;
+  for (int v = v0 + grp; v < v1; v += 64) {  // four rows per 16-lane row in flight
+    float r[4][EPL];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (v + 16 * u < v1) load_piece<T, EPL>(W + (int64_t)(v + 16 * u) * RANK + sub * EPL, r[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (v + 16 * u < v1) {
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < EPL; ++j) s = fmaf(r[u][j], r[u][j], s);
+        mx = fmaxf(mx, row16_sum(s));
+      }
+  }
+  mx = wave_max(mx);
+  if ((tid & 63) == 0) red[tid >> 6] = mx;
+  __syncthreads();
+  if (tid == 0) partial[blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+template <typename T, int EPT>
+__global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const uint64_t* cand,
+                                                 const float* wpart, int n_wpart, const T* E, const T* W,
+                                                 const int* bonus, int* drafts, int* next_spine, float* margins,
+                                                 int* flag, int* status) {
+  constexpr int RANK = 16 * EPT;
+  __shared__ uint64_t lists[16][kMaxSplits * kKeys];  // the split lists of 16 rows in flight
+  __shared__ uint64_t ck[kMaxGamma][kKeys];           // per row: top kTopK keys, then the bound key
+  __shared__ float es[RANK];                          // E(y_{i-1})
+  __shared__ float zs[kTopK];
+  __shared__ float red[4];
+  __shared__ int ybc, stop;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kc = tid >> 4, slice = tid & 15;  // 16-lane row kc: candidate kc, rank slice `slice`
+
+  int y0 = bonus[b];
+  if (y0 < 0 || y0 >= V) {
+    if (tid == 0) raise_status(status, 1);
+    y0 = 0;
+  }
+  if (tid == 0) {
+    next_spine[b * (gamma + 1)] = y0;
+    stop = *flag;  // some candidate row was not decidable: the full head recomputes everything
+  }
+  float wm = 0.f;
+  for (int i = tid; i < n_wpart; i += 256) wm = fmaxf(wm, wpart[i]);
+  wm = wave_max(wm);
+  if (lane == 0) red[wave] = wm;
+  if (tid < RANK) es[tid] = ld_f(E + (int64_t)y0 * RANK + tid);
+
+  // merge: 16 head rows at a time, lane `slice` of row kc walks split list `slice`
+  for (int j0 = 0; j0 < gamma; j0 += 16) {
+    const int nrow = min(16, gamma - j0);
+    for (int i = tid; i < nrow * S * kKeys; i += 256) {
+      const int rr = i / (S * kKeys), q = i % (S * kKeys);
+      lists[rr][q] = cand[((int64_t)(b * gamma + j0 + rr)) * S * kKeys + q];
+    }
+    __syncthreads();
+    if (kc < nrow) {
+      int pos = 0;
+      uint64_t head = slice < S ? lists[kc][slice * kKeys] : 0;
+      for (int t = 0; t < kKeys; ++t) {
+        const uint64_t m = row16_max_u64(head);
+        if (slice == 0) ck[j0 + kc][t] = m;
+        if (head == m && head != 0) {
+          ++pos;
+          head = pos < kKeys ? lists[kc][slice * kKeys + pos] : 0;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (stop) return;
+  const float wmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * (1.0f + 1e-5f);
+
+  // candidate indices are clamped into the vocabulary (keys of a complete list always are)
+  auto cand_v = [&](uint64_t k) { return (int)min(key_index(k), (uint32_t)(V - 1)); };
+  float wr[EPT], er[EPT];
+  {
+    const int v = cand_v(ck[0][kc]);
+    load_piece<T, EPT>(W + (int64_t)v * RANK + slice * EPT, wr);
+    load_piece<T, EPT>(E + (int64_t)v * RANK + slice * EPT, er);
+  }
+  for (int i = 1; i <= gamma; ++i) {
+    float wn[EPT], en[EPT];
+    if (i < gamma) {  // step i+1's candidate rows
+      const int vn = cand_v(ck[i][kc]);
+      load_piece<T, EPT>(W + (int64_t)vn * RANK + slice * EPT, wn);
+      load_piece<T, EPT>(E + (int64_t)vn * RANK + slice * EPT, en);
+    }
+    float d = 0.f, ee = 0.f;
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      const float ej = es[slice * EPT + j];
+      d = fmaf(wr[j], ej, d);
+      ee = fmaf(ej, ej, ee);
+    }
+    d = row16_sum(d);
+    ee = row16_sum(ee);
+    const uint64_t key = ck[i - 1][kc];
+    if (slice == 0) zs[kc] = key_value(key) + d;
+    __syncthreads();
+    if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
+      uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
+      float v2 = -INFINITY;
+      top2_merge(k1, v2, dpp_u64<kDppXor1>(k1), dpp_f<kDppXor1>(v2));
+      top2_merge(k1, v2, dpp_u64<kDppXor2>(k1), dpp_f<kDppXor2>(v2));
+      top2_merge(k1, v2, dpp_u64<kDppHalfMirror>(k1), dpp_f<kDppHalfMirror>(v2));
+      top2_merge(k1, v2, dpp_u64<kDppMirror>(k1), dpp_f<kDppMirror>(v2));
+      if (tid == 0) {
+        const float lb = key_value(ck[i - 1][kTopK]);
+        const float bound = lb + wmax * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
+        const bool ok = v2 > bound;
+        const int y = (int)key_index(k1);
+        if (ok) {
+          drafts[b * gamma + i - 1] = y;
+          next_spine[b * (gamma + 1) + i] = y;
+          if (margins) margins[b * gamma + i - 1] = key_value(k1) - v2;
+        } else {
+          atomicOr(flag, 2);
+        }
+        stop = ok ? 0 : 1;
+        ybc = y;
+      }
+    }
+    __syncthreads();
+    if (stop) return;
+    if (i < gamma) {
+      if ((int)key_index(key) == ybc) {  // the winner's row holds E(y_i)
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) es[slice * EPT + j] = er[j];
+      }
+#pragma unroll
+      for (int j = 0; j < EPT; ++j) {
+        wr[j] = wn[j];
+        er[j] = en[j];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+int head_prune_splits(int rows, int V) {
+  int S = 256 / (rows > 0 ? rows : 1);
+  if (S > kMaxSplits) S = kMaxSplits;
+  while (S > 1 && V / S < 64) --S;
+  return S < 1 ? 1 : S;
+}
+
+int head_prune_wparts() { return 512; }
+
+bool head_prune_supported(int dtype, int gamma, int V, int rank) {
+  return gamma >= 1 && gamma <= kMaxGamma && V >= 64 && (rank == 64 || rank == 128 || rank == 256) &&
+         (dtype == 0 || dtype == 1);
+}
+
+size_t head_prune_cand_bytes(int rows, int V) { return (size_t)rows * head_prune_splits(rows, V) * kKeys * 8; }
+
+hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
+                              const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
+                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st) {
+  if (!head_prune_supported(dtype, gamma, V, rank) || B < 1) return hipErrorNotSupported;
+  const int rows = B * gamma;
+  const int S = head_prune_splits(rows, V);
+  const int per = ((V + S - 1) / S + 3) / 4 * 4;
+  const int nw = head_prune_wparts();
+  Phase ph("ar_step", st);
+#define DPARA_WNORM(TT, RK) \
+  hipLaunchKernelGGL((w_rownorm_max<TT, RK>), dim3(nw), dim3(256), 0, st, (const TT*)W, V, wpart, flag)
+  if (dtype == 1) {
+    if (rank == 64) DPARA_WNORM(bf16_t, 64);
+    else if (rank == 128) DPARA_WNORM(bf16_t, 128);
+    else DPARA_WNORM(bf16_t, 256);
+  } else {
+    if (rank == 64) DPARA_WNORM(float, 64);
+    else if (rank == 128) DPARA_WNORM(float, 128);
+    else DPARA_WNORM(float, 256);
+  }
+#undef DPARA_WNORM
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(logit_topk, dim3(S, rows), dim3(256), 0, st, logits, V, S, per, cand, flag);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+#define DPARA_PRUNED(TT, EPT)                                                                             \
+  hipLaunchKernelGGL((ar_pruned<TT, EPT>), dim3(B), dim3(256), 0, st, gamma, V, S, cand, wpart, nw,      \
+                     (const TT*)E, (const TT*)W, bonus, drafts, next_spine, margins, flag, status)
+  if (dtype == 1) {
+    if (rank == 64) DPARA_PRUNED(bf16_t, 4);
+    else if (rank == 128) DPARA_PRUNED(bf16_t, 8);
+    else DPARA_PRUNED(bf16_t, 16);
+  } else {
+    if (rank == 64) DPARA_PRUNED(float, 4);
+    else if (rank == 128) DPARA_PRUNED(float, 8);
+    else DPARA_PRUNED(float, 16);
+  }
+#undef DPARA_PRUNED
+  return hipGetLastError();
+}
+
+}  // namespace dpara

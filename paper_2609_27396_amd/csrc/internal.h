@@ -68,6 +68,9 @@ struct AttnArgs {
   int spine_only;      // 1: rows are only the causal spine (no branches)
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st);
+// Largest key split S of the bf16 path (the fold kernel holds every partial of a row in
+// registers).
+constexpr int kMaxAttnSplits = 16;
 int attn_rows_per_workgroup();  // query rows (over the heads of a KV group) per bf16 workgroup
 
 // ---------------------------------------------------------------- elementwise
@@ -116,12 +119,28 @@ int ar_head_chunk(int dtype, int rank);  // vocabulary rows per AR-step workgrou
 int ar_persistent_grid(int rank, int V);
 hipError_t launch_ar_head_persistent(int B, int gamma, int V, int rank, const float* logits, const void* E,
                                      const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                                     uint64_t* part, int part_grid, int* status, hipStream_t st);
+                                     uint64_t* part, int part_grid, int* status, const int* only_if,
+                                     hipStream_t st);
 // bf16 with ppart (zero tags, ppart_grid = ar_persistent_grid) runs the persistent head when
-// the device allows it; otherwise gamma+1 step kernels with partials in `part`.
+// the device allows it; otherwise gamma+1 step kernels with partials in `part`.  With a
+// non-NULL only_if, every kernel returns at once unless *only_if != 0 when it runs.
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits,
                           const void* E, const void* W, const int* bonus, int* drafts,
                           int* next_spine, float* margins, uint64_t* part, int n_chunks,
-                          int chunk, uint64_t* ppart, int ppart_grid, int* status, hipStream_t st);
+                          int chunk, uint64_t* ppart, int ppart_grid, int* status, const int* only_if,
+                          hipStream_t st);
+// Exact bound-pruned head (head_prune.hip): top candidates per logit row, the largest W row
+// norm, then all gamma steps over the candidates only.  Where a row or a step cannot be
+// decided exactly it sets *flag != 0 (the flag is cleared first), and the caller runs
+// launch_ar_head with only_if = flag, which recomputes every request.  `cand` holds
+// head_prune_cand_bytes(B * gamma, V) bytes, `wpart` head_prune_wparts() floats.
+// Returns hipErrorNotSupported (nothing launched) outside head_prune_supported().
+bool head_prune_supported(int dtype, int gamma, int V, int rank);
+int head_prune_splits(int rows, int V);
+int head_prune_wparts();
+size_t head_prune_cand_bytes(int rows, int V);
+hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
+                              const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
+                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st);
 
 }  // namespace dpara

@@ -123,18 +123,6 @@ __global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const flo
   }
 }
 
-// Merge (key1, second-best value) pairs.
-__device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1, float ov2) {
-  const float va = k1 ? key_value(k1) : -INFINITY;
-  const float vb = ok1 ? key_value(ok1) : -INFINITY;
-  if (ok1 > k1) {
-    v2 = fmaxf(fmaxf(v2, ov2), va);
-    k1 = ok1;
-  } else {
-    v2 = fmaxf(fmaxf(v2, ov2), vb);
-  }
-}
-
 // Rows per 8-lane group of the prefetching AR step for P 16-byte pieces per lane per row:
 // NR * P <= 32 pieces (128 VGPRs) in flight per lane.
 __host__ __device__ constexpr int ar_rows_per_group(int P) { return P <= 4 ? 8 : (P <= 8 ? 4 : 0); }
@@ -208,7 +196,8 @@ template <typename T>
 __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int rank, const float* logits,
                                                const T* E, const T* W, const int* bonus, int* drafts,
                                                int* next_spine, float* margins, uint64_t* part,
-                                               int n_chunks, int chunk, int B, int* status) {
+                                               int n_chunks, int chunk, int B, int* status, const int* only_if) {
+  if (only_if && *only_if == 0) return;
   __shared__ float e[1024];
   __shared__ uint64_t rk[4];
   __shared__ float rv[4];
@@ -280,7 +269,8 @@ template <typename T, int P>
 __global__ __launch_bounds__(256) void ar_step_pf(int step, int gamma, int V, int rank, const float* logits,
                                                   const T* E, const T* W, const int* bonus, int* drafts,
                                                   int* next_spine, float* margins, uint64_t* part,
-                                                  int n_chunks, int chunk, int B, int* status) {
+                                                  int n_chunks, int chunk, int B, int* status, const int* only_if) {
+  if (only_if && *only_if == 0) return;
   constexpr int NR = ar_rows_per_group(P);
   __shared__ __attribute__((aligned(16))) float e[1024];
   __shared__ uint64_t rk[4];
@@ -425,19 +415,20 @@ int ar_head_chunk(int dtype, int rank) {
 template <typename T, int P>
 hipError_t launch_ar_pf(dim3 grid, hipStream_t st, int step, int gamma, int V, int rank, const float* logits,
                         const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
-                        float* margins, uint64_t* part, int n_chunks, int chunk, int B, int* status) {
+                        float* margins, uint64_t* part, int n_chunks, int chunk, int B, int* status,
+                        const int* only_if) {
   hipLaunchKernelGGL((ar_step_pf<T, P>), grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const T*)E,
-                     (const T*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+                     (const T*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status, only_if);
   return hipGetLastError();
 }
 
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                           const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                           uint64_t* part, int n_chunks, int chunk, uint64_t* ppart, int ppart_grid, int* status,
-                          hipStream_t st) {
+                          const int* only_if, hipStream_t st) {
   if (dtype == 1 && ppart && ppart_grid > 0) {
     const hipError_t e = launch_ar_head_persistent(B, gamma, V, rank, logits, E, W, bonus, drafts, next_spine,
-                                                   margins, ppart, ppart_grid, status, st);
+                                                   margins, ppart, ppart_grid, status, only_if, st);
     if (e != hipErrorNotSupported) return e;
   }
   if (chunk != ar_head_chunk(dtype, rank) || n_chunks != (V + chunk - 1) / chunk) return hipErrorInvalidValue;
@@ -448,7 +439,7 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
     hipError_t e = hipErrorInvalidValue;
 #define DPARA_AR_PF(TT, PP) \
   e = launch_ar_pf<TT, PP>(grid, st, step, gamma, V, rank, logits, E, W, bonus, drafts, next_spine, margins, part, \
-                           n_chunks, chunk, B, status)
+                           n_chunks, chunk, B, status, only_if)
     if (dtype == 1) {
       switch (P) {
         case 1: DPARA_AR_PF(bf16_t, 1); break;
@@ -461,7 +452,8 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
         case 8: DPARA_AR_PF(bf16_t, 8); break;
         default:
           hipLaunchKernelGGL(ar_step<bf16_t>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const bf16_t*)E,
-                             (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+                             (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status,
+                             only_if);
           e = hipGetLastError();
       }
     } else {
@@ -472,7 +464,8 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
         case 8: DPARA_AR_PF(float, 8); break;
         default:
           hipLaunchKernelGGL(ar_step<float>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const float*)E,
-                             (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status);
+                             (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status,
+                             only_if);
           e = hipGetLastError();
       }
     }

@@ -299,6 +299,11 @@ class Workspace:
         import torch
         return int(self.buf[:4].view(torch.int32).item())
 
+    def head_fallback(self) -> int:
+        """Nonzero if the last select_and_head on this workspace needed the full head."""
+        import torch
+        return int(self.buf[4:8].view(torch.int32).item())
+
 
 # ---------------------------------------------------------------- tensor-level calls
 def ctx_append(d: DeviceDrafter, ctx: DeviceContext, feats, n_new, ws: Workspace, stream=None):

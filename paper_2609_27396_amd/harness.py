@@ -82,6 +82,11 @@ class DeviceRound:
         torch.cuda.synchronize()
         return self.ws.status()
 
+    def head_fallback(self) -> int:
+        """Nonzero if the last head call needed the full head (a step the pruned head could not prove)."""
+        torch.cuda.synchronize()
+        return self.ws.head_fallback()
+
 
 def upload_cache(ctx, k, v, ctx_lens, dtype):
     """Write host K/V (k[l][b], v[l][b]: [n_b, n_kv, hd]) into a DeviceContext and set ctx_len."""

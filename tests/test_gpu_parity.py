@@ -153,6 +153,33 @@ def test_small_parity(case):
     check_reps(shape, errs, case)
 
 
+HEAD_SHAPE = synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
+                                vocab=5000, gamma=6, ar_rank=128, qk_norm=True, dtype="bf16")
+
+
+@pytest.mark.parametrize("regime", ["pruned", "full"])
+def test_head_pruned_bound_and_fallback(regime):
+    """The exact bound-pruned head proves every step when the correction W.E(y) is small
+    next to the logit gaps (small ar_W), and hands the call to the full head when it cannot
+    (large ar_W and ar_E: the bound max|W_v| |e| swamps every gap); both give the oracle's
+    drafts and margins."""
+    shape = HEAD_SHAPE
+    _say("case head", regime)
+    wl = synth.Workload("head_" + regime, shape, batch=3, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=11,
+                        logits_dtype="bf16")
+    big = regime == "full"
+    w = synth.make_weights(shape, seed=5, gain_jitter=0.1, ar_w_std=2.0 if big else 0.005,
+                           ar_e_std=1.0 if big else 0.02)
+    ri = synth.make_round(wl, ctx_lens=[40, 0, 100])
+    dr = run_full(wl, w, ri)
+    check_verify(ri, dr)
+    fb = dr.head_fallback()
+    _say(regime, "fallback flag", fb)
+    assert (fb != 0) if big else (fb == 0)
+    skipped = sum(check_head(shape, w, dr, "bf16", b) for b in range(wl.batch))
+    assert skipped < wl.batch * shape.gamma // 2
+
+
 def test_append_equivalence_and_determinism():
     shape, _ = SMALL_CASES["h256_hd128_g5"]
     wl = synth.Workload("app", shape, batch=2, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=9)
