@@ -22,9 +22,10 @@
 //                   global top kTopK and the bound, the (kTopK+1)-th key: every logit left
 //                   out of a split's list is at most that split's last key, which no more
 //                   than kTopK keys of the union exceed.  Per step, 16 lanes per candidate
-//                   take the dot product W_v . e over rank slices; the candidates of step
-//                   i+1 depend on the row only, so their W and E rows are fetched while step
-//                   i runs, and the winner's E row is already in registers when it ends.
+//                   take the dot product W_v . e over rank slices; the candidates of a step
+//                   depend on the row only, so their W and E rows are fetched three steps
+//                   ahead into registers, and the winner's E row is in registers when the
+//                   step ends.
 //
 // A row whose candidate collection overflows, or a step whose bound does not hold, sets
 // the fallback flag; the full head (launch_ar_head with only_if = flag) then recomputes
@@ -211,12 +212,43 @@ __global__ __launch_bounds__(256) void w_rownorm_max(const T* W, int V, float* p
   if (tid == 0) partial[blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
+// 16-byte (or 8-byte) raw pieces of EPT elements, converted to float at use.
 template <typename T, int EPT>
+struct RawPiece {
+  static constexpr int WORDS = EPT * (int)sizeof(T) / 4;
+  uint32_t w[WORDS];
+  __device__ __forceinline__ void load(const T* p) {
+    if constexpr (WORDS % 4 == 0) {
+#pragma unroll
+      for (int q = 0; q < WORDS / 4; ++q) {
+        const uint4 u = ((const uint4*)p)[q];
+        w[4 * q] = u.x;
+        w[4 * q + 1] = u.y;
+        w[4 * q + 2] = u.z;
+        w[4 * q + 3] = u.w;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < WORDS / 2; ++q) {
+        const uint2 u = ((const uint2*)p)[q];
+        w[2 * q] = u.x;
+        w[2 * q + 1] = u.y;
+      }
+    }
+  }
+  __device__ __forceinline__ float at(int j) const {
+    if constexpr (sizeof(T) == 2) return __uint_as_float((j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16));
+    else return __uint_as_float(w[j]);
+  }
+};
+
+template <typename T, int RANK>
 __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const uint64_t* cand,
                                                  const float* wpart, int n_wpart, const T* E, const T* W,
                                                  const int* bonus, int* drafts, int* next_spine, float* margins,
                                                  int* flag, int* status) {
-  constexpr int RANK = 16 * EPT;
+  constexpr int EPT = RANK / 16;
+  constexpr int D = 4;  // steps of candidate rows in flight, in registers
   __shared__ uint64_t lists[16][kMaxSplits * kKeys];  // the split lists of 16 rows in flight
   __shared__ uint64_t ck[kMaxGamma][kKeys];           // per row: top kTopK keys, then the bound key
   __shared__ float es[RANK];                          // E(y_{i-1})
@@ -266,74 +298,80 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
   if (stop) return;
   const float wmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * (1.0f + 1e-5f);
 
-  // candidate indices are clamped into the vocabulary (keys of a complete list always are)
-  auto cand_v = [&](uint64_t k) { return (int)min(key_index(k), (uint32_t)(V - 1)); };
-  float wr[EPT], er[EPT];
-  {
-    const int v = cand_v(ck[0][kc]);
-    load_piece<T, EPT>(W + (int64_t)v * RANK + slice * EPT, wr);
-    load_piece<T, EPT>(E + (int64_t)v * RANK + slice * EPT, er);
-  }
-  for (int i = 1; i <= gamma; ++i) {
-    float wn[EPT], en[EPT];
-    if (i < gamma) {  // step i+1's candidate rows
-      const int vn = cand_v(ck[i][kc]);
-      load_piece<T, EPT>(W + (int64_t)vn * RANK + slice * EPT, wn);
-      load_piece<T, EPT>(E + (int64_t)vn * RANK + slice * EPT, en);
-    }
-    float d = 0.f, ee = 0.f;
+  // Step s's (1-based) candidate rows; steps past gamma reload step gamma's (in bounds,
+  // never used).  Candidate indices are clamped into the vocabulary (keys of a complete
+  // list always are).
+  RawPiece<T, EPT> wb[D], eb[D];
+  auto fetch = [&](int s, RawPiece<T, EPT>& w, RawPiece<T, EPT>& e) {
+    const int v = (int)min(key_index(ck[min(s, gamma) - 1][kc]), (uint32_t)(V - 1));
+    w.load(W + (int64_t)v * RANK + slice * EPT);
+    e.load(E + (int64_t)v * RANK + slice * EPT);
+  };
 #pragma unroll
-    for (int j = 0; j < EPT; ++j) {
-      const float ej = es[slice * EPT + j];
-      d = fmaf(wr[j], ej, d);
-      ee = fmaf(ej, ej, ee);
-    }
-    d = row16_sum(d);
-    ee = row16_sum(ee);
-    const uint64_t key = ck[i - 1][kc];
-    if (slice == 0) zs[kc] = key_value(key) + d;
-    __syncthreads();
-    if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
-      uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
-      float v2 = -INFINITY;
-      top2_merge(k1, v2, dpp_u64<kDppXor1>(k1), dpp_f<kDppXor1>(v2));
-      top2_merge(k1, v2, dpp_u64<kDppXor2>(k1), dpp_f<kDppXor2>(v2));
-      top2_merge(k1, v2, dpp_u64<kDppHalfMirror>(k1), dpp_f<kDppHalfMirror>(v2));
-      top2_merge(k1, v2, dpp_u64<kDppMirror>(k1), dpp_f<kDppMirror>(v2));
-      if (tid == 0) {
-        const float lb = key_value(ck[i - 1][kTopK]);
-        const float bound = lb + wmax * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
-        const bool ok = v2 > bound;
-        const int y = (int)key_index(k1);
-        if (ok) {
-          drafts[b * gamma + i - 1] = y;
-          next_spine[b * (gamma + 1) + i] = y;
-          if (margins) margins[b * gamma + i - 1] = key_value(k1) - v2;
-        } else {
-          atomicOr(flag, 2);
-        }
-        stop = ok ? 0 : 1;
-        ybc = y;
-      }
-    }
-    __syncthreads();
-    if (stop) return;
-    if (i < gamma) {
-      if ((int)key_index(key) == ybc) {  // the winner's row holds E(y_i)
+  for (int s = 1; s < D; ++s) fetch(s, wb[s - 1], eb[s - 1]);
+
+  for (int i0 = 1; i0 <= gamma; i0 += D) {
 #pragma unroll
-        for (int j = 0; j < EPT; ++j) es[slice * EPT + j] = er[j];
-      }
+    for (int u = 0; u < D; ++u) {
+      const int i = i0 + u;
+      if (i > gamma) break;
+      fetch(i + D - 1, wb[(u + D - 1) % D], eb[(u + D - 1) % D]);
+      float d = 0.f, ee = 0.f;
 #pragma unroll
       for (int j = 0; j < EPT; ++j) {
-        wr[j] = wn[j];
-        er[j] = en[j];
+        const float ej = es[slice * EPT + j];
+        d = fmaf(wb[u].at(j), ej, d);
+        ee = fmaf(ej, ej, ee);
       }
+      d = row16_sum(d);
+      ee = row16_sum(ee);
+      const uint64_t key = ck[i - 1][kc];
+      if (slice == 0) zs[kc] = key_value(key) + d;
+      __syncthreads();
+      if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
+        uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
+        float v2 = -INFINITY;
+        top2_merge(k1, v2, dpp_u64<kDppXor1>(k1), dpp_f<kDppXor1>(v2));
+        top2_merge(k1, v2, dpp_u64<kDppXor2>(k1), dpp_f<kDppXor2>(v2));
+        top2_merge(k1, v2, dpp_u64<kDppHalfMirror>(k1), dpp_f<kDppHalfMirror>(v2));
+        top2_merge(k1, v2, dpp_u64<kDppMirror>(k1), dpp_f<kDppMirror>(v2));
+        if (tid == 0) {
+          const float lb = key_value(ck[i - 1][kTopK]);
+          const float bound = lb + wmax * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
+          const bool ok = v2 > bound;
+          const int y = (int)key_index(k1);
+          if (ok) {
+            drafts[b * gamma + i - 1] = y;
+            next_spine[b * (gamma + 1) + i] = y;
+            if (margins) margins[b * gamma + i - 1] = key_value(k1) - v2;
+          } else {
+            atomicOr(flag, 2);
+          }
+          stop = ok ? 0 : 1;
+          ybc = y;
+        }
+      }
+      __syncthreads();
+      if (stop) return;
+      if ((int)key_index(key) == ybc) {  // the winner's row holds E(y_i)
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) es[slice * EPT + j] = eb[u].at(j);
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 }
 
 }  // namespace
+
+template <typename T, int RANK>
+hipError_t launch_pruned(int B, int gamma, int V, int S, const uint64_t* cand, const float* wpart, int nw,
+                         const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
+                         float* margins, int* flag, int* status, hipStream_t st) {
+  hipLaunchKernelGGL((ar_pruned<T, RANK>), dim3(B), dim3(256), 0, st, gamma, V, S, cand, wpart, nw, (const T*)E,
+                     (const T*)W, bonus, drafts, next_spine, margins, flag, status);
+  return hipGetLastError();
+}
 
 int head_prune_splits(int rows, int V) {
   int S = 256 / (rows > 0 ? rows : 1);
@@ -377,20 +415,14 @@ hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, cons
   hipLaunchKernelGGL(logit_topk, dim3(S, rows), dim3(256), 0, st, logits, V, S, per, cand, flag);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-#define DPARA_PRUNED(TT, EPT)                                                                             \
-  hipLaunchKernelGGL((ar_pruned<TT, EPT>), dim3(B), dim3(256), 0, st, gamma, V, S, cand, wpart, nw,      \
-                     (const TT*)E, (const TT*)W, bonus, drafts, next_spine, margins, flag, status)
   if (dtype == 1) {
-    if (rank == 64) DPARA_PRUNED(bf16_t, 4);
-    else if (rank == 128) DPARA_PRUNED(bf16_t, 8);
-    else DPARA_PRUNED(bf16_t, 16);
-  } else {
-    if (rank == 64) DPARA_PRUNED(float, 4);
-    else if (rank == 128) DPARA_PRUNED(float, 8);
-    else DPARA_PRUNED(float, 16);
+    if (rank == 64) return launch_pruned<bf16_t, 64>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
+    if (rank == 128) return launch_pruned<bf16_t, 128>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
+    return launch_pruned<bf16_t, 256>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
   }
-#undef DPARA_PRUNED
-  return hipGetLastError();
+  if (rank == 64) return launch_pruned<float, 64>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
+  if (rank == 128) return launch_pruned<float, 128>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
+  return launch_pruned<float, 256>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
 }
 
 }  // namespace dpara
