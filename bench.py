@@ -216,22 +216,18 @@ def recorded_traffic(kernel: str):
 
 
 def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
-    """Select + AR head alone (gather, LM head over gamma rows, gamma AR steps) at several
-    batch sizes, on synthetic branch representations; microseconds per call."""
+    """Select + AR head alone at several batch sizes, on synthetic branch representations
+    (microseconds per call): the plain call (gather, LM head over gamma rows, gamma AR
+    steps), and the off-serial-path variant: the branch-candidates call (every branch row's
+    LM head with top-2 tiles, timed on its own) and the serial call that uses them."""
     import torch
     from paper_2609_27396_amd import dpara as D
     g, H, V = shape.gamma, shape.hidden, shape.vocab
     gen = torch.Generator(device="cuda")
     gen.manual_seed(1234)
-    out, fallback = {}, {}
-    for B in batches:
-        ws = D.Workspace(dr.d.cfg, B, 64)
-        reps = torch.randn((B, g + 1, g, H), generator=gen, device="cuda", dtype=torch.float32)
-        acc = torch.randint(0, g + 1, (B,), generator=gen, device="cuda", dtype=torch.int32)
-        bon = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
-        drafts = torch.empty((B, g), dtype=torch.int32, device="cuda")
-        nspine = torch.empty((B, g + 1), dtype=torch.int32, device="cuda")
-        call = lambda: D.select_and_head(dr.d, reps, acc, bon, None, drafts, nspine, None, ws)
+    out = {"plain_us": {}, "plain_fallback": {}, "candidates_us": {}, "cand_serial_us": {}, "cand_fallback": {}}
+
+    def timed(call):
         for _ in range(3):
             call()
         torch.cuda.synchronize()
@@ -241,11 +237,26 @@ def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
             call()
         e1.record()
         torch.cuda.synchronize()
+        return 1000.0 * e0.elapsed_time(e1) / iters
+
+    for B in batches:
+        ws = D.Workspace(dr.d.cfg, B, 64)
+        reps = torch.randn((B, g + 1, g, H), generator=gen, device="cuda", dtype=torch.float32)
+        acc = torch.randint(0, g + 1, (B,), generator=gen, device="cuda", dtype=torch.int32)
+        bon = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
+        drafts = torch.empty((B, g), dtype=torch.int32, device="cuda")
+        nspine = torch.empty((B, g + 1), dtype=torch.int32, device="cuda")
+        k = str(B)
+        out["plain_us"][k] = timed(lambda: D.select_and_head(dr.d, reps, acc, bon, None, drafts, nspine, None, ws))
+        out["plain_fallback"][k] = ws.head_fallback()
+        cand = D.branch_candidates_buffer(dr.d, B)
+        out["candidates_us"][k] = timed(lambda: D.branch_candidates(dr.d, reps, cand, ws))
+        out["cand_serial_us"][k] = timed(
+            lambda: D.select_and_head_cand(dr.d, reps, cand, acc, bon, None, drafts, nspine, None, ws))
+        out["cand_fallback"][k] = ws.head_fallback()
         assert ws.status() == 0, f"device status {ws.status()}"
-        out[str(B)] = 1000.0 * e0.elapsed_time(e1) / iters
-        fallback[str(B)] = ws.head_fallback()
-        del ws, reps
-    return out, fallback
+        del ws, reps, cand
+    return out
 
 
 def main():
@@ -376,7 +387,9 @@ def main():
         "phases": phases,
     }
     if shape.dtype == "bf16" and not args.no_head_sweep:
-        out["head_us_by_batch"], out["head_full_fallback_by_batch"] = head_sweep(dr, shape)
+        hs = head_sweep(dr, shape)
+        out["head_us_by_batch"] = hs.pop("plain_us")
+        out["head_variants_by_batch"] = hs
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(wl, weights, ri)

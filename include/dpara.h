@@ -187,6 +187,31 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
                           float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
                           void* ws, size_t ws_bytes, void* stream);
 
+/* Head variant with every branch's base logits computed off the serial path (Algorithm 1
+ * computes the base logits during Precompute).
+ * dpara_branch_candidates, issued after the backbone (for instance on its stream, where it
+ * overlaps verification), scores every row reps[b][r][i-1] against embed (the tied LM head,
+ * float32 rows applied as bf16 hi + lo) and keeps in `cand`, per row, the 16 largest
+ * logits and a bound on all the others (the largest remaining logit or the third largest of
+ * any 128-column tile, whichever is larger), plus max_v |ar_W[v]|^2.
+ * cand: device buffer of dpara_branch_candidates_bytes(cfg, batch) bytes, 256-byte aligned;
+ *       its layout is private to the library.
+ * dpara_select_and_head_cand takes the accepted branch's candidates and produces the same
+ * outputs as dpara_select_and_head (same inputs, same meaning): the gather, then the gamma
+ * exact candidate steps; the LM head over the gathered rows and the full head run only if
+ * some step is not proven (the int32 at byte offset 4 of `ws` is then nonzero).
+ * bf16 drafters with ar_rank in {64, 128, 256}, vocab >= 64 and gamma <= 63 only (else
+ * DPARA_E_UNSUPPORTED).  ws: a workspace of dpara_workspace_bytes(cfg, batch, ctx_cap) bytes
+ * with ctx_cap >= 64. */
+size_t dpara_branch_candidates_bytes(const dpara_config_t* cfg, int32_t batch);
+int dpara_branch_candidates(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
+                            const float* reps, void* cand, void* ws, size_t ws_bytes, void* stream);
+int dpara_select_and_head_cand(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
+                               const float* reps, const void* cand, const int32_t* accept_len,
+                               const int32_t* bonus, float* gathered, int32_t* drafts,
+                               int32_t* next_spine, float* margins, void* ws, size_t ws_bytes,
+                               void* stream);
+
 /* Target verification forward, used for the single-GPU overlap of verification and drafting
  * (Algorithm 1, Verify; Section 4.3.2 and Appendix D: both passes on two streams of one GPU).
  * A causal Qwen3-shaped decoder (same layer structure and dpara_config_t fields as the drafter;

@@ -136,6 +136,49 @@ __device__ __forceinline__ void top2_merge(uint64_t& k1, float& v2, uint64_t ok1
   }
 }
 
+// The two largest argmax keys of a set and the third largest value (-inf if none).
+struct Top3 {
+  uint64_t k1 = 0, k2 = 0;
+  float v3 = -INFINITY;
+  __device__ __forceinline__ static float val(uint64_t k) { return k ? key_value(k) : -INFINITY; }
+  __device__ __forceinline__ void add(uint64_t k) {
+    if (k > k1) {
+      v3 = fmaxf(v3, val(k2));
+      k2 = k1;
+      k1 = k;
+    } else if (k > k2) {
+      v3 = fmaxf(v3, val(k2));
+      k2 = k;
+    } else {
+      v3 = fmaxf(v3, val(k));
+    }
+  }
+  __device__ __forceinline__ static Top3 merge(const Top3& a, const Top3& b) {
+    Top3 m = a;
+    m.v3 = fmaxf(a.v3, b.v3);
+    m.add(b.k1);
+    m.add(b.k2);
+    return m;
+  }
+  template <int CTRL>
+  __device__ __forceinline__ Top3 shifted() const {
+    Top3 o;
+    o.k1 = dpp_u64<CTRL>(k1);
+    o.k2 = dpp_u64<CTRL>(k2);
+    o.v3 = dpp_f<CTRL>(v3);
+    return o;
+  }
+  // merge over the 16 lanes of a DPP row: every lane ends with the row's result
+  __device__ __forceinline__ Top3 row16() const {
+    Top3 m = *this;
+    m = merge(m, m.shifted<kDppXor1>());
+    m = merge(m, m.shifted<kDppXor2>());
+    m = merge(m, m.shifted<kDppHalfMirror>());
+    m = merge(m, m.shifted<kDppMirror>());
+    return m;
+  }
+};
+
 // Status word (int32 at byte offset 0 of the workspace).
 __device__ __forceinline__ void raise_status(int* status, int bit) { atomicOr(status, bit); }
 

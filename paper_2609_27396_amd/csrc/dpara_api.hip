@@ -115,7 +115,7 @@ struct Plan {
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
-      hflag, F, KV32, rope_app;
+      hflag, F, KV32, rope_app, csplit, cpart;
   int ar_grid;  // persistent AR head grid (0: step kernels only)
   size_t total;
 };
@@ -190,6 +190,10 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   const size_t kv_rows = (size_t)B * p.CH > 16 * 320 ? (size_t)B * p.CH : 16 * 320;
   p.KV32 = take(kv_rows * 2 * nkv * hd * 4);
   p.rope_app = take((size_t)B * p.CH * (hd / 2) * 8);  // (cos, sin) of the appended rows' positions
+  // branch candidates (bf16): hi/lo planes of every branch row and the per-tile top-2 words
+  const size_t crows = (size_t)B * (c->gamma + 1) * c->gamma;
+  p.csplit = take(c->dtype == DPARA_BF16 ? 2 * crows * H * 2 : 0);
+  p.cpart = take(c->dtype == DPARA_BF16 ? head_cand_part_bytes(B, c->gamma, c->vocab) : 0);
   p.total = off;
   return p;
 }
@@ -671,6 +675,95 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
                          p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status,
                          pe == hipSuccess ? hflag : nullptr, st),
+          "ar head");
+  return DPARA_OK;
+}
+
+size_t dpara_branch_candidates_bytes(const dpara_config_t* cfg, int32_t batch) {
+  if (check_cfg(cfg) || batch < 1) return 0;
+  return head_cand_bytes(batch, cfg->gamma);
+}
+
+int dpara_branch_candidates(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch, const float* reps,
+                            void* cand, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if (cfg->dtype != DPARA_BF16) return fail(DPARA_E_UNSUPPORTED, "branch candidates need a bf16 drafter");
+  if (!head_prune_supported(1, cfg->gamma, cfg->vocab, cfg->ar_rank))
+    return fail(DPARA_E_UNSUPPORTED, "branch candidates need ar_rank in {64, 128, 256}, vocab >= 64, gamma <= 63");
+  if ((rc = check_weights(cfg, w, false))) return rc;
+  CHECK_PTR(reps, "reps");
+  CHECK_PTR(cand, "cand");
+  if (!aligned16(reps)) return fail(DPARA_E_INVALID, "reps is not 16-byte aligned");
+  if (((uintptr_t)cand & 255u) != 0) return fail(DPARA_E_INVALID, "cand must be 256-byte aligned");
+  if (cfg->hidden % 4) return fail(DPARA_E_UNSUPPORTED, "hidden must be a multiple of 4");
+  const Plan p = make_plan(cfg, batch, 64);
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
+  if (ws_bytes < p.total) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, p.total);
+  if ((rc = check_device())) return rc;
+  HIP_TRY(launch_branch_candidates(batch, cfg->gamma, cfg->hidden, cfg->vocab, cfg->ar_rank, reps, w->embed, w->ar_W,
+                                   cand, at<bf16_t>(ws, p.csplit), at<uint64_t>(ws, p.cpart), (hipStream_t)stream),
+          "branch candidates");
+  return DPARA_OK;
+}
+
+int dpara_select_and_head_cand(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
+                               const float* reps, const void* cand, const int32_t* accept_len, const int32_t* bonus,
+                               float* gathered, int32_t* drafts, int32_t* next_spine, float* margins, void* ws,
+                               size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if (cfg->dtype != DPARA_BF16) return fail(DPARA_E_UNSUPPORTED, "branch candidates need a bf16 drafter");
+  if (!head_prune_supported(1, cfg->gamma, cfg->vocab, cfg->ar_rank))
+    return fail(DPARA_E_UNSUPPORTED, "branch candidates need ar_rank in {64, 128, 256}, vocab >= 64, gamma <= 63");
+  if ((rc = check_weights(cfg, w, false))) return rc;
+  CHECK_PTR(reps, "reps");
+  CHECK_PTR(cand, "cand");
+  if (gathered && !aligned16(gathered)) return fail(DPARA_E_INVALID, "gathered is not 16-byte aligned");
+  if (!accept_len || !bonus || !drafts || !next_spine)
+    return fail(DPARA_E_INVALID, "accept_len, bonus, drafts and next_spine must be non-NULL");
+  const Plan p = make_plan(cfg, batch, 64);
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
+  const size_t need = p.hwpart + up256((size_t)head_prune_wparts() * 4);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if ((rc = check_device())) return rc;
+
+  hipStream_t st = (hipStream_t)stream;
+  const int g = cfg->gamma, H = cfg->hidden, V = cfg->vocab;
+  int* status = at<int>(ws, 0);
+  int* hflag = at<int>(ws, p.hflag);
+  bf16_t* Gs = at<bf16_t>(ws, p.Gsplit);
+  HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, at<float>(ws, p.G), gathered, Gs,
+                               at<uint64_t>(ws, p.arpart), (int64_t)2 * 16 * p.ar_grid * 2, status, st),
+          "gather_branch");
+  HIP_TRY(launch_head_from_candidates(batch, g, V, cfg->ar_rank, cand, w->ar_E, w->ar_W, accept_len, bonus, drafts,
+                                      next_spine, margins, hflag, status, st),
+          "pruned head");
+  // Only if some step was not proven: the LM head over the gathered rows and the full head
+  // (both return at once otherwise).
+  GemmArgs lm{};
+  lm.A = Gs;
+  lm.lo_off = (int64_t)batch * g * H;
+  lm.lda = H;
+  lm.B0 = lm.B1 = lm.B2 = w->embed;
+  lm.n1 = lm.n2 = V;
+  lm.M = batch * g;
+  lm.N = V;
+  lm.K = H;
+  lm.C = at<void>(ws, p.logits);
+  lm.ldc = V;
+  lm.only_if = hflag;
+  {
+    Phase ph("lm_head", st);
+    HIP_TRY(launch_gemm(A_BF16_DUAL, EPI_STORE_F32, lm, st), "lm head gemm");
+  }
+  HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
+                         drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
+                         p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status, hflag, st),
           "ar head");
   return DPARA_OK;
 }

@@ -93,6 +93,7 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
   constexpr int STAGE_BYTES = (A_ROWS + BN) * BKB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
+  if (a.only_if && *a.only_if == 0) return;
   // Split-K: the S splits of one output tile are consecutive logical workgroups; split s
   // covers K range [s*K/S, (s+1)*K/S) and stores into plane s of C.
   const int S = a.splits;
@@ -175,6 +176,44 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     }
   }
 
+  if constexpr (EPI == EPI_TOP2) {
+    static_assert(BN == 128, "the top-2 tiles are 128 columns");
+    // Per lane: its columns of each row (FN of them); then the 16 lanes that share the row
+    // (DPP); then the WNW wave columns through LDS, which the K loop no longer uses.
+    Top3 t[FM][4];
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        t[mi][r] = Top3{};
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) {
+          const int col = nt * BN + wn * WN + ni * 16 + lr;
+          if (col < a.N) t[mi][r].add(argmax_key(acc[mi][ni][r], (uint32_t)col));
+        }
+        t[mi][r] = t[mi][r].row16();
+      }
+    __syncthreads();
+    Top3* xs = (Top3*)smem;  // [WNW][BM]
+    if (lr == 0) {
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) xs[wn * BM + wm * WM + mi * 16 + (lane >> 4) * 4 + r] = t[mi][r];
+    }
+    __syncthreads();
+    for (int lrow = threadIdx.x; lrow < BM; lrow += blockDim.x) {
+      const int row = m0 + lrow;
+      if (row >= a.M) continue;
+      Top3 m = xs[lrow];
+      for (int c = 1; c < WNW; ++c) m = Top3::merge(m, xs[c * BM + lrow]);
+      uint64_t* o = (uint64_t*)a.C + ((int64_t)row * a.ldc + nt) * 3;
+      o[0] = m.k1;
+      o[1] = m.k2;
+      o[2] = (uint64_t)__float_as_uint(m.v3);
+    }
+    return;
+  }
 #pragma unroll
   for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
@@ -489,10 +528,16 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     }
   }
   if (amode == A_BF16_DUAL) {
+    if (epi == EPI_TOP2) {
+      if (a.ldc < (a.N + 127) / 128) return hipErrorInvalidValue;
+      if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_TOP2, 1>(a, st);
+      return run_pipe<128, 128, 4, 2, 3, 128, EPI_TOP2, 1>(a, st);
+    }
     if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 128, EPI_STORE_F32, 1>(a, st);
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }
+  if (epi == EPI_TOP2) return hipErrorInvalidValue;
   const bool small = a.M <= 512;
   if (amode == A_F32SPLIT) {
     return small ? run_mfma<64, 128, EPI_STORE_F32, A_F32SPLIT>(a, st)

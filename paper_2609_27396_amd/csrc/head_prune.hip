@@ -182,6 +182,90 @@ __global__ __launch_bounds__(256) void logit_topk(const float* logits, int V, in
   }
 }
 
+// fp32 rows -> bf16 hi + lo planes (hi = bf16(x), lo = bf16(x - hi)), 4 elements a thread.
+__global__ __launch_bounds__(256) void split_hi_lo(const float* X, int64_t n4, bf16_t* hi, bf16_t* lo) {
+  const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (k >= n4) return;
+  const float4 v = ((const float4*)X)[k];
+  const float x[4] = {v.x, v.y, v.z, v.w};
+  bf16_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    h[j] = f2bf(x[j]);
+    l[j] = f2bf(x[j] - bf2f(h[j]));
+  }
+  *(uint2*)(hi + 4 * k) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+  *(uint2*)(lo + 4 * k) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+}
+
+// Per row: the tiles' (key1, key2, third value) triples of the top-2 GEMM epilogue ->
+// the kTopK largest keys of the row and, in slot kTopK, a key whose value bounds every
+// other logit of the row: the largest of the remaining keys and of the tiles' third values
+// (a logit that is not among its tile's two largest is at most that tile's third value).
+// Fewer than kTopK keys (a vocabulary of few tiles) leave zero keys, which never win.
+__global__ __launch_bounds__(256) void tile_top2_merge(const uint64_t* part, int NT, uint64_t* out, int* flag) {
+  __shared__ __attribute__((aligned(16))) uint64_t tm[256];
+  __shared__ uint64_t buf[kCollect];
+  __shared__ float red[4];
+  __shared__ uint64_t thr;
+  __shared__ int cnt;
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const uint64_t* pr = part + (int64_t)row * NT * 3;
+  uint64_t best = 0;
+  float v3 = -INFINITY;
+  for (int t = tid; t < NT; t += 256) {
+    const uint64_t k1 = pr[3 * t];
+    best = k1 > best ? k1 : best;  // the tile's second key is smaller
+    v3 = fmaxf(v3, __uint_as_float((uint32_t)pr[3 * t + 2]));
+  }
+  tm[tid] = best;
+  v3 = wave_max(v3);
+  if ((tid & 63) == 0) red[tid >> 6] = v3;
+  if (tid == 0) {
+    cnt = 0;
+    thr = 0;
+  }
+  __syncthreads();
+  int r = 0;
+  for (int j = 0; j < 256; j += 2) {
+    const uint4 u = *(const uint4*)&tm[j];
+    r += (((uint64_t)u.y << 32 | u.x) > best) + (((uint64_t)u.w << 32 | u.z) > best);
+  }
+  if (r == kTopK && best != 0) thr = best;
+  __syncthreads();
+  const uint64_t T = thr;  // 0: fewer than kKeys tiles hold a key; then every key is taken
+  for (int t = tid; t < NT; t += 256)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const uint64_t k = pr[3 * t + q];
+      if (k != 0 && k >= T) {
+        const int pos = atomicAdd(&cnt, 1);
+        if (pos < kCollect) buf[pos] = k;
+      }
+    }
+  __syncthreads();
+  const int n = cnt;
+  uint64_t* o = out + (int64_t)row * kKeys;
+  if (n > kCollect) {
+    if (tid == 0) atomicOr(flag, 1);
+    return;
+  }
+  for (int e = tid; e < kKeys; e += 256) o[e] = 0;
+  __syncthreads();
+  for (int e = tid; e < n; e += 256) {
+    const uint64_t k = buf[e];
+    int rr = 0;
+    for (int j = 0; j < n; ++j) rr += buf[j] > k;
+    if (rr < kKeys) o[rr] = k;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float bound = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    if (n > kTopK) bound = fmaxf(bound, key_value(o[kTopK]));
+    o[kTopK] = argmax_key(bound, 0xFFFFFFFEu);
+  }
+}
+
 template <typename T, int RANK>
 __global__ __launch_bounds__(256) void w_rownorm_max(const T* W, int V, float* partial, int* flag) {
   constexpr int EPL = RANK / 16;
@@ -246,7 +330,8 @@ template <typename T, int RANK>
 __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const uint64_t* cand,
                                                  const float* wpart, int n_wpart, const T* E, const T* W,
                                                  const int* bonus, int* drafts, int* next_spine, float* margins,
-                                                 int* flag, int* status) {
+                                                 int* flag, int* status, const int* accept_len,
+                                                 const int* pre_flag) {
   constexpr int EPT = RANK / 16;
   constexpr int D = 4;  // steps of candidate rows in flight, in registers
   __shared__ uint64_t lists[16][kMaxSplits * kKeys];  // the split lists of 16 rows in flight
@@ -265,8 +350,15 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
   }
   if (tid == 0) {
     next_spine[b * (gamma + 1)] = y0;
-    stop = *flag;  // some candidate row was not decidable: the full head recomputes everything
+    // some candidate row was not decidable: the full head recomputes everything
+    const int pre = pre_flag ? *pre_flag : 0;
+    if (pre && b == 0) atomicOr(flag, 1);
+    stop = *flag | pre;
   }
+  // candidate rows of this request: its gamma head rows, or (precomputed candidates of every
+  // branch) the rows of its accepted branch
+  int row0 = b * gamma;
+  if (accept_len) row0 = (b * (gamma + 1) + min(max(accept_len[b], 0), gamma)) * gamma;
   float wm = 0.f;
   for (int i = tid; i < n_wpart; i += 256) wm = fmaxf(wm, wpart[i]);
   wm = wave_max(wm);
@@ -278,7 +370,7 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
     const int nrow = min(16, gamma - j0);
     for (int i = tid; i < nrow * S * kKeys; i += 256) {
       const int rr = i / (S * kKeys), q = i % (S * kKeys);
-      lists[rr][q] = cand[((int64_t)(b * gamma + j0 + rr)) * S * kKeys + q];
+      lists[rr][q] = cand[((int64_t)(row0 + j0 + rr)) * S * kKeys + q];
     }
     __syncthreads();
     if (kc < nrow) {
@@ -326,7 +418,7 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
       d = row16_sum(d);
       ee = row16_sum(ee);
       const uint64_t key = ck[i - 1][kc];
-      if (slice == 0) zs[kc] = key_value(key) + d;
+      if (slice == 0) zs[kc] = key ? key_value(key) + d : -INFINITY;  // fewer than kTopK candidates
       __syncthreads();
       if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
         uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
@@ -367,10 +459,46 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
 template <typename T, int RANK>
 hipError_t launch_pruned(int B, int gamma, int V, int S, const uint64_t* cand, const float* wpart, int nw,
                          const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
-                         float* margins, int* flag, int* status, hipStream_t st) {
+                         float* margins, int* flag, int* status, const int* accept_len, const int* pre_flag,
+                         hipStream_t st) {
   hipLaunchKernelGGL((ar_pruned<T, RANK>), dim3(B), dim3(256), 0, st, gamma, V, S, cand, wpart, nw, (const T*)E,
-                     (const T*)W, bonus, drafts, next_spine, margins, flag, status);
+                     (const T*)W, bonus, drafts, next_spine, margins, flag, status, accept_len, pre_flag);
   return hipGetLastError();
+}
+
+hipError_t launch_wnorm(int dtype, int rank, const void* W, int V, float* wpart, int* flag, hipStream_t st) {
+  const int nw = 512;
+#define DPARA_WNORM(TT, RK) \
+  hipLaunchKernelGGL((w_rownorm_max<TT, RK>), dim3(nw), dim3(256), 0, st, (const TT*)W, V, wpart, flag)
+  if (dtype == 1) {
+    if (rank == 64) DPARA_WNORM(bf16_t, 64);
+    else if (rank == 128) DPARA_WNORM(bf16_t, 128);
+    else DPARA_WNORM(bf16_t, 256);
+  } else {
+    if (rank == 64) DPARA_WNORM(float, 64);
+    else if (rank == 128) DPARA_WNORM(float, 128);
+    else DPARA_WNORM(float, 256);
+  }
+#undef DPARA_WNORM
+  return hipGetLastError();
+}
+
+hipError_t dispatch_pruned(int dtype, int rank, int B, int gamma, int V, int S, const uint64_t* cand,
+                           const float* wpart, int nw, const void* E, const void* W, const int* bonus, int* drafts,
+                           int* next_spine, float* margins, int* flag, int* status, const int* accept_len,
+                           const int* pre_flag, hipStream_t st) {
+#define DPARA_PRUNED(TT, RK)                                                                                   \
+  return launch_pruned<TT, RK>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, \
+                               status, accept_len, pre_flag, st)
+  if (dtype == 1) {
+    if (rank == 64) DPARA_PRUNED(bf16_t, 64);
+    if (rank == 128) DPARA_PRUNED(bf16_t, 128);
+    DPARA_PRUNED(bf16_t, 256);
+  }
+  if (rank == 64) DPARA_PRUNED(float, 64);
+  if (rank == 128) DPARA_PRUNED(float, 128);
+  DPARA_PRUNED(float, 256);
+#undef DPARA_PRUNED
 }
 
 int head_prune_splits(int rows, int V) {
@@ -381,6 +509,54 @@ int head_prune_splits(int rows, int V) {
 }
 
 int head_prune_wparts() { return 512; }
+
+size_t head_cand_bytes(int B, int gamma) { return 4096 + (size_t)B * (gamma + 1) * gamma * kKeys * 8; }
+size_t head_cand_part_bytes(int B, int gamma, int V) { return (size_t)B * (gamma + 1) * gamma * ((V + 127) / 128) * 24; }
+
+hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
+                                    const void* W, void* cand, bf16_t* split, uint64_t* part, hipStream_t st) {
+  if (!head_prune_supported(1, gamma, V, rank) || B < 1 || H % 4) return hipErrorNotSupported;
+  int* overflow = (int*)cand;
+  float* wpart = (float*)((unsigned char*)cand + 256);
+  uint64_t* keys = (uint64_t*)((unsigned char*)cand + 4096);
+  const int rows = B * (gamma + 1) * gamma;
+  const int NT = (V + 127) / 128;
+  Phase ph("lm_head", st);
+  const int64_t n4 = (int64_t)rows * H / 4;
+  hipLaunchKernelGGL(split_hi_lo, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, st, reps, n4, split,
+                     split + (int64_t)rows * H);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if ((e = launch_wnorm(1, rank, W, V, wpart, overflow, st)) != hipSuccess) return e;  // also clears `overflow`
+  GemmArgs g{};
+  g.A = split;
+  g.lo_off = (int64_t)rows * H;
+  g.lda = H;
+  g.B0 = g.B1 = g.B2 = embed;
+  g.n1 = g.n2 = V;
+  g.M = rows;
+  g.N = V;
+  g.K = H;
+  g.C = part;
+  g.ldc = NT;
+  if ((e = launch_gemm(A_BF16_DUAL, EPI_TOP2, g, st)) != hipSuccess) return e;
+  hipLaunchKernelGGL(tile_top2_merge, dim3(rows), dim3(256), 0, st, part, NT, keys, overflow);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_from_candidates(int B, int gamma, int V, int rank, const void* cand, const void* E,
+                                       const void* W, const int* accept_len, const int* bonus, int* drafts,
+                                       int* next_spine, float* margins, int* flag, int* status, hipStream_t st) {
+  if (!head_prune_supported(1, gamma, V, rank) || B < 1) return hipErrorNotSupported;
+  const int* overflow = (const int*)cand;
+  const float* wpart = (const float*)((const unsigned char*)cand + 256);
+  const uint64_t* keys = (const uint64_t*)((const unsigned char*)cand + 4096);
+  Phase ph("ar_step", st);
+  hipError_t e = launch_clear_status(flag, st);
+  if (e != hipSuccess) return e;
+  return dispatch_pruned(1, rank, B, gamma, V, 1, keys, wpart, head_prune_wparts(), E, W, bonus, drafts, next_spine,
+                         margins, flag, status, accept_len, overflow, st);
+}
 
 bool head_prune_supported(int dtype, int gamma, int V, int rank) {
   return gamma >= 1 && gamma <= kMaxGamma && V >= 64 && (rank == 64 || rank == 128 || rank == 256) &&
@@ -398,31 +574,13 @@ hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, cons
   const int per = ((V + S - 1) / S + 3) / 4 * 4;
   const int nw = head_prune_wparts();
   Phase ph("ar_step", st);
-#define DPARA_WNORM(TT, RK) \
-  hipLaunchKernelGGL((w_rownorm_max<TT, RK>), dim3(nw), dim3(256), 0, st, (const TT*)W, V, wpart, flag)
-  if (dtype == 1) {
-    if (rank == 64) DPARA_WNORM(bf16_t, 64);
-    else if (rank == 128) DPARA_WNORM(bf16_t, 128);
-    else DPARA_WNORM(bf16_t, 256);
-  } else {
-    if (rank == 64) DPARA_WNORM(float, 64);
-    else if (rank == 128) DPARA_WNORM(float, 128);
-    else DPARA_WNORM(float, 256);
-  }
-#undef DPARA_WNORM
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_wnorm(dtype, rank, W, V, wpart, flag, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(logit_topk, dim3(S, rows), dim3(256), 0, st, logits, V, S, per, cand, flag);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (dtype == 1) {
-    if (rank == 64) return launch_pruned<bf16_t, 64>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
-    if (rank == 128) return launch_pruned<bf16_t, 128>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
-    return launch_pruned<bf16_t, 256>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
-  }
-  if (rank == 64) return launch_pruned<float, 64>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
-  if (rank == 128) return launch_pruned<float, 128>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
-  return launch_pruned<float, 256>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, status, st);
+  return dispatch_pruned(dtype, rank, B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag,
+                         status, nullptr, nullptr, st);
 }
 
 }  // namespace dpara

@@ -21,7 +21,7 @@ struct Phase {
 // ---------------------------------------------------------------- GEMM
 // C[M, N] (op)= A[M, K] . B[N, K]^T with B given in up to three row segments
 // (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2).
-enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3 };
+enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3, EPI_TOP2 = 4 };
 // A_BF16: A is bf16.  A_F32SPLIT: A is float32 and is applied as hi + lo bf16 parts
 // (two MFMA passes), which keeps ~16 significant bits of A.  A_F32: float32 FMA kernel
 // (the float32 model path; B is then float32 too).
@@ -43,6 +43,11 @@ struct GemmArgs {
   int splits = 1;  // split-K: S >= 1 fp32 planes of C (plane stride M*ldc); EPI_STORE_F32 only
   // EPI_SWIGLU: B0 = gate [N, K], B1 = up [N, K], C = bf16/f32 [M, N] of silu(g) * u,
   // where N is the FFN width.
+  // EPI_TOP2 (A_BF16_DUAL only): instead of C, per row and 128-column tile t the two largest
+  // (value, column) argmax keys of the row's tile and the third largest value, as three
+  // uint64 words at C + (row * ldc + t) * 3 (the value's float bits in the low word);
+  // columns past N do not count.  ldc >= ceil(N / 128).
+  const int* only_if = nullptr;  // non-NULL: every workgroup returns at once unless *only_if != 0
 };
 
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st);
@@ -142,5 +147,16 @@ size_t head_prune_cand_bytes(int rows, int V);
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                               uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st);
+// Candidates of every branch row, off the serial path (bf16): reps [B, gamma+1, gamma, H]
+// fp32 -> `cand` (head_cand_bytes: a 4 KB header with an overflow flag at 0 and the
+// |W_v|^2 maxima at byte 256, then kTopK+1 keys per row); `split` holds 2 * rows * H bf16,
+// `part` head_cand_part_bytes.  The serial step then takes the accepted branch's rows.
+size_t head_cand_bytes(int B, int gamma);
+size_t head_cand_part_bytes(int B, int gamma, int V);
+hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
+                                    const void* W, void* cand, bf16_t* split, uint64_t* part, hipStream_t st);
+hipError_t launch_head_from_candidates(int B, int gamma, int V, int rank, const void* cand, const void* E,
+                                       const void* W, const int* accept_len, const int* bonus, int* drafts,
+                                       int* next_spine, float* margins, int* flag, int* status, hipStream_t st);
 
 }  // namespace dpara

@@ -22,7 +22,8 @@ DPARA_F32, DPARA_BF16 = 0, 1
 STATUS_TOKEN_RANGE, STATUS_CTX_FULL, STATUS_VERDICT_RANGE, STATUS_COUNT_RANGE, STATUS_HEAD_TIMEOUT = 1, 2, 4, 8, 16
 
 EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boundaries",
-           "dpara_verify_greedy", "dpara_select_and_head", "dpara_clear_status",
+           "dpara_verify_greedy", "dpara_select_and_head", "dpara_branch_candidates_bytes",
+           "dpara_branch_candidates", "dpara_select_and_head_cand", "dpara_clear_status",
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
            "dpara_target_workspace_bytes", "dpara_target_forward")
 
@@ -85,6 +86,11 @@ def lib():
         L.dpara_verify_greedy.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, VP, VP, VP, SZ, VP]
         L.dpara_select_and_head.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP, VP, VP,
                                             SZ, VP]
+        L.dpara_branch_candidates_bytes.argtypes = [P(DparaConfig), I32]
+        L.dpara_branch_candidates_bytes.restype = SZ
+        L.dpara_branch_candidates.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, SZ, VP]
+        L.dpara_select_and_head_cand.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP, VP,
+                                                 VP, VP, SZ, VP]
         L.dpara_clear_status.argtypes = [VP, VP]
         L.dpara_target_workspace_bytes.argtypes = [P(DparaConfig), I32, I32]
         L.dpara_target_workspace_bytes.restype = SZ
@@ -95,7 +101,8 @@ def lib():
         L.dpara_profile_enable.argtypes = [I32]
         L.dpara_profile_read.argtypes = [ctypes.c_char_p, P(ctypes.c_double), P(ctypes.c_int64)]
         for name in ("dpara_ctx_append", "dpara_backbone_all_boundaries", "dpara_verify_greedy",
-                     "dpara_select_and_head", "dpara_clear_status", "dpara_profile_enable",
+                     "dpara_select_and_head", "dpara_branch_candidates", "dpara_select_and_head_cand",
+                     "dpara_clear_status", "dpara_profile_enable",
                      "dpara_profile_read", "dpara_target_forward"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -135,6 +142,20 @@ def dpara_select_and_head(cfg, w, batch, reps, accept_len, bonus, gathered, draf
                           ws_bytes, stream):
     _check(lib().dpara_select_and_head(_ref(cfg), _ref(w), batch, reps, accept_len, bonus, gathered, drafts,
                                        next_spine, margins, ws, ws_bytes, stream))
+
+
+def dpara_branch_candidates_bytes(cfg: DparaConfig, batch: int) -> int:
+    return int(lib().dpara_branch_candidates_bytes(_ref(cfg), batch))
+
+
+def dpara_branch_candidates(cfg, w, batch, reps, cand, ws, ws_bytes, stream):
+    _check(lib().dpara_branch_candidates(_ref(cfg), _ref(w), batch, reps, cand, ws, ws_bytes, stream))
+
+
+def dpara_select_and_head_cand(cfg, w, batch, reps, cand, accept_len, bonus, gathered, drafts, next_spine, margins,
+                               ws, ws_bytes, stream):
+    _check(lib().dpara_select_and_head_cand(_ref(cfg), _ref(w), batch, reps, cand, accept_len, bonus, gathered,
+                                            drafts, next_spine, margins, ws, ws_bytes, stream))
 
 
 def dpara_target_workspace_bytes(cfg: DparaConfig, batch: int, ctx_cap: int) -> int:
@@ -329,6 +350,25 @@ def select_and_head(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts,
     dpara_select_and_head(d.cfg, d.w, int(accept_len.shape[0]), _ptr(reps), _ptr(accept_len), _ptr(bonus),
                           _ptr(gathered), _ptr(drafts), _ptr(next_spine), _ptr(margins), ws.ptr, ws.nbytes,
                           _stream(stream))
+
+
+def branch_candidates_buffer(d: DeviceDrafter, batch: int, device="cuda"):
+    """A device buffer for dpara_branch_candidates (256-byte aligned)."""
+    import torch
+    n = dpara_branch_candidates_bytes(d.cfg, batch)
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def branch_candidates(d: DeviceDrafter, reps, cand, ws: Workspace, stream=None):
+    dpara_branch_candidates(d.cfg, d.w, int(reps.shape[0]), _ptr(reps), _ptr(cand), ws.ptr, ws.nbytes,
+                            _stream(stream))
+
+
+def select_and_head_cand(d: DeviceDrafter, reps, cand, accept_len, bonus, gathered, drafts, next_spine, margins,
+                         ws: Workspace, stream=None):
+    dpara_select_and_head_cand(d.cfg, d.w, int(accept_len.shape[0]), _ptr(reps), _ptr(cand), _ptr(accept_len),
+                               _ptr(bonus), _ptr(gathered), _ptr(drafts), _ptr(next_spine), _ptr(margins), ws.ptr,
+                               ws.nbytes, _stream(stream))
 
 
 def target_forward(t: DeviceTarget, ctx: DeviceContext, block, logits, ws: Workspace, stream=None):

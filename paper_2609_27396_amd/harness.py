@@ -78,6 +78,16 @@ class DeviceRound:
         D.select_and_head(self.d, self.reps, self.accept, self.bonus, self.gathered, self.drafts,
                           self.next_spine, self.margins, self.ws, stream)
 
+    def candidates(self, stream=None):
+        """Every branch row's head candidates (the off-serial-path head variant)."""
+        if getattr(self, "cand", None) is None:
+            self.cand = D.branch_candidates_buffer(self.d, self.B)
+        D.branch_candidates(self.d, self.reps, self.cand, self.ws, stream)
+
+    def head_cand(self, stream=None):
+        D.select_and_head_cand(self.d, self.reps, self.cand, self.accept, self.bonus, self.gathered, self.drafts,
+                               self.next_spine, self.margins, self.ws, stream)
+
     def status(self) -> int:
         torch.cuda.synchronize()
         return self.ws.status()

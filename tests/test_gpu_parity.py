@@ -180,6 +180,40 @@ def test_head_pruned_bound_and_fallback(regime):
     assert skipped < wl.batch * shape.gamma // 2
 
 
+@pytest.mark.parametrize("regime", ["pruned", "full"])
+def test_head_from_branch_candidates(regime):
+    """The off-serial-path head variant: candidates of every branch row computed after the
+    backbone, then the serial step from the accepted branch's candidates.  Drafts, margins,
+    next spine and gathered rows agree with the plain select + head where both prove every
+    step, and with the oracle either way (the large-W regime takes the fallback)."""
+    shape = HEAD_SHAPE
+    _say("case head from candidates", regime)
+    wl = synth.Workload("headc_" + regime, shape, batch=3, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=13,
+                        logits_dtype="bf16")
+    big = regime == "full"
+    w = synth.make_weights(shape, seed=6, gain_jitter=0.1, ar_w_std=2.0 if big else 0.005,
+                           ar_e_std=1.0 if big else 0.02)
+    ri = synth.make_round(wl, ctx_lens=[70, 5, 0])
+    dr = run_full(wl, w, ri)
+    plain = {k: getattr(dr, k).clone() for k in ("drafts", "next_spine", "margins", "gathered")}
+    fb_plain = dr.head_fallback()
+    for k in ("drafts", "next_spine", "margins", "gathered"):
+        getattr(dr, k).fill_(-7)
+    dr.candidates()
+    dr.head_cand()
+    torch.cuda.synchronize()
+    assert dr.status() == 0
+    fb = dr.head_fallback()
+    _say(regime, "fallback flags plain / candidates", fb_plain, fb)
+    assert (fb != 0) if big else (fb == 0)
+    assert torch.equal(dr.gathered, plain["gathered"])
+    if fb == 0 and fb_plain == 0:
+        for k in ("drafts", "next_spine", "margins"):
+            assert torch.equal(getattr(dr, k), plain[k]), k
+    for b in range(wl.batch):
+        check_head(shape, w, dr, "bf16", b)
+
+
 def test_append_equivalence_and_determinism():
     shape, _ = SMALL_CASES["h256_hd128_g5"]
     wl = synth.Workload("app", shape, batch=2, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=9)
