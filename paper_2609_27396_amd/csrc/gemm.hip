@@ -528,10 +528,12 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     }
   }
   if (amode == A_BF16_DUAL) {
+    // Top-2 over every branch row (hundreds to thousands of rows, compute-bound): 96-row
+    // tiles with a 2-deep ring (80 KB of LDS, two workgroups per CU) measured 12-30% faster
+    // on MI355X than one workgroup per CU with a 3-deep ring.
     if (epi == EPI_TOP2) {
       if (a.ldc < (a.N + 127) / 128) return hipErrorInvalidValue;
-      if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_TOP2, 1>(a, st);
-      return run_pipe<128, 128, 4, 2, 3, 128, EPI_TOP2, 1>(a, st);
+      return run_pipe<96, 128, 2, 2, 2, 128, EPI_TOP2, 1>(a, st);
     }
     if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 128, EPI_STORE_F32, 1>(a, st);
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
