@@ -230,34 +230,49 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = hd / 2;
   const float* src = KV + (int64_t)m * 2 * n_kv * hd;
-  {
-    const int kvh = blockIdx.x * 4 + wave;  // one wave per (row, kv head)
-    if (kvh >= n_kv) return;
-    const float* x = src + kvh * hd;
-    const bool act = lane < half;
-    float x1 = 0.f, x2 = 0.f;
-    if (act) {
-      x1 = sum_planes(0.f, x + lane, pstride, S);
-      x2 = sum_planes(0.f, x + lane + half, pstride, S);
-    }
-    if (qk_norm) {
-      const float ss = wave_sum(x1 * x1 + x2 * x2);
-      const float r = 1.0f / sqrtf(ss / (float)hd + eps);
-      if (act) {
-        x1 = x1 * r * kn[lane];
-        x2 = x2 * r * kn[lane + half];
-      }
-    }
-    const int64_t kvb = (int64_t)(b * n_kv + kvh);
-    if (act) {
-      const float2 cs = rope[(int64_t)m * half + lane];  // row m of this chunk, position pos
-      T* kd = Kc + (kvb * cap + pos) * hd;
-      st_f(kd + lane, x1 * cs.x - x2 * cs.y);
-      st_f(kd + lane + half, x2 * cs.x + x1 * cs.y);
-    }
-    const float* xv = src + (n_kv + kvh) * hd;
-    for (int d = lane; d < hd; d += 64) st_f(Vc + (kvb * hd + d) * cap + pos, sum_planes(0.f, xv + d, pstride, S));
+  const int kvh = blockIdx.x * 4 + wave;  // one wave per (row, kv head)
+  if (kvh >= n_kv) return;
+  const float* x = src + kvh * hd;
+  const float* xv = src + (n_kv + kvh) * hd;
+  const bool act = lane < half;
+  // every plane of the row's K pair and V entries is requested before any is summed
+  float pk1[kMaxPlanes], pk2[kMaxPlanes], pv[2][kMaxPlanes];
+#pragma unroll
+  for (int s = 0; s < kMaxPlanes; ++s) {
+    const bool on = s < S;
+    pk1[s] = on && act ? x[s * pstride + lane] : 0.f;
+    pk2[s] = on && act ? x[s * pstride + lane + half] : 0.f;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) pv[q][s] = on && lane + 64 * q < hd ? xv[s * pstride + lane + 64 * q] : 0.f;
   }
+  float x1 = 0.f, x2 = 0.f, v[2] = {0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < kMaxPlanes; ++s) {
+    if (s < S) {
+      x1 += pk1[s];
+      x2 += pk2[s];
+      v[0] += pv[0][s];
+      v[1] += pv[1][s];
+    }
+  }
+  if (qk_norm) {
+    const float ss = wave_sum(x1 * x1 + x2 * x2);
+    const float r = 1.0f / sqrtf(ss / (float)hd + eps);
+    if (act) {
+      x1 = x1 * r * kn[lane];
+      x2 = x2 * r * kn[lane + half];
+    }
+  }
+  const int64_t kvb = (int64_t)(b * n_kv + kvh);
+  if (act) {
+    const float2 cs = rope[(int64_t)m * half + lane];  // row m of this chunk, position pos
+    T* kd = Kc + (kvb * cap + pos) * hd;
+    st_f(kd + lane, x1 * cs.x - x2 * cs.y);
+    st_f(kd + lane + half, x2 * cs.x + x1 * cs.y);
+  }
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+    if (lane + 64 * q < hd) st_f(Vc + (kvb * hd + lane + 64 * q) * cap + pos, v[q]);
 }
 
 __global__ void ctx_len_update_kernel(int B, int n_max, int cap, const int* n_new, int* ctx_len, int* status) {

@@ -494,12 +494,13 @@ hipError_t run_pipe(const GemmArgs& a, hipStream_t st) {
 //             320x96 tiles of 4 waves, 80 x (48 gate + 48 up) each).  The
 //             fp32-store GEMMs (QKV, O, down, append) split K so that about 256 workgroups
 //             run; their consumers add the S partial planes (gemm_splits).
-//  M <= 1024: 64x128 tiles, 3-deep ring;
+//  M <= 64 (the context append, up to gamma+1 rows per request) and 320 < M <= 1024:
+//             64x128 tiles, 3-deep ring;
 //  larger   : 256x256 tiles, 8 waves (128x64 per wave), 2-deep ring.
 template <int EPI>
 hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
   if (a.M > 1024) return run_pipe<256, 256, 2, 4, 2, 128, EPI>(a, st);
-  if (a.M > 320) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
+  if (a.M > 320 || (a.M <= 64 && EPI != EPI_SWIGLU)) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
   // SwiGLU: 48 gate + 48 up rows per tile, so that the Qwen3-8B FFN (12288) gives 256 tiles
   if constexpr (EPI == EPI_SWIGLU) return run_pipe<320, 96, 4, 1, 2, 128, EPI>(a, st);
   return run_pipe<320, 128, 4, 2, 2, 128, EPI>(a, st);
