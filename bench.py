@@ -358,7 +358,7 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": gf / g_avg_s / 1e12, "peak": peak_flops, "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["kernel"] = "gemm_pipe_kernel<320, 96, 4, 1, 2, 128, 2, 0>" if M <= 320 else "gemm_pipe_kernel (gate/up SwiGLU)"
+    roof["kernel"] = "gemm_adir_kernel<2, 4>" if M <= 320 else "gemm_pipe_kernel (gate/up SwiGLU)"
     roof["traffic"] = recorded_traffic(roof["kernel"]) if wl.name == "qwen3_8b_b1" else None
     roof["algorithmic_bytes_per_launch"] = gb
     roof["algorithmic_flops_per_launch"] = gf

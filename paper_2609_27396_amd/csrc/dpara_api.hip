@@ -113,6 +113,7 @@ int check_ctx(const dpara_ctx_t* x, int batch) {
 struct Plan {
   int B, R, Rp, M, S, chunk, CH, esz;
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
+  bool afrag;              // normed activations in MFMA fragment order (QKV and gate/up GEMMs)
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
       hflag, F, KV32, rope_app, csplit, cpart;
@@ -153,7 +154,9 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.h_chunk = ar_head_chunk(c->dtype == DPARA_BF16 ? 1 : 0, c->ar_rank);
   p.h_chunks = (c->vocab + p.h_chunk - 1) / p.h_chunk;
   const int amode = c->dtype == DPARA_BF16 ? A_BF16 : A_F32;
-  p.s_qkv = gemm_splits(amode, EPI_STORE_F32, p.M, (nq + 2 * nkv) * hd, H);
+  // Up to 320 rows the GEMMs fed by an RMSNorm read their activations in fragment order.
+  p.afrag = c->dtype == DPARA_BF16 && p.M <= 320 && H % 256 == 0;
+  p.s_qkv = gemm_splits(p.afrag ? A_BF16_FRAG : amode, EPI_STORE_F32, p.M, (nq + 2 * nkv) * hd, H);
   p.s_o = gemm_splits(amode, EPI_STORE_F32, p.M, H, nq * hd);
   p.s_down = gemm_splits(amode, EPI_STORE_F32, p.M, H, c->ffn);
   const size_t M = p.M;
@@ -164,7 +167,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
     return o;
   };
   p.X = take(M * H * 4);
-  p.A = take(M * H * p.esz);
+  p.A = take((p.afrag ? (M + 15) / 16 * 16 : M) * H * p.esz);
   p.QKV = take((size_t)p.s_qkv * M * (nq + 2 * nkv) * hd * 4);
   p.Q = take(M * (size_t)nq * hd * p.esz);
   p.Kb = take((size_t)B * nkv * p.Rp * hd * p.esz);  // [Rp][hd] per request and KV head
@@ -289,9 +292,13 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     const dpara_layer_weights_t& Lw = layers[l];
     {
     Phase ph("rmsnorm", st);
-    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, P, pend, (int64_t)M * H, 1, Lw.attn_norm, cfg->rms_eps,
-                           at<void>(ws, p.A), st),
-            "attn_norm");
+    if (p.afrag)
+      HIP_TRY(launch_rmsnorm_frag(M, H, X, P, pend, (int64_t)M * H, Lw.attn_norm, cfg->rms_eps, at<void>(ws, p.A), st),
+              "attn_norm");
+    else
+      HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, P, pend, (int64_t)M * H, 1, Lw.attn_norm, cfg->rms_eps,
+                             at<void>(ws, p.A), st),
+              "attn_norm");
     pend = 0;
     }
     GemmArgs q{};
@@ -310,7 +317,7 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     q.splits = p.s_qkv;
     {
     Phase ph("qkv_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_STORE_F32, q, st), "qkv gemm");
+    HIP_TRY(launch_gemm(p.afrag ? A_BF16_FRAG : amode, EPI_STORE_F32, q, st), "qkv gemm");
     }
     {
     Phase ph("qk_norm_rope", st);
@@ -358,9 +365,13 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     }
     {
     Phase ph("rmsnorm", st);
-    HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, P, p.s_o, (int64_t)M * H, 1, Lw.mlp_norm, cfg->rms_eps,
-                           at<void>(ws, p.A), st),
-            "mlp_norm");
+    if (p.afrag)
+      HIP_TRY(launch_rmsnorm_frag(M, H, X, P, p.s_o, (int64_t)M * H, Lw.mlp_norm, cfg->rms_eps, at<void>(ws, p.A), st),
+              "mlp_norm");
+    else
+      HIP_TRY(launch_rmsnorm(dt, M, H, X, M, 0, 0, P, p.s_o, (int64_t)M * H, 1, Lw.mlp_norm, cfg->rms_eps,
+                             at<void>(ws, p.A), st),
+              "mlp_norm");
     }
     GemmArgs gu{};
     gu.A = at<void>(ws, p.A);
@@ -376,7 +387,7 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     gu.ldc = F;
     {
     Phase ph("gateup_gemm", st);
-    HIP_TRY(launch_gemm(amode, EPI_SWIGLU, gu, st), "gate/up gemm");
+    HIP_TRY(launch_gemm(p.afrag ? A_BF16_FRAG : amode, EPI_SWIGLU, gu, st), "gate/up gemm");
     }
     GemmArgs dn{};
     dn.A = at<void>(ws, p.Hmid);

@@ -87,7 +87,8 @@ __global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, in
 // split-K partial planes of that row (added in plane order); optionally x is written back
 // into X; y = x / rms(x) * g.
 constexpr int kNormThreads = 512;
-template <typename TO, int VN>
+// FRAG: Y is bf16 in MFMA fragment order (frag_index) instead of row-major.
+template <typename TO, int VN, int FRAG = 0>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, int grp, int64_t in_stride,
                                                              int in_off, const float* P, int S, int64_t pstride,
                                                              int write_back, const float* g, float eps, TO* Y) {
@@ -109,12 +110,21 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, in
   }
   ss = block_sum<kNormThreads / 64>(ss, red);
   const float r = 1.0f / sqrtf(ss / (float)H + eps);
-  TO* y = Y + (int64_t)m * H;
+  // fragment order: 4 consecutive k of one row stay consecutive (k % 8 is 0 or 4)
+  TO* y = FRAG ? Y : Y + (int64_t)m * H;
 #pragma unroll
   for (int t = 0; t < VN; ++t) {
     const int i = (threadIdx.x + kNormThreads * t) * 4;
     if (i < H) {
       const float4 gg = *(const float4*)(g + i);
+      if (FRAG) {
+        TO* yf = Y + frag_index(m, i, H);
+        st_f(yf + 0, v[t].x * r * gg.x);
+        st_f(yf + 1, v[t].y * r * gg.y);
+        st_f(yf + 2, v[t].z * r * gg.z);
+        st_f(yf + 3, v[t].w * r * gg.w);
+        continue;
+      }
       st_f(y + i + 0, v[t].x * r * gg.x);
       st_f(y + i + 1, v[t].y * r * gg.y);
       st_f(y + i + 2, v[t].z * r * gg.z);
@@ -336,6 +346,25 @@ hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int
   if (out_dtype == 1)
     return rmsnorm_dispatch<bf16_t>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st);
   return rmsnorm_dispatch<float>(rows, H, X, grp, in_stride, in_off, P, S, pstride, write_back, g, eps, Y, st);
+}
+
+hipError_t launch_rmsnorm_frag(int rows, int H, float* X, const float* P, int S, int64_t pstride,
+                               const float* g, float eps, void* Y, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (H > 16 * kNormThreads || H % 32 || S < 0 || S > kMaxPlanes) return hipErrorInvalidValue;
+  const int vn = (H / 4 + kNormThreads - 1) / kNormThreads;
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(rows), dim3(kNormThreads), 0, st, H, X, rows, (int64_t)0, 0, P, S, pstride, 1, g,
+                       eps, (bf16_t*)Y);
+    return hipGetLastError();
+  };
+  switch (vn) {
+    case 1: return go(rmsnorm_rows<bf16_t, 1, 1>);
+    case 2: return go(rmsnorm_rows<bf16_t, 2, 1>);
+    case 3: return go(rmsnorm_rows<bf16_t, 3, 1>);
+    case 4: return go(rmsnorm_rows<bf16_t, 4, 1>);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len, int pos_off,

@@ -1,11 +1,12 @@
 // Dense projections of the drafter: C[M, N] (op)= A[M, K] . B[N, K]^T.
 //
 // bf16 path: v_mfma_f32_16x16x32_bf16 kernels with fp32 accumulation and fused
-// epilogues (store fp32, add into the fp32 residual stream, SwiGLU -> bf16).  The
-// projections use a multi-stage direct-to-LDS pipeline (gemm_pipe_kernel); the LM head,
-// whose fp32 A operand is split into bf16 hi + lo on the way into LDS, uses a
-// register-staged double-buffered kernel (gemm_mfma_kernel).  The tile order is XCD-aware: the M tiles that share one weight
-// tile run on the same XCD back to back, so a weight tile is fetched from HBM once
+// epilogues (store fp32 or split-K fp32 planes, SwiGLU -> bf16, per-tile top-2 keys).
+// gemm_pipe_kernel streams both operands through a multi-stage direct-to-LDS ring; the LM
+// head's fp32 A operand arrives as two bf16 planes (hi + lo) that both meet every weight
+// tile.  gemm_adir_kernel (M <= 320) takes A in MFMA fragment order straight into registers
+// and only the weights through LDS.  Tile orders are XCD-aware: the tiles that share one
+// weight tile run on the same XCD back to back, so a weight tile is fetched from HBM once
 // and served to the others from that XCD's L2.
 // float32 path: a plain LDS-tiled FMA kernel for the float32 model configuration.
 #include "common.h"
@@ -14,8 +15,6 @@
 namespace dpara {
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;  // padded LDS row in bf16 elements (144 bytes)
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + expf(-g)); }
 
@@ -249,81 +248,66 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
   }
 }
 
-template <int BM, int BN, int EPI, int AMODE>
-__global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs a, int MT, int NT) {
-  constexpr int NA = (AMODE == A_F32SPLIT) ? 2 : 1;
-  constexpr int WM = BM / 2, WN = BN / 2;
-  constexpr int FM = WM / 16, FN = WN / 16;
-  constexpr int A_LD = (AMODE == A_F32SPLIT) ? BM * BK / 4 / 256 : BM * BK / 8 / 256;
-  constexpr int B_LD = BN * BK / 8 / 256;
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][NA][BM * LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LDK];
 
+// ------------------------------------------------------------------ float32 FMA path
+// ------------------------------------------------------------ fragment-ordered A path
+// For M <= 320 one 320-row tile covers every row, so each workgroup multiplies the whole
+// activation operand with its own weight slice: A is re-read by every workgroup, the weights
+// once.  A therefore bypasses LDS: it arrives in MFMA fragment order (frag_index), and each
+// of the 4 waves (one per SIMD) loads the fragments of its own 80 rows straight into a
+// register ring SB stages deep (one 16-byte load per lane per 1 KB block).  Only the weight
+// tile (96 rows of B per 64-deep K step) goes through an LDS ring filled by direct DMA and
+// read by all four waves.  Row blocks past the last valid one are clamped to it (their
+// accumulator rows are never stored).  SwiGLU tiles hold 48 gate + 48 up columns; the fp32
+// store splits K over `splits` workgroups writing planes [S][M][ldc].
+template <int EPI, int SB>
+__global__ __launch_bounds__(256) void gemm_adir_kernel(GemmArgs a, int NT) {
+  constexpr int BM = 320, BN = 96, BKB = 128, KB = 64, KS = KB / 32, CH = BKB / 16, RPI = 1024 / BKB;
+  constexpr int NW = 4, WM = BM / NW, FM = WM / 16, FN = BN / 16;
+  constexpr int B_INS = BN / RPI / NW;
+  constexpr int STAGE_BYTES = BN * BKB;
+  static_assert(B_INS * RPI * NW == BN, "weight rows must split evenly over waves");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+  const int S = a.splits;
   int mt, nt;
-  tile_of(blockIdx.x, MT, NT, mt, nt);
-  const int m0 = mt * BM;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  tile_of(blockIdx.x / S, 1, NT, mt, nt);
+  const int split = blockIdx.x % S;
+  const int Ks = a.K / S, kbeg = split * Ks;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lc = lane >> 4;
 
-  // global source rows of this thread's loads
-  const bf16_t* bp[B_LD];
-  bool bok[B_LD];
+  const int KC = a.K / 32, last_rb = (a.M - 1) >> 4;
+  const bf16_t* ap[FM];
 #pragma unroll
-  for (int i = 0; i < B_LD; ++i) bp[i] = b_row<bf16_t, BN, EPI>(a, nt, tid / 8 + 32 * i, bok[i]);
-  const int bcol = (tid & 7) * 8;
+  for (int mi = 0; mi < FM; ++mi) {
+    const int rb = min(wave * FM + mi, last_rb);
+    ap[mi] = (const bf16_t*)a.A + ((int64_t)rb * KC + kbeg / 32) * 512 + lane * 8;
+  }
+  const bf16_t* bsrc[B_INS];
+  const int lrow = lane / CH, lslot = lane % CH;
+#pragma unroll
+  for (int j = 0; j < B_INS; ++j) {
+    const int r = (wave + NW * j) * RPI + lrow;
+    bool ok;
+    bsrc[j] = b_row<bf16_t, BN, EPI>(a, nt, r, ok) + kbeg + swz<CH>(r, lslot) * 8;
+  }
 
-  uint4 ra[A_LD];
-  float4 rf[(AMODE == A_F32SPLIT) ? A_LD : 1];
-  uint4 rb[B_LD];
-
-  auto load_tile = [&](int kt) {
-    const int k0 = kt * BK;
-    if constexpr (AMODE == A_F32SPLIT) {
-      const float* A = (const float*)a.A;
+  bf16x8_t abuf[SB][KS][FM];
+  // K step k_ld's A fragments into register slot `buf`, its weight tile into LDS slot `slot`
+  auto issue = [&](int k_ld, int slot, int buf) {
 #pragma unroll
-      for (int i = 0; i < A_LD; ++i) {
-        const int gm = m0 + tid / 16 + 16 * i;
-        rf[i] = gm < a.M ? *(const float4*)(A + (int64_t)gm * a.lda + k0 + (tid & 15) * 4)
-                         : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-    } else {
-      const bf16_t* A = (const bf16_t*)a.A;
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int i = 0; i < A_LD; ++i) {
-        const int gm = m0 + tid / 8 + 32 * i;
-        ra[i] = gm < a.M ? *(const uint4*)(A + (int64_t)gm * a.lda + k0 + (tid & 7) * 8)
-                         : make_uint4(0, 0, 0, 0);
-      }
-    }
+      for (int mi = 0; mi < FM; ++mi)
+        abuf[buf][ks][mi] = *(const bf16x8_t*)(ap[mi] + (int64_t)(k_ld * KS + ks) * 512);
+    __builtin_amdgcn_sched_barrier(0);
+    unsigned char* sb = smem + slot * STAGE_BYTES;
 #pragma unroll
-    for (int i = 0; i < B_LD; ++i)
-      rb[i] = bok[i] ? *(const uint4*)(bp[i] + k0 + bcol) : make_uint4(0, 0, 0, 0);
-  };
-
-  auto store_tile = [&](int buf) {
-    if constexpr (AMODE == A_F32SPLIT) {
-#pragma unroll
-      for (int i = 0; i < A_LD; ++i) {
-        const int r = tid / 16 + 16 * i, c = (tid & 15) * 4;
-        const float x[4] = {rf[i].x, rf[i].y, rf[i].z, rf[i].w};
-        bf16_t hi[4], lo[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          hi[j] = f2bf(x[j]);
-          lo[j] = f2bf(x[j] - bf2f(hi[j]));
-        }
-        *(uint2*)&As[buf][0][r * LDK + c] =
-            make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-        *(uint2*)&As[buf][NA - 1][r * LDK + c] =
-            make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < A_LD; ++i)
-        *(uint4*)&As[buf][0][(tid / 8 + 32 * i) * LDK + (tid & 7) * 8] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) *(uint4*)&Bs[buf][(tid / 8 + 32 * i) * LDK + bcol] = rb[i];
+    for (int j = 0; j < B_INS; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(bsrc[j] + k_ld * KB), (lds_void_t*)(sb + (wave + NW * j) * 1024),
+                                       16, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   f32x4_t acc[FM][FN];
@@ -332,67 +316,65 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs a, int MT, int 
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = a.K / BK;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  const int lr = lane & 15, lk = (lane >> 4) * 8;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) load_tile(kt + 1);
+  // KT is a multiple of SB (host check).  Step kt's loads were issued SB-1 steps earlier;
+  // past the end the refill repeats the last step into a slot nobody reads again.
+  constexpr int PER = KS * FM + B_INS;  // vector memory instructions per issue
+  const int KT = Ks / KB;
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8_t bfr[FN];
+  for (int s = 0; s < SB - 1; ++s) issue(s, s, s);
+  for (int kt0 = 0; kt0 < KT; kt0 += SB) {
 #pragma unroll
-      for (int ni = 0; ni < FN; ++ni)
-        bfr[ni] = *(const bf16x8_t*)&Bs[buf][(b_frag_row<BN, WN, FN, EPI>(wn, ni) + lr) * LDK +
-                                             ks * 32 + lk];
+    for (int u = 0; u < SB; ++u) {
+      const int kt = kt0 + u;
+      wait_vmcnt<(SB - 2) * PER>();
+      __builtin_amdgcn_s_barrier();
+      const int nx = kt + SB - 1;
+      issue(min(nx, KT - 1), nx % SB, (u + SB - 1) % SB);
+      const unsigned char* sb = smem + (kt % SB) * STAGE_BYTES;
 #pragma unroll
-      for (int h = 0; h < NA; ++h) {
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c = ks * 4 + lc;
+        bf16x8_t bfr[FN];
 #pragma unroll
-        for (int mi = 0; mi < FM; ++mi) {
-          const bf16x8_t afr =
-              *(const bf16x8_t*)&As[buf][h][(wm * WM + mi * 16 + lr) * LDK + ks * 32 + lk];
+        for (int ni = 0; ni < FN; ++ni) {
+          const int r = b_frag_row<BN, BN, FN, EPI>(0, ni) + lr;
+          bfr[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
+        }
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
           for (int ni = 0; ni < FN; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[ni], acc[mi][ni], 0, 0, 0);
-        }
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(abuf[u][ks][mi], bfr[ni], acc[mi][ni], 0, 0, 0);
       }
     }
-    if (kt + 1 < KT) store_tile(buf ^ 1);
-    __syncthreads();
   }
+  wait_vmcnt<0>();
 
-  // epilogue: acc[mi][ni][r] = C[row = .. + 4*(lane/16) + r][col = .. + lane%16]
 #pragma unroll
   for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = m0 + wm * WM + mi * 16 + (lane >> 4) * 4 + r;
+      const int row = wave * WM + mi * 16 + lc * 4 + r;
       if (row >= a.M) continue;
       if constexpr (EPI == EPI_SWIGLU) {
         bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
 #pragma unroll
         for (int ni = 0; ni < FN / 2; ++ni) {
-          const int f = nt * (BN / 2) + wn * (WN / 2) + ni * 16 + lr;
+          const int f = nt * (BN / 2) + ni * 16 + lr;
           if (f < a.N) C[f] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
         }
       } else {
-        float* C = (float*)a.C + (int64_t)row * a.ldc;
+        float* C = (float*)a.C + ((int64_t)split * a.M + row) * a.ldc;
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni) {
-          const int col = nt * BN + wn * WN + ni * 16 + lr;
-          if (col < a.N) {
-            if constexpr (EPI == EPI_ADD_F32) C[col] += acc[mi][ni][r];
-            else C[col] = acc[mi][ni][r];
-          }
+          const int col = nt * BN + ni * 16 + lr;
+          if (col < a.N) C[col] = acc[mi][ni][r];
         }
       }
     }
   }
 }
 
-// ------------------------------------------------------------------ float32 FMA path
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int MT, int NT) {
   constexpr int BM = 64, BN = 64, BKF = 16;
@@ -455,19 +437,28 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int MT, int N
   }
 }
 
-template <int BM, int BN, int EPI, int AMODE>
-hipError_t run_mfma(const GemmArgs& a, hipStream_t st) {
-  const int MT = (a.M + BM - 1) / BM;
-  const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
-  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, EPI, AMODE>), dim3(MT * NT), dim3(256), 0, st, a, MT, NT);
-  return hipGetLastError();
-}
 
 template <int EPI>
 hipError_t run_f32(const GemmArgs& a, hipStream_t st) {
   const int MT = (a.M + 63) / 64;
   const int NT = EPI == EPI_SWIGLU ? (a.N + 31) / 32 : (a.N + 63) / 64;
   hipLaunchKernelGGL((gemm_f32_kernel<EPI>), dim3(MT * NT), dim3(256), 0, st, a, MT, NT);
+  return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t run_adir(const GemmArgs& a, hipStream_t st) {
+  constexpr int SB = 4, BN = 96, lds = SB * BN * 128;
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_STORE_F32, "fragment-ordered A: SwiGLU or fp32 store");
+  if (a.M > 320 || a.K % 32) return hipErrorInvalidValue;
+  if (a.splits < 1 || (a.splits > 1 && EPI != EPI_STORE_F32) || a.K % (a.splits * 64 * SB) != 0)
+    return hipErrorInvalidValue;
+  const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
+  auto kern = gemm_adir_kernel<EPI, SB>;
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kern, dim3(NT * a.splits), dim3(256), lds, st, a, NT);
   return hipGetLastError();
 }
 
@@ -509,6 +500,14 @@ hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
 }  // namespace
 
 int gemm_splits(int amode, int epi, int M, int N, int K) {
+  if (amode == A_BF16_FRAG) {
+    // 96-column tiles; K steps of each split a multiple of the 4-deep ring
+    if (epi != EPI_STORE_F32) return 1;
+    const int NT = (N + 95) / 96;
+    int S = 1;
+    while (S < 16 && NT * S * 2 <= 256 && K % (256 * S * 2) == 0) S *= 2;
+    return S;
+  }
   if (amode != A_BF16 || epi != EPI_STORE_F32 || M > 320) return 1;
   const int NT = (N + 127) / 128;
   int S = 1;
@@ -519,7 +518,7 @@ int gemm_splits(int amode, int epi, int M, int N, int K) {
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.splits < 1) return hipErrorInvalidValue;
-  if (a.splits > 1 && amode != A_BF16) return hipErrorInvalidValue;
+  if (a.splits > 1 && amode != A_BF16 && amode != A_BF16_FRAG) return hipErrorInvalidValue;
   if (amode == A_F32) {
     switch (epi) {
       case EPI_STORE_F32: return run_f32<EPI_STORE_F32>(a, st);
@@ -541,11 +540,12 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }
   if (epi == EPI_TOP2) return hipErrorInvalidValue;
-  const bool small = a.M <= 512;
-  if (amode == A_F32SPLIT) {
-    return small ? run_mfma<64, 128, EPI_STORE_F32, A_F32SPLIT>(a, st)
-                 : run_mfma<128, 128, EPI_STORE_F32, A_F32SPLIT>(a, st);
+  if (amode == A_BF16_FRAG) {
+    if (epi == EPI_SWIGLU) return run_adir<EPI_SWIGLU>(a, st);
+    if (epi == EPI_STORE_F32) return run_adir<EPI_STORE_F32>(a, st);
+    return hipErrorInvalidValue;
   }
+  if (amode != A_BF16) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_STORE_BF16: return run_bf16<EPI_STORE_BF16>(a, st);
     case EPI_STORE_F32: return run_bf16<EPI_STORE_F32>(a, st);

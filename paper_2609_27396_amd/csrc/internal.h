@@ -22,12 +22,21 @@ struct Phase {
 // C[M, N] (op)= A[M, K] . B[N, K]^T with B given in up to three row segments
 // (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2).
 enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3, EPI_TOP2 = 4 };
-// A_BF16: A is bf16.  A_F32SPLIT: A is float32 and is applied as hi + lo bf16 parts
-// (two MFMA passes), which keeps ~16 significant bits of A.  A_F32: float32 FMA kernel
+// A_BF16: A is bf16, row-major with leading dimension lda.  A_F32: float32 FMA kernel
 // (the float32 model path; B is then float32 too).
 // A_BF16_DUAL: A given as two bf16 planes hi (at A) and lo (at A + lo_off elements) with
 // hi + lo = the float32 operand to ~16 significant bits; both planes meet every weight tile.
-enum GemmAMode { A_BF16 = 0, A_F32SPLIT = 1, A_F32 = 2, A_BF16_DUAL = 3 };
+// A_BF16_FRAG: A is bf16 in MFMA fragment order (frag_index; lda unused), M <= 320,
+// K a multiple of 256 * splits; EPI_SWIGLU or EPI_STORE_F32 only.
+enum GemmAMode { A_BF16 = 0, A_BF16_FRAG = 1, A_F32 = 2, A_BF16_DUAL = 3 };
+
+// Element (row, k) of a bf16 operand stored in MFMA fragment order: blocks of 16 rows x 32 k
+// (ceil(rows/16) x K/32 of them, row blocks outermost), each 64 lanes x 8 values, where lane
+// l holds row 16*rb + l%16 and k = 32*kc + 8*(l/16) .. +7.  One wave loads one block (1 KB)
+// with one 16-byte load per lane, already in the operand layout of v_mfma_f32_16x16x32_bf16.
+__host__ __device__ inline int64_t frag_index(int row, int k, int K) {
+  return ((int64_t)(row >> 4) * (K >> 5) + (k >> 5)) * 512 + ((((k & 31) >> 3) << 4) + (row & 15)) * 8 + (k & 7);
+}
 
 struct GemmArgs {
   const void* A;
@@ -88,6 +97,10 @@ hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V
 hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int64_t in_stride,
                           int in_off, const float* P, int S, int64_t pstride, int write_back,
                           const float* g, float eps, void* Y, hipStream_t st);
+// The same with Y written as bf16 in MFMA fragment order (frag_index, K = H; rows past
+// `rows` in the last 16-row block are left untouched).  H a multiple of 32.
+hipError_t launch_rmsnorm_frag(int rows, int H, float* X, const float* P, int S, int64_t pstride,
+                               const float* g, float eps, void* Y, hipStream_t st);
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len,
                              int pos_off, float2* table, hipStream_t st);
 // QKV: S fp32 planes [S][B*R][(n_q+2n_kv)*hd], summed in order.
