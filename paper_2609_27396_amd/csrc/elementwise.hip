@@ -1,6 +1,8 @@
 // Row assembly, RMSNorm, q/k-norm + RoPE and the context-append kernels.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -9,17 +11,6 @@ namespace {
 
 constexpr int kMaxPlanes = 16;  // split-K partial planes a consumer may have to add
 
-// acc + p[0] + p[stride] + ... + p[(n-1)*stride], added in plane order; all n loads are
-// issued before the first add so that their latencies overlap.
-__device__ __forceinline__ float sum_planes(float acc, const float* p, int64_t stride, int n) {
-  float v[kMaxPlanes];
-#pragma unroll
-  for (int s = 0; s < kMaxPlanes; ++s) v[s] = s < n ? p[s * stride] : 0.f;
-#pragma unroll
-  for (int s = 0; s < kMaxPlanes; ++s)
-    if (s < n) acc += v[s];
-  return acc;
-}
 // float4 form for the row kernels: planes are loaded in batches of 4 (bounded registers,
 // still 4 loads in flight per slot), added in plane order.
 __device__ __forceinline__ float4 sum_planes4(float4 acc, const float* p, int64_t stride, int n) {
@@ -145,65 +136,89 @@ __global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx
   table[((int64_t)b * n_pos + i) * half + p] = make_float2(c, s);
 }
 
-// Grid (head-slot groups of 4, rows): one wave per (row, head slot); the slots are the q heads,
-// then the k heads, then the v heads of the fused QKV row, summed over the S split-K planes.
+// Grid (head-slot groups, rows): HD/4 lanes per (row, head slot), 4 consecutive entries per
+// lane, so a wave covers 64 / (HD/4) slots; the slots are the q heads, then the k heads, then
+// the v heads of the fused QKV row, summed over the S split-K planes (in plane order).  The
+// rotate-half partner of a lane's entries sits HD/8 lanes away in the same group.
 // In-block keys are stored [Rp][hd] and values transposed [hd][Rp] per request and KV head
 // (Rp = R rounded up to 64 keys) for the MFMA attention pass.
-template <typename T>
-__global__ __launch_bounds__(256) void qk_norm_rope(int R, int Rp, int gamma, int n_q, int n_kv, int hd, int qk_norm,
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void qk_norm_rope(int R, int Rp, int gamma, int n_q, int n_kv, int qk_norm,
                                                     float eps, const float* QKV, int S, int64_t pstride,
-                                                    const float* qn,
-                                                    const float* kn, const float2* table, T* Q, T* Kb,
-                                                    T* Vb) {
+                                                    const float* qn, const float* kn, const float2* table, T* Q,
+                                                    T* Kb, T* Vb) {
+  constexpr int LPS = HD / 4, SPW = 64 / LPS, HALF = HD / 2;
   const int m = blockIdx.y;
   const int b = m / R, row = m % R;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int half = hd / 2, grp = n_q / n_kv;
-  const int n_slots = n_q + 2 * n_kv;
-  const float* src = QKV + (int64_t)m * n_slots * hd;
-  const float2* cs = table + ((int64_t)b * (2 * gamma + 1) + row_pos_offset(row, gamma)) * half;
-  {
-    const int slot = blockIdx.x * 4 + wave;  // one wave per head slot (q heads, k heads, v heads)
-    if (slot >= n_slots) return;
-    const float* x = src + slot * hd;
-    if (slot < n_q + n_kv) {
-      const bool isq = slot < n_q;
-      const bool act = lane < half;
-      float x1 = 0.f, x2 = 0.f;
-      if (act) {
-        x1 = sum_planes(0.f, x + lane, pstride, S);
-        x2 = sum_planes(0.f, x + lane + half, pstride, S);
-      }
-      if (qk_norm) {
-        const float ss = wave_sum(x1 * x1 + x2 * x2);
-        const float r = 1.0f / sqrtf(ss / (float)hd + eps);
-        const float* gn = isq ? qn : kn;
-        if (act) {
-          x1 = x1 * r * gn[lane];
-          x2 = x2 * r * gn[lane + half];
-        }
-      }
-      if (act) {
-        const float2 c = cs[lane];
-        const float y1 = x1 * c.x - x2 * c.y;
-        const float y2 = x2 * c.x + x1 * c.y;
-        T* dst;
-        if (isq) {
-          const int h = slot, kvh = h / grp, gi = h % grp;
-          dst = Q + (((int64_t)(b * n_kv + kvh) * grp + gi) * R + row) * hd;
-        } else {
-          const int kvh = slot - n_q;
-          dst = Kb + ((int64_t)(b * n_kv + kvh) * Rp + row) * hd;
-        }
-        st_f(dst + lane, y1);
-        st_f(dst + lane + half, y2);
-      }
-    } else {
-      const int kvh = slot - n_q - n_kv;
-      T* dst = Vb + (int64_t)(b * n_kv + kvh) * hd * Rp + row;  // transposed: [hd][Rp]
-      for (int d = lane; d < hd; d += 64) st_f(dst + (int64_t)d * Rp, sum_planes(0.f, x + d, pstride, S));
+  const int sl = lane % LPS, j0 = sl * 4;
+  const int slot = (blockIdx.x * 4 + wave) * SPW + lane / LPS;
+  const int grp = n_q / n_kv, n_slots = n_q + 2 * n_kv;
+  const bool valid = slot < n_slots;
+  const float* x = QKV + ((int64_t)m * n_slots + (valid ? slot : 0)) * HD + j0;
+  float4 pv[kMaxPlanes];
+#pragma unroll
+  for (int s = 0; s < kMaxPlanes; ++s)
+    pv[s] = (valid && s < S) ? *(const float4*)(x + s * pstride) : make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int s = 0; s < kMaxPlanes; ++s)
+    if (s < S) {
+      v.x += pv[s].x;
+      v.y += pv[s].y;
+      v.z += pv[s].z;
+      v.w += pv[s].w;
     }
+  if (slot >= n_q + n_kv) {  // values (or past the last slot): transposed store [hd][Rp]
+    if (!valid) return;
+    const int kvh = slot - n_q - n_kv;
+    T* dst = Vb + ((int64_t)(b * n_kv + kvh) * HD + j0) * Rp + row;
+    st_f(dst, v.x);
+    st_f(dst + Rp, v.y);
+    st_f(dst + 2 * Rp, v.z);
+    st_f(dst + 3 * (int64_t)Rp, v.w);
+    return;
   }
+  // q/k slots: whole lane groups take this branch together (the v slots follow them)
+  const bool isq = slot < n_q;
+  if (qk_norm) {
+    float ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+    for (int o = LPS / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    const float r = 1.0f / sqrtf(ss / (float)HD + eps);
+    const float4 gg = *(const float4*)((isq ? qn : kn) + j0);
+    v.x = v.x * r * gg.x;
+    v.y = v.y * r * gg.y;
+    v.z = v.z * r * gg.z;
+    v.w = v.w * r * gg.w;
+  }
+  float4 pr;  // the rotate-half partner entries
+  pr.x = __shfl_xor(v.x, LPS / 2, 64);
+  pr.y = __shfl_xor(v.y, LPS / 2, 64);
+  pr.z = __shfl_xor(v.z, LPS / 2, 64);
+  pr.w = __shfl_xor(v.w, LPS / 2, 64);
+  const bool first = j0 < HALF;
+  const float2* cs = table + ((int64_t)b * (2 * gamma + 1) + row_pos_offset(row, gamma)) * HALF + (j0 % HALF);
+  const float2 c0 = cs[0], c1 = cs[1], c2 = cs[2], c3 = cs[3];
+  // first half: y = x cos - x' sin; second half: y = x cos + x' sin (x' = the partner entry)
+  const float sg = first ? -1.f : 1.f;
+  const float y0 = v.x * c0.x + sg * pr.x * c0.y;
+  const float y1 = v.y * c1.x + sg * pr.y * c1.y;
+  const float y2 = v.z * c2.x + sg * pr.z * c2.y;
+  const float y3 = v.w * c3.x + sg * pr.w * c3.y;
+  if (!valid) return;
+  T* dst;
+  if (isq) {
+    const int kvh = slot / grp, gi = slot % grp;
+    dst = Q + (((int64_t)(b * n_kv + kvh) * grp + gi) * R + row) * HD + j0;
+  } else {
+    const int kvh = slot - n_q;
+    dst = Kb + ((int64_t)(b * n_kv + kvh) * Rp + row) * HD + j0;
+  }
+  st_f(dst, y0);
+  st_f(dst + 1, y1);
+  st_f(dst + 2, y2);
+  st_f(dst + 3, y3);
 }
 
 template <typename T>
@@ -379,16 +394,19 @@ hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ct
 hipError_t launch_qk_norm_rope(int dtype, int B, int R, int Rp, int gamma, int n_q, int n_kv, int hd, int qk_norm,
                                float eps, const float* QKV, int S, const float* qn, const float* kn,
                                const float2* table, void* Q, void* Kb, void* Vb, hipStream_t st) {
-  if (Rp < R || S < 1 || S > kMaxPlanes) return hipErrorInvalidValue;
-  dim3 grid((n_q + 2 * n_kv + 3) / 4, B * R);
-  const int64_t pstride = (int64_t)B * R * (n_q + 2 * n_kv) * hd;
+  if (Rp < R || S < 1 || S > kMaxPlanes || (hd != 64 && hd != 128)) return hipErrorInvalidValue;
+  const int n_slots = n_q + 2 * n_kv, per_block = 4 * (256 / hd);
+  dim3 grid((n_slots + per_block - 1) / per_block, B * R);
+  const int64_t pstride = (int64_t)B * R * n_slots * hd;
+  auto go = [&](auto kern, auto* q) {
+    using TT = std::remove_pointer_t<decltype(q)>;
+    hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, R, Rp, gamma, n_q, n_kv, qk_norm, eps, QKV, S, pstride, qn, kn,
+                       table, (TT*)Q, (TT*)Kb, (TT*)Vb);
+    return hipGetLastError();
+  };
   if (dtype == 1)
-    hipLaunchKernelGGL(qk_norm_rope<bf16_t>, grid, dim3(256), 0, st, R, Rp, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
-                       S, pstride, qn, kn, table, (bf16_t*)Q, (bf16_t*)Kb, (bf16_t*)Vb);
-  else
-    hipLaunchKernelGGL(qk_norm_rope<float>, grid, dim3(256), 0, st, R, Rp, gamma, n_q, n_kv, hd, qk_norm, eps, QKV,
-                       S, pstride, qn, kn, table, (float*)Q, (float*)Kb, (float*)Vb);
-  return hipGetLastError();
+    return hd == 128 ? go(qk_norm_rope<bf16_t, 128>, (bf16_t*)nullptr) : go(qk_norm_rope<bf16_t, 64>, (bf16_t*)nullptr);
+  return hd == 128 ? go(qk_norm_rope<float, 128>, (float*)nullptr) : go(qk_norm_rope<float, 64>, (float*)nullptr);
 }
 
 hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int H, const void* feats,
