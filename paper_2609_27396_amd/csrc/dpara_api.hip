@@ -189,9 +189,11 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.hwpart = take((size_t)head_prune_wparts() * 4);                // pruned head: |W_v|^2 maxima
   p.hflag = 4;  // pruned head: fallback flag, int32 in the header after the status word
   p.F = take((size_t)B * p.CH * H * p.esz);
-  // append K|V planes: split only when the append GEMM has at most 320 rows (16 planes max)
+  // append K|V planes of one layer group: split only when the append GEMM has at most 320
+  // rows (16 planes max)
+  const int app_layers = c->n_layers < kMaxAppendLayers ? c->n_layers : kMaxAppendLayers;
   const size_t kv_rows = (size_t)B * p.CH > 16 * 320 ? (size_t)B * p.CH : 16 * 320;
-  p.KV32 = take(kv_rows * 2 * nkv * hd * 4);
+  p.KV32 = take(kv_rows * app_layers * 2 * nkv * hd * 4);
   p.rope_app = take((size_t)B * p.CH * (hd / 2) * 8);  // (cos, sin) of the appended rows' positions
   // branch candidates (bf16): hi/lo planes of every branch row and the per-tile top-2 words
   const size_t crows = (size_t)B * (c->gamma + 1) * c->gamma;
@@ -490,17 +492,22 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
     HIP_TRY(launch_gather_feats(dt, batch, CH, c0, n_max, H, feats, at<void>(ws, p.F), st), "gather_feats");
     HIP_TRY(launch_rope_table(batch, CH, hd, cfg->rope_base, ctx->ctx_len, c0, at<float2>(ws, p.rope_app), st),
             "rope_table");
-    for (int l = 0; l < cfg->n_layers; ++l) {
+    // All layers project the same features: up to kMaxAppendLayers layers share one K|V GEMM
+    // (weight segments W_k, W_v of each layer) and one store launch.
+    for (int l0 = 0; l0 < cfg->n_layers; l0 += kMaxAppendLayers) {
+      const int nl = cfg->n_layers - l0 < kMaxAppendLayers ? cfg->n_layers - l0 : kMaxAppendLayers;
       GemmArgs g{};
       g.A = at<void>(ws, p.F);
       g.lda = H;
-      g.B0 = w->layers[l].wk;
-      g.B1 = w->layers[l].wv;
-      g.B2 = w->layers[l].wv;
-      g.n1 = nkv * hd;
-      g.n2 = 2 * nkv * hd;
+      g.seg_rows = nkv * hd;
+      KvLayers kn{};
+      for (int j = 0; j < nl; ++j) {
+        g.seg[2 * j] = w->layers[l0 + j].wk;
+        g.seg[2 * j + 1] = w->layers[l0 + j].wv;
+        kn.kn[j] = w->layers[l0 + j].k_norm;
+      }
       g.M = batch * CH;
-      g.N = 2 * nkv * hd;
+      g.N = nl * 2 * nkv * hd;
       g.K = H;
       g.C = at<void>(ws, p.KV32);
       g.ldc = g.N;
@@ -509,12 +516,11 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
         Phase ph("append_gemm", st);
         HIP_TRY(launch_gemm(dt == DPARA_BF16 ? A_BF16 : A_F32, EPI_STORE_F32, g, st), "append kv gemm");
       }
-      char* kc = (char*)ctx->k + l * layer_elems * esz;
-      char* vc = (char*)ctx->v + l * layer_elems * esz;
       Phase ph("append_store", st);
       HIP_TRY(launch_kv_store(dt, batch, CH, c0, n_max, nkv, hd, cfg->qk_norm, cfg->rms_eps,
-                              at<float2>(ws, p.rope_app), at<float>(ws, p.KV32), g.splits, w->layers[l].k_norm, n_new, ctx->ctx_len, ctx->ctx_cap, kc,
-                              vc, status, st),
+                              at<float2>(ws, p.rope_app), at<float>(ws, p.KV32), g.splits, nl, kn, n_new,
+                              ctx->ctx_len, ctx->ctx_cap, (char*)ctx->k + l0 * layer_elems * esz,
+                              (char*)ctx->v + l0 * layer_elems * esz, layer_elems, status, st),
               "kv_store");
     }
   }

@@ -241,20 +241,23 @@ __device__ __forceinline__ int clamp_count(int n, int n_max) { return n < 0 ? 0 
 
 // K/V of appended rows: k = RoPE(kNorm(W_k f)) at its position, v = W_v f; K rows go to
 // [pos][hd], V to the transposed cache [hd][pos].
+// Grid (kv-head groups of 4, rows, layers).
 template <typename T>
 __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n_kv, int hd, int qk_norm, float eps,
                                                 const float2* rope, const float* KV, int S, int64_t pstride,
-                                                const float* kn,
-                                                const int* n_new, const int* ctx_len, int cap, T* Kc,
-                                                T* Vc) {
-  const int m = blockIdx.y, b = m / CH, i = m % CH;
+                                                KvLayers kls, const int* n_new, const int* ctx_len, int cap,
+                                                T* Kc, T* Vc, int64_t layer_elems) {
+  const int m = blockIdx.y, b = m / CH, i = m % CH, l = blockIdx.z, nl = gridDim.z;
   const int c = c0 + i;
   if (c >= clamp_count(n_new[b], n_max)) return;
   const int pos = max(ctx_len[b], 0) + c;
   if (pos >= cap) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = hd / 2;
-  const float* src = KV + (int64_t)m * 2 * n_kv * hd;
+  const float* kn = kls.kn[l];
+  Kc += l * layer_elems;
+  Vc += l * layer_elems;
+  const float* src = KV + ((int64_t)m * nl + l) * 2 * n_kv * hd;
   const int kvh = blockIdx.x * 4 + wave;  // one wave per (row, kv head)
   if (kvh >= n_kv) return;
   const float* x = src + kvh * hd;
@@ -421,18 +424,21 @@ hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int 
 }
 
 hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd, int qk_norm,
-                           float eps, const float2* rope, const float* KV, int S, const float* kn, const int* n_new,
-                           const int* ctx_len, int cap, void* Kc, void* Vc, int* status, hipStream_t st) {
+                           float eps, const float2* rope, const float* KV, int S, int nl, const KvLayers& kn,
+                           const int* n_new, const int* ctx_len, int cap, void* Kc, void* Vc, size_t layer_elems,
+                           int* status, hipStream_t st) {
   (void)status;
-  if (S < 1 || S > kMaxPlanes) return hipErrorInvalidValue;
-  const int64_t pstride = (int64_t)B * CH * 2 * n_kv * hd;
-  const dim3 grid((n_kv + 3) / 4, B * CH);
+  if (S < 1 || S > kMaxPlanes || nl < 1 || nl > kMaxAppendLayers) return hipErrorInvalidValue;
+  const int64_t pstride = (int64_t)B * CH * nl * 2 * n_kv * hd;
+  const dim3 grid((n_kv + 3) / 4, B * CH, nl);
   if (dtype == 1)
     hipLaunchKernelGGL(kv_store<bf16_t>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
-                       rope, KV, S, pstride, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc);
+                       rope, KV, S, pstride, kn, n_new, ctx_len, cap, (bf16_t*)Kc, (bf16_t*)Vc,
+                       (int64_t)layer_elems);
   else
     hipLaunchKernelGGL(kv_store<float>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
-                       rope, KV, S, pstride, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc);
+                       rope, KV, S, pstride, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc,
+                       (int64_t)layer_elems);
   return hipGetLastError();
 }
 

@@ -42,6 +42,10 @@ __device__ __forceinline__ const TB* b_row(const GemmArgs& a, int nt, int lr, bo
     int n = nt * BN + lr;
     ok = n < a.N;
     if (!ok) n = 0;
+    if (a.seg_rows > 0) {
+      const int si = n / a.seg_rows;
+      return (const TB*)a.seg[si] + (int64_t)(n - si * a.seg_rows) * a.K;
+    }
     if (n < a.n1) return (const TB*)a.B0 + (int64_t)n * a.K;
     if (n < a.n2) return (const TB*)a.B1 + (int64_t)(n - a.n1) * a.K;
     return (const TB*)a.B2 + (int64_t)(n - a.n2) * a.K;
@@ -510,13 +514,16 @@ int gemm_splits(int amode, int epi, int M, int N, int K) {
   }
   if (amode != A_BF16 || epi != EPI_STORE_F32 || M > 320) return 1;
   const int NT = (N + 127) / 128;
+  const int max_wg = M <= 64 ? 512 : 256;  // the M <= 64 tile fits two workgroups per CU
   int S = 1;
-  while (S < 16 && NT * S * 2 <= 256 && K % (64 * S * 2) == 0 && K / (S * 2) >= 256) S *= 2;
+  while (S < 16 && NT * S * 2 <= max_wg && K % (64 * S * 2) == 0 && K / (S * 2) >= 256) S *= 2;
   return S;
 }
 
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.seg_rows < 0 || (a.seg_rows > 0 && (epi == EPI_SWIGLU || a.N > kMaxGemmSegs * a.seg_rows)))
+    return hipErrorInvalidValue;
   if (a.splits < 1) return hipErrorInvalidValue;
   if (a.splits > 1 && amode != A_BF16 && amode != A_BF16_FRAG) return hipErrorInvalidValue;
   if (amode == A_F32) {

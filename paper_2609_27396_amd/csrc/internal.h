@@ -20,7 +20,8 @@ struct Phase {
 
 // ---------------------------------------------------------------- GEMM
 // C[M, N] (op)= A[M, K] . B[N, K]^T with B given in up to three row segments
-// (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2).
+// (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2), or, with seg_rows > 0 (not for
+// EPI_SWIGLU), in equal segments: row n from seg[n / seg_rows], row n % seg_rows.
 enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3, EPI_TOP2 = 4 };
 // A_BF16: A is bf16, row-major with leading dimension lda.  A_F32: float32 FMA kernel
 // (the float32 model path; B is then float32 too).
@@ -57,8 +58,11 @@ struct GemmArgs {
   // uint64 words at C + (row * ldc + t) * 3 (the value's float bits in the low word);
   // columns past N do not count.  ldc >= ceil(N / 128).
   const int* only_if = nullptr;  // non-NULL: every workgroup returns at once unless *only_if != 0
+  int seg_rows = 0;               // > 0: B rows from seg[] (N <= kMaxGemmSegs * seg_rows)
+  const void* seg[16] = {};
 };
 
+constexpr int kMaxGemmSegs = 16;
 hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st);
 // Split-K factor launch_gemm uses for a bf16 fp32-store GEMM of this shape (1 = no split).
 // The consumer of C sums the S planes in order 0..S-1.
@@ -110,12 +114,18 @@ hipError_t launch_qk_norm_rope(int dtype, int B, int R, int Rp, int gamma, int n
                                void* Vb, hipStream_t st);
 hipError_t launch_gather_feats(int dtype, int B, int CH, int c0, int n_max, int H,
                                const void* feats, void* F, hipStream_t st);
-// KV: S fp32 planes [S][B*CH][2*n_kv*hd], summed in order.
+// K/V of the appended rows for nl consecutive layers: KV holds S fp32 planes
+// [S][B*CH][nl][2*n_kv*hd] (layer j's K then V entries), summed in order; layer j uses
+// kn[j] and writes the caches at Kc/Vc + j * layer_elems.
 // rope: [B*CH][hd/2] (cos, sin) of row m's position max(ctx_len[b], 0) + c0 + (m % CH).
+constexpr int kMaxAppendLayers = 8;
+struct KvLayers {
+  const float* kn[kMaxAppendLayers];
+};
 hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv, int hd,
                            int qk_norm, float eps, const float2* rope, const float* KV, int S,
-                           const float* kn, const int* n_new, const int* ctx_len, int cap,
-                           void* Kc, void* Vc, int* status, hipStream_t st);
+                           int nl, const KvLayers& kn, const int* n_new, const int* ctx_len, int cap,
+                           void* Kc, void* Vc, size_t layer_elems, int* status, hipStream_t st);
 hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, int* ctx_len,
                                  int* status, hipStream_t st);
 hipError_t launch_clear_status(int* status, hipStream_t st);
