@@ -156,26 +156,37 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const unsigned char* sa = smem + (kt % STAGES) * STAGE_BYTES;
     const unsigned char* sb = sa + A_ROWS * BKB;
-#pragma unroll
-    for (int ks = 0; ks < KB / 32; ++ks) {
+    // Fragments of k-step ks+1 are read from LDS before k-step ks's MFMAs are issued (two
+    // register sets), so the LDS latency hides behind the math.
+    auto load_frags = [&](int ks, bf16x8_t(&af)[NPL][FM], bf16x8_t(&bf)[FN]) {
       const int c = ks * 4 + lc;
-      bf16x8_t bfr[FN];
 #pragma unroll
       for (int ni = 0; ni < FN; ++ni) {
         const int r = b_frag_row<BN, WN, FN, EPI>(wn, ni) + lr;
-        bfr[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
+        bf[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
       }
 #pragma unroll
-      for (int pl = 0; pl < NPL; ++pl) {
+      for (int pl = 0; pl < NPL; ++pl)
 #pragma unroll
         for (int mi = 0; mi < FM; ++mi) {
           const int r = pl * BM + wm * WM + mi * 16 + lr;
-          const bf16x8_t afr = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
+          af[pl][mi] = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
+        }
+    };
+    bf16x8_t af[2][NPL][FM], bfr[2][FN];
+    load_frags(0, af[0], bfr[0]);
+#pragma unroll
+    for (int ks = 0; ks < KB / 32; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < KB / 32) load_frags(ks + 1, af[cur ^ 1], bfr[cur ^ 1]);
+      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of this step's MFMAs
+#pragma unroll
+      for (int pl = 0; pl < NPL; ++pl)
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
           for (int ni = 0; ni < FN; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[ni], acc[mi][ni], 0, 0, 0);
-        }
-      }
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[cur][pl][mi], bfr[cur][ni], acc[mi][ni], 0, 0, 0);
     }
   }
 
