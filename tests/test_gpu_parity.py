@@ -214,8 +214,42 @@ def test_head_from_branch_candidates(regime):
         check_head(shape, w, dr, "bf16", b)
 
 
-def test_append_equivalence_and_determinism():
-    shape, _ = SMALL_CASES["h256_hd128_g5"]
+# Nine layers: the context append projects K|V for at most eight layers per GEMM, so this
+# takes two layer groups (8 + 1), each layer with its own W_k, W_v and k-norm gains.
+L9_SHAPE = synth.DrafterShape(n_layers=9, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=512,
+                              vocab=3000, gamma=4, ar_rank=64, qk_norm=True, dtype="bf16")
+
+
+def test_append_layer_groups_against_oracle():
+    """Every layer's cached K and V after the prefill (context append over nine layers, two
+    projection groups) is that layer's own incremental projection of the cached features:
+    the oracle's context K/V within one bf16 rounding.  (The nine-layer reps themselves are
+    not held to the single-layer bar: bf16 rounding flips compound through depth.)"""
+    shape, ctx = L9_SHAPE, [45, 130]
+    wl = synth.Workload("l9", shape, batch=len(ctx), ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=7)
+    w = synth.make_weights(shape, seed=3, gain_jitter=0.1)
+    ri = synth.make_round(wl, ctx_lens=ctx)
+    DeviceRound = _harness()
+    dr = DeviceRound(shape, w, ri)
+    torch.cuda.synchronize()
+    assert dr.status() == 0
+    rnd = O.Rounding("bf16")
+    worst = 0.0
+    for b, n in enumerate(ctx):
+        for l in range(shape.n_layers):
+            k_ref, v_ref = O.context_kv(shape, w, l, ri.ctx_feats[b], 0, rnd)
+            k = dr.ctx.k[l, b, :, :n].float().cpu().numpy().transpose(1, 0, 2)     # [n, n_kv, hd]
+            v = dr.ctx.v[l, b, :, :, :n].float().cpu().numpy().transpose(2, 0, 1)  # [n, n_kv, hd]
+            for got, ref in ((k, k_ref), (v, v_ref)):
+                err = np.abs(got - ref)
+                worst = max(worst, float((err / (np.abs(ref) + 1e-4)).max()))
+                assert np.all(err <= 2.0 ** -7 * np.abs(ref) + 1e-4), (b, l)
+    _say("l9 append: worst relative |cache - oracle|", worst)
+
+
+@pytest.mark.parametrize("case", ["h256_hd128_g5", "l9"])
+def test_append_equivalence_and_determinism(case):
+    shape = L9_SHAPE if case == "l9" else SMALL_CASES[case][0]
     wl = synth.Workload("app", shape, batch=2, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=9)
     w = synth.make_weights(shape, seed=4)
     ri = synth.make_round(wl, ctx_lens=[120, 61])
