@@ -267,6 +267,7 @@ def main():
     ap.add_argument("--workload", default="qwen3_8b_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-head-sweep", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="skip timing the step as HIP graph replays")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run a plain 256 MiB device copy 3 times (known HBM bytes, to scale "
                          "profiler traffic counters)")
@@ -329,6 +330,28 @@ def main():
     ms = ev0.elapsed_time(ev1) / args.steps
     log(f"[bench] {args.steps} steps: {ms:.3f} ms/step")
 
+    # the same step captured into a HIP graph and replayed K times (same kernels, same work)
+    graph_ms = None
+    if not args.no_graph:
+        g = torch.cuda.CUDAGraph()
+        cs = torch.cuda.Stream()
+        cs.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cs):
+            with torch.cuda.graph(g, stream=cs):
+                step()
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(args.steps):
+            g.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        graph_ms = ev0.elapsed_time(ev1) / args.steps
+        assert dr.status() == 0, f"device status {dr.status()}"
+        log(f"[bench] {args.steps} graph replays: {graph_ms:.3f} ms/step")
+
     # per-phase durations (HIP events recorded by the library on the launching stream)
     prof_steps = 5
     D.dpara_profile_enable(True)
@@ -385,6 +408,7 @@ def main():
         "verify_us_per_round": 1000.0 * sum_ms(["verify"]),
         "append_us_per_round": 1000.0 * sum_ms(["append_gemm", "append_store"]),
         "phases": phases,
+        "graph_ms_per_step": graph_ms,
     }
     if shape.dtype == "bf16" and not args.no_head_sweep:
         hs = head_sweep(dr, shape)

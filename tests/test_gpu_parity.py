@@ -448,3 +448,65 @@ def test_backbone_and_target_on_concurrent_streams():
         torch.cuda.synchronize()
         assert torch.equal(reps1, dr.reps)
         assert torch.equal(l1, l2)
+
+
+# ----------------------------------------------------------------------------- HIP graph of a round
+@pytest.mark.parametrize("case", ["h256_hd128_g5", "qwen3_8b_b1"])
+def test_round_graph_replays(case):
+    """One steady-state round (context rewind, append of the accepted rows' features,
+    all-boundary backbone, greedy verify, select + head) captured into a HIP graph: every
+    replay, with eager work that overwrites the outputs and synchronisations between the
+    replays, gives the eager round's results bit for bit (the library takes all scratch from
+    the caller's workspace and launches only kernels on the caller's stream)."""
+    if case == "qwen3_8b_b1":
+        wl = synth.WORKLOADS[case]
+        w = synth.make_weights(wl.shape, seed=wl.seed_w)
+        ri = synth.make_round(wl)
+    else:
+        shape, ctx = SMALL_CASES[case]
+        wl = synth.Workload(case, shape, batch=len(ctx), ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=7,
+                            logits_dtype="bf16")
+        w = synth.make_weights(shape, seed=3, gain_jitter=0.1)
+        ri = synth.make_round(wl, ctx_lens=ctx)
+    DeviceRound = _harness()
+    dr = DeviceRound(wl.shape, w, ri)
+    B = wl.batch
+    n_new_h = ri.accept_planted.astype(np.int32) + 1
+    n_new = torch.from_numpy(n_new_h).cuda()
+    base_len = torch.from_numpy((ri.ctx_lens - n_new_h).astype(np.int32)).cuda()
+    outs = ("reps", "accept", "bonus", "targmax", "gathered", "drafts", "next_spine", "margins")
+
+    def step():
+        dr.ctx.ctx_len[:B].copy_(base_len)
+        dr.append(n_new)
+        dr.backbone()
+        dr.verify()
+        dr.head()
+
+    step()  # eager (also the first call of every launcher outside the capture)
+    torch.cuda.synchronize()
+    assert dr.status() == 0
+    ref = {k: getattr(dr, k).clone() for k in outs}
+    ref_len = dr.ctx.ctx_len.clone()
+    ref_k, ref_v = dr.ctx.k.clone(), dr.ctx.v.clone()
+    g = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cs):
+        with torch.cuda.graph(g, stream=cs):
+            step()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for k in outs:  # eager work between the replays
+            t = getattr(dr, k)
+            t.fill_(-7 if t.dtype == torch.int32 else float("nan"))
+        dr.ctx.ctx_len.fill_(0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in outs:
+            assert torch.equal(getattr(dr, k), ref[k]), (rep, k)
+        assert torch.equal(dr.ctx.ctx_len, ref_len)
+        assert torch.equal(dr.ctx.k, ref_k) and torch.equal(dr.ctx.v, ref_v)
+        assert dr.status() == 0
+    _say(case, "graph replays identical to the eager round: 4")
