@@ -215,6 +215,35 @@ def recorded_traffic(kernel: str):
     return float(rec["bytes_per_launch"])
 
 
+def fuse_timing(shape, rows=(17, 2048), n_feat=3, iters=20):
+    """Feature fusion (the step before the cache update) alone: f = RMSNorm(fc [h_1; h_2;
+    h_3]) * g for a round's rows at b=1 and for a 2048-row prefill, on device-generated
+    weights and hidden states (microseconds per call, and the call's weight + row bytes
+    over its time)."""
+    import torch
+    from paper_2609_27396_amd import dpara as D, synth
+    fus = D.DeviceFusion(shape, None, n_feat)
+    H = shape.hidden
+    out = {}
+    for n in rows:
+        hid = synth.device_normal_(torch.empty((n, n_feat * H), dtype=torch.bfloat16, device="cuda"), 13 + n)
+        f = torch.empty((n, H), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty(D.dpara_fuse_workspace_bytes(fus.cfg, n, n_feat), dtype=torch.uint8, device="cuda")
+        for _ in range(3):
+            D.fuse_features(fus, hid, f, ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            D.fuse_features(fus, hid, f, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        us = 1000.0 * e0.elapsed_time(e1) / iters
+        nbytes = H * n_feat * H * 2 + n * n_feat * H * 2 + n * H * 2
+        out[str(n)] = {"us": us, "GB_s": nbytes / us / 1e3}
+    return out
+
+
 def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
     """Select + AR head alone at several batch sizes, on synthetic branch representations
     (microseconds per call): the plain call (gather, LM head over gamma rows, gamma AR
@@ -414,6 +443,8 @@ def main():
         hs = head_sweep(dr, shape)
         out["head_us_by_batch"] = hs.pop("plain_us")
         out["head_variants_by_batch"] = hs
+    if shape.dtype == "bf16" and not args.no_head_sweep:
+        out["fuse_by_rows"] = fuse_timing(shape)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(wl, weights, ri)

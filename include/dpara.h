@@ -236,6 +236,27 @@ int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t
                          const dpara_ctx_t* ctx, int32_t batch, const int32_t* block, void* logits,
                          int32_t logits_dtype, void* ws, size_t ws_bytes, void* stream);
 
+/* Feature fusion, the step before the cache update (Section 3.2, "Trainable and frozen
+ * parameters": the projection that fuses the concatenated multi-layer target features, and
+ * the input normalization).  For every row x of `hidden` (the target's hidden states at
+ * n_feat layers, concatenated): f = RMSNorm(x fc^T) * norm (eps cfg->rms_eps), the fused
+ * feature dpara_ctx_append takes.  The projection accumulates in float32; f is rounded to
+ * the cfg dtype.
+ * hidden: [n_rows, n_feat * hidden] (device, cfg dtype, 16-byte aligned).
+ * feats:  [n_rows, hidden] (device, cfg dtype, output, 16-byte aligned).
+ * ws: dpara_fuse_workspace_bytes(cfg, n_rows, n_feat) bytes, 256-byte aligned (its own
+ *     scratch: it need not be the drafter's workspace).  n_feat in [1, 8]; any n_rows >= 1
+ *     (rows are processed in passes of at most 4096). */
+typedef struct dpara_fusion_weights {
+  const void* fc;     /* [hidden, n_feat * hidden] (device, cfg dtype), no bias */
+  const float* norm;  /* [hidden] (device) */
+  int32_t n_feat;
+} dpara_fusion_weights_t;
+
+size_t dpara_fuse_workspace_bytes(const dpara_config_t* cfg, int32_t n_rows, int32_t n_feat);
+int dpara_fuse_features(const dpara_config_t* cfg, const dpara_fusion_weights_t* fw, int32_t n_rows,
+                        const void* hidden, void* feats, void* ws, size_t ws_bytes, void* stream);
+
 /* Enqueue a clear of the status word at byte offset 0 of `ws` (a fill kernel). */
 int dpara_clear_status(void* ws, void* stream);
 
@@ -246,7 +267,7 @@ int dpara_clear_status(void* ws, void* stream);
  * and returns their summed duration and launch count.  Phases: "append_gemm",
  * "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
  * "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather",
- * "lm_head", "ar_step".  Not for use while a stream is being captured into a graph. */
+ * "lm_head", "ar_step", "fuse_gemm", "fuse_norm".  Not for use while a stream is being captured into a graph. */
 int dpara_profile_enable(int32_t on);
 int dpara_profile_read(const char* phase, double* total_ms, int64_t* count);
 

@@ -185,6 +185,18 @@ def row_positions(gamma: int, n_b: int) -> np.ndarray:
 # ----------------------------------------------------------------------------
 # drafter layers
 # ----------------------------------------------------------------------------
+def fuse_features(shape, wf, hidden, mode: str = "bf16"):
+    """Fused target features, the rows the feature cache C takes (Section 3.2, "Trainable
+    and frozen parameters": the projection fusing the concatenated multi-layer target
+    features, and the input normalization).  Reading R16: f = RMSNorm(fc x) * g for x the
+    concatenation of the target's hidden states at n_feat layers, fc [H, n_feat*H] without
+    bias; the projection is kept in float32 and the result rounded to the cache dtype.
+    hidden: [n, n_feat*H] -> [n, H]."""
+    rnd = Rounding(mode)
+    x = rnd.r32(_f64(hidden) @ _f64(wf["fc"]).T)
+    return rnd.r16(rmsnorm(x, wf["fc_norm"], shape.rms_eps))
+
+
 def context_kv(shape, w, layer: int, feats, pos0: int, rnd: Rounding):
     """Per-layer K/V of cached fused target features (incremental projection).
 

@@ -696,6 +696,70 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
   return DPARA_OK;
 }
 
+// Feature fusion: passes of at most kFuseChunk rows; the fp32 projection goes to split-K
+// planes (up to 16 of them for a pass of at most 320 rows) that the RMSNorm adds.
+namespace {
+constexpr int kFuseChunk = 4096;
+size_t fuse_ws_bytes(const dpara_config_t* c, int n_rows) {
+  const size_t small = (size_t)16 * (n_rows < 320 ? n_rows : 320);
+  const size_t big = (size_t)(n_rows < kFuseChunk ? n_rows : kFuseChunk);
+  return 256 + up256((small > big ? small : big) * c->hidden * 4);
+}
+}  // namespace
+
+size_t dpara_fuse_workspace_bytes(const dpara_config_t* cfg, int32_t n_rows, int32_t n_feat) {
+  if (check_cfg(cfg) || n_rows < 1 || n_feat < 1 || n_feat > 8) return 0;
+  return fuse_ws_bytes(cfg, n_rows);
+}
+
+int dpara_fuse_features(const dpara_config_t* cfg, const dpara_fusion_weights_t* fw, int32_t n_rows,
+                        const void* hidden, void* feats, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!fw) return fail(DPARA_E_INVALID, "fusion weights are NULL");
+  CHECK_PTR(fw->fc, "fc");
+  CHECK_PTR(fw->norm, "fusion norm");
+  if (fw->n_feat < 1 || fw->n_feat > 8) return fail(DPARA_E_INVALID, "n_feat must be in [1, 8]");
+  if (n_rows < 1) return fail(DPARA_E_INVALID, "n_rows must be >= 1");
+  CHECK_PTR(hidden, "hidden");
+  CHECK_PTR(feats, "feats");
+  if (!aligned16(hidden) || !aligned16(feats)) return fail(DPARA_E_INVALID, "hidden and feats must be 16-byte aligned");
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
+  const size_t need = fuse_ws_bytes(cfg, n_rows);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  const int H = cfg->hidden, K = fw->n_feat * cfg->hidden, dt = cfg->dtype;
+  const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
+  const size_t esz = dt == DPARA_BF16 ? 2 : 4;
+  float* planes = at<float>(ws, 256);
+  for (int r0 = 0; r0 < n_rows; r0 += kFuseChunk) {
+    const int m = n_rows - r0 < kFuseChunk ? n_rows - r0 : kFuseChunk;
+    GemmArgs g{};
+    g.A = (const char*)hidden + (size_t)r0 * K * esz;
+    g.lda = K;
+    g.B0 = g.B1 = g.B2 = fw->fc;
+    g.n1 = g.n2 = H;
+    g.M = m;
+    g.N = H;
+    g.K = K;
+    g.C = planes;
+    g.ldc = H;
+    g.splits = gemm_splits(amode, EPI_STORE_F32, m, H, K);
+    {
+      Phase ph("fuse_gemm", st);
+      HIP_TRY(launch_gemm(amode, EPI_STORE_F32, g, st), "fusion gemm");
+    }
+    // plane 0 stands in for the residual row; the other planes are added to it
+    Phase ph("fuse_norm", st);
+    HIP_TRY(launch_rmsnorm(dt, m, H, planes, m, 0, 0, planes + (size_t)m * H, g.splits - 1, (int64_t)m * H, 0,
+                           fw->norm, cfg->rms_eps, (char*)feats + (size_t)r0 * H * esz, st),
+            "fusion norm");
+  }
+  return DPARA_OK;
+}
+
 size_t dpara_branch_candidates_bytes(const dpara_config_t* cfg, int32_t batch) {
   if (check_cfg(cfg) || batch < 1) return 0;
   return head_cand_bytes(batch, cfg->gamma);

@@ -25,11 +25,12 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_verify_greedy", "dpara_select_and_head", "dpara_branch_candidates_bytes",
            "dpara_branch_candidates", "dpara_select_and_head_cand", "dpara_clear_status",
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
-           "dpara_target_workspace_bytes", "dpara_target_forward")
+           "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_fuse_workspace_bytes",
+           "dpara_fuse_features")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
-          "ar_step")
+          "ar_step", "fuse_gemm", "fuse_norm")
 
 
 class DparaError(RuntimeError):
@@ -60,6 +61,10 @@ class DparaWeights(ctypes.Structure):
 class DparaTargetWeights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
                 ("layers", ctypes.POINTER(DparaLayerWeights))]
+
+
+class DparaFusionWeights(ctypes.Structure):
+    _fields_ = [("fc", ctypes.c_void_p), ("norm", ctypes.c_void_p), ("n_feat", ctypes.c_int32)]
 
 
 class DparaCtx(ctypes.Structure):
@@ -96,6 +101,9 @@ def lib():
         L.dpara_target_workspace_bytes.restype = SZ
         L.dpara_target_forward.argtypes = [P(DparaConfig), P(DparaTargetWeights), P(DparaCtx), I32, VP, VP, I32,
                                            VP, SZ, VP]
+        L.dpara_fuse_workspace_bytes.argtypes = [P(DparaConfig), I32, I32]
+        L.dpara_fuse_workspace_bytes.restype = SZ
+        L.dpara_fuse_features.argtypes = [P(DparaConfig), P(DparaFusionWeights), I32, VP, VP, VP, SZ, VP]
         L.dpara_last_error.restype = ctypes.c_char_p
         L.dpara_version.restype = I32
         L.dpara_profile_enable.argtypes = [I32]
@@ -103,7 +111,7 @@ def lib():
         for name in ("dpara_ctx_append", "dpara_backbone_all_boundaries", "dpara_verify_greedy",
                      "dpara_select_and_head", "dpara_branch_candidates", "dpara_select_and_head_cand",
                      "dpara_clear_status", "dpara_profile_enable",
-                     "dpara_profile_read", "dpara_target_forward"):
+                     "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -369,6 +377,43 @@ def select_and_head_cand(d: DeviceDrafter, reps, cand, accept_len, bonus, gather
     dpara_select_and_head_cand(d.cfg, d.w, int(accept_len.shape[0]), _ptr(reps), _ptr(cand), _ptr(accept_len),
                                _ptr(bonus), _ptr(gathered), _ptr(drafts), _ptr(next_spine), _ptr(margins), ws.ptr,
                                ws.nbytes, _stream(stream))
+
+
+def dpara_fuse_workspace_bytes(cfg, n_rows: int, n_feat: int) -> int:
+    return int(lib().dpara_fuse_workspace_bytes(ctypes.byref(cfg), n_rows, n_feat))
+
+
+def dpara_fuse_features(cfg, fw, n_rows, hidden, feats, ws, ws_bytes, stream):
+    _check(lib().dpara_fuse_features(_ref(cfg), _ref(fw), n_rows, hidden, feats, ws, ws_bytes, stream))
+
+
+class DeviceFusion:
+    """Feature-fusion weights resident in HBM (fc [H, n_feat*H], norm gain [H]) plus the
+    C struct that points at them."""
+
+    def __init__(self, shape, weights: dict | None, n_feat: int, device="cuda", seed: int = 7):
+        import torch
+        from . import synth
+        self.shape = shape
+        self.cfg = make_config(shape)
+        mdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        if weights is None:  # generated on device (timing only)
+            self.fc = synth.device_normal_(torch.empty((shape.hidden, n_feat * shape.hidden), dtype=mdt,
+                                                       device=device), seed, 0.02)
+            self.norm = torch.ones(shape.hidden, dtype=torch.float32, device=device)
+        else:
+            self.fc = torch.from_numpy(np.ascontiguousarray(weights["fc"])).to(device=device, dtype=mdt)
+            self.norm = torch.from_numpy(np.ascontiguousarray(weights["fc_norm"])).to(device=device,
+                                                                                       dtype=torch.float32)
+        self.n_feat = n_feat
+        self.w = DparaFusionWeights(fc=_ptr(self.fc), norm=_ptr(self.norm), n_feat=n_feat)
+
+
+def fuse_features(f: DeviceFusion, hidden, feats, ws, stream=None):
+    """hidden [n, n_feat*H] -> feats [n, H] (cfg dtype, on device); ws a uint8 device tensor
+    of at least dpara_fuse_workspace_bytes bytes."""
+    n = int(hidden.shape[0])
+    dpara_fuse_features(f.cfg, f.w, n, _ptr(hidden), _ptr(feats), _ptr(ws), int(ws.numel()), _stream(stream))
 
 
 def target_forward(t: DeviceTarget, ctx: DeviceContext, block, logits, ws: Workspace, stream=None):

@@ -213,6 +213,23 @@ def make_target_weights(s: DrafterShape, seed: int = 100, **kw) -> dict:
     return w
 
 
+def make_fusion_weights(s: DrafterShape, n_feat: int = 3, seed: int = 0, gain_jitter: float = 0.0,
+                        weight_std: float = 0.02) -> dict:
+    """The feature-fusion projection `fc` [H, n_feat*H] (N(0, weight_std), bf16-valued in
+    bf16 mode) and its RMSNorm gain `fc_norm` [H] (float32)."""
+    fc, g = normal_tensors([(7, (s.hidden, n_feat * s.hidden), weight_std, 0.0, s.dtype == "bf16"),
+                            (8, (s.hidden,), gain_jitter, 1.0, False)], seed)
+    return {"fc": fc, "fc_norm": g}
+
+
+def make_target_hidden(s: DrafterShape, n_rows: int, n_feat: int = 3, seed: int = 1,
+                       std: float = 1.0) -> np.ndarray:
+    """Concatenated target hidden states [n_rows, n_feat*H] of the rows to be fused,
+    N(0, std) (bf16-valued in bf16 mode)."""
+    (h,) = normal_tensors([(9, (n_rows, n_feat * s.hidden), std, 0.0, s.dtype == "bf16")], seed)
+    return h
+
+
 def make_target_cache(s: DrafterShape, ctx_lens, seed: int = 101):
     """The target's own per-layer context K/V: k[l][b], v[l][b] of shape [n_b, n_kv, hd],
     N(0, 1) (bf16-valued in bf16 mode)."""

@@ -433,3 +433,24 @@ def test_target_forward_matches_hf_causal_lm_with_cache():
         vs = [cache.layers[l].values[0].permute(1, 0, 2).numpy() for l in range(s.n_layers)]
     got = O.target_forward(s, w, ks, vs, block, "exact")
     np.testing.assert_allclose(got, full[len(prefix):].numpy(), rtol=2e-5, atol=2e-5)
+
+
+def test_fuse_features_matches_torch_linear_rms_norm():
+    """The fusion projection against torch's own linear map and RMSNorm (float64), and the
+    invariant that unit gains give rows of mean square mean(y^2) / (mean(y^2) + eps)."""
+    s = synth.DrafterShape(n_layers=1, hidden=64, n_q_heads=2, n_kv_heads=1, head_dim=64, ffn=128,
+                           vocab=100, gamma=2, ar_rank=64, qk_norm=False, dtype="f32")
+    wf = synth.make_fusion_weights(s, n_feat=3, seed=5, gain_jitter=0.2)
+    x = synth.make_target_hidden(s, 7, n_feat=3, seed=6)
+    got = O.fuse_features(s, wf, x, "exact")
+    t = torch.nn.functional.linear(torch.from_numpy(x).double(), torch.from_numpy(wf["fc"]).double())
+    ref = torch.nn.functional.rms_norm(t, (64,), torch.from_numpy(wf["fc_norm"]).double(), eps=s.rms_eps)
+    np.testing.assert_allclose(got, ref.numpy(), rtol=1e-12, atol=1e-12)
+    wf1 = dict(wf, fc_norm=np.ones(64, np.float32))
+    f = O.fuse_features(s, wf1, x, "exact")
+    y = np.asarray(x, np.float64) @ np.asarray(wf["fc"], np.float64).T
+    ms = (y * y).mean(-1)
+    np.testing.assert_allclose((f * f).mean(-1), ms / (ms + s.rms_eps), rtol=1e-12)
+    # bf16 mode: the fused rows are bf16 values
+    fb = O.fuse_features(s, wf, x, "bf16")
+    np.testing.assert_array_equal(fb, O.round_bf16(fb))
