@@ -112,3 +112,25 @@ def test_binding_raises_loudly_on_error():
     with pytest.raises(D.DparaError) as e:
         D.dpara_verify_greedy(cfg, 1, FAKE, 9, FAKE, FAKE, FAKE, None, FAKE, 1 << 20, None)
     assert e.value.code == D.DPARA_E_UNSUPPORTED
+
+
+def test_fusion_validation_without_gpu():
+    """dpara_fuse_features rejects bad arguments on the host, before any launch."""
+    cfg = D.make_config(synth.QWEN3_8B)
+    need = D.dpara_fuse_workspace_bytes(cfg, 17, 3)
+    assert need > 0
+    assert D.dpara_fuse_workspace_bytes(cfg, 4100, 3) > need
+    assert D.dpara_fuse_workspace_bytes(cfg, 0, 3) == 0
+    assert D.dpara_fuse_workspace_bytes(cfg, 17, 9) == 0
+    fw = D.DparaFusionWeights(fc=FAKE, norm=FAKE, n_feat=3)
+    R = ctypes.byref
+    ws = 1 << 24  # 256-byte aligned, never dereferenced
+    assert _rc("dpara_fuse_features", R(cfg), R(fw), 17, FAKE, FAKE, ws, need - 1, None) == D.DPARA_E_WORKSPACE
+    assert _rc("dpara_fuse_features", R(cfg), R(fw), 0, FAKE, FAKE, ws, need, None) == D.DPARA_E_INVALID
+    assert _rc("dpara_fuse_features", R(cfg), R(fw), 17, FAKE + 8, FAKE, ws, need, None) == D.DPARA_E_INVALID
+    assert _rc("dpara_fuse_features", R(cfg), R(fw), 17, FAKE, FAKE, ws + 64, need, None) == D.DPARA_E_INVALID
+    bad = D.DparaFusionWeights(fc=FAKE, norm=FAKE, n_feat=0)
+    assert _rc("dpara_fuse_features", R(cfg), R(bad), 17, FAKE, FAKE, ws, need, None) == D.DPARA_E_INVALID
+    assert "n_feat" in D.dpara_last_error()
+    bad = D.DparaFusionWeights(fc=None, norm=FAKE, n_feat=3)
+    assert _rc("dpara_fuse_features", R(cfg), R(bad), 17, FAKE, FAKE, ws, need, None) == D.DPARA_E_INVALID
