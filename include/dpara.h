@@ -235,6 +235,15 @@ size_t dpara_target_workspace_bytes(const dpara_config_t* cfg, int32_t batch, in
 int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t* w,
                          const dpara_ctx_t* ctx, int32_t batch, const int32_t* block, void* logits,
                          int32_t logits_dtype, void* ws, size_t ws_bytes, void* stream);
+/* The same forward, also emitting the block rows' hidden states after n_feat layers (the
+ * multi-layer target features the drafter fuses, Section 3.2; dpara_fuse_features):
+ * feat_layers: [n_feat] int32 (HOST array), layer indices in [0, n_layers), n_feat in [0, 8];
+ * hidden: [batch, gamma+1, n_feat, hidden] bf16 (device, output, 16-byte aligned): the
+ *         residual stream of row t_j after layer feat_layers[i] at hidden[b][j][i]. */
+int dpara_target_forward_hidden(const dpara_config_t* cfg, const dpara_target_weights_t* w,
+                                const dpara_ctx_t* ctx, int32_t batch, const int32_t* block,
+                                void* logits, int32_t logits_dtype, const int32_t* feat_layers,
+                                int32_t n_feat, void* hidden, void* ws, size_t ws_bytes, void* stream);
 
 /* Feature fusion, the step before the cache update (Section 3.2, "Trainable and frozen
  * parameters": the projection that fuses the concatenated multi-layer target features, and

@@ -370,24 +370,32 @@ def select_and_head(shape, w, reps, r: int, bonus: int, mode: str = "bf16", teac
 # ----------------------------------------------------------------------------
 # target verification forward (Algorithm 1, Verify; Section 4.3.2 colocation)
 # ----------------------------------------------------------------------------
-def target_forward(shape, w, ctx_k, ctx_v, block, mode: str = "bf16"):
+def target_forward(shape, w, ctx_k, ctx_v, block, mode: str = "bf16", feat_layers=None):
     """The target forwards the block t_0..t_d of one request (Algorithm 1, Verify).
 
     A causal decoder with the same block structure as the drafter layers, reading its own
     cached context K/V per layer (ctx_k[l], ctx_v[l]: [n_b, n_kv, hd], already normed and
     rotated, as a decoder stores them); block token t_j sits at position n_b + j.  Final
     RMSNorm, then an untied LM head w["lm_head"] [V, H] (the normed hidden state is a
-    16-bit rounding point).  Returns logits [d+1, V] (row j scores the token after t_j)."""
+    16-bit rounding point).  Returns logits [d+1, V] (row j scores the token after t_j).
+    With feat_layers, also the rows' hidden states after those layers, rounded to 16 bits
+    (the multi-layer target features the drafter fuses, Section 3.2): (logits, hidden
+    [d+1, len(feat_layers), H])."""
     rnd = Rounding(mode)
     n = len(block)
     n_b = int(np.asarray(ctx_k[0]).shape[0])
     X = rnd.r32(np.stack([_f64(w["embed"][int(t)]) for t in block]))
     pos = n_b + np.arange(n)
     vis = np.tril(np.ones((n, n), bool))
+    feats = {}
     for l in range(shape.n_layers):
         X = layer_forward(shape, w, l, X, pos, _f64(ctx_k[l]), _f64(ctx_v[l]), vis, rnd)
+        feats[l] = rnd.r16(X)
     hN = rnd.r16(rmsnorm(X, w["final_norm"], shape.rms_eps))
-    return rnd.r32(hN @ _f64(w["lm_head"]).T)
+    logits = rnd.r32(hN @ _f64(w["lm_head"]).T)
+    if feat_layers is None:
+        return logits
+    return logits, np.stack([feats[int(l)] for l in feat_layers], axis=1)
 
 
 def dpara_round(shape, w, ctx_feats, spine, target_logits, mode: str = "bf16"):

@@ -271,9 +271,12 @@ namespace {
 // O + residual -> RMSNorm -> gate|up + SwiGLU -> down + residual).  spine_only selects the
 // causal block (the target's verification pass); otherwise rows follow the tree layout.
 // Leaves the residual stream in ws[p.X].
+// hid_layers / n_hid / hid: optionally emit the rows' hidden state after those layers
+// (hid[m * n_hid + j] after layer hid_layers[j], bf16).
 int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, const void* embed,
                 const void* mask_emb, const dpara_ctx_t* ctx, int32_t batch, const int32_t* tokens,
-                int spine_only, const Plan& p, void* ws, hipStream_t st, int* pending) {
+                int spine_only, const Plan& p, void* ws, hipStream_t st, int* pending,
+                const int32_t* hid_layers = nullptr, int n_hid = 0, void* hid = nullptr) {
   const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q_heads, nkv = cfg->n_kv_heads;
   const int g = cfg->gamma, R = p.R, M = p.M, F = cfg->ffn;
   const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
@@ -407,6 +410,9 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     HIP_TRY(launch_gemm(amode, EPI_STORE_F32, dn, st), "down gemm");
     }
     pend = p.s_down;
+    for (int j = 0; j < n_hid; ++j)
+      if (hid_layers[j] == l)
+        HIP_TRY(launch_emit_hidden(M, H, X, P, pend, (int64_t)M * H, hid, n_hid, j, st), "emit hidden");
   }
   *pending = pend;
   return DPARA_OK;
@@ -566,7 +572,24 @@ size_t dpara_target_workspace_bytes(const dpara_config_t* cfg, int32_t batch, in
 int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t* w, const dpara_ctx_t* ctx,
                          int32_t batch, const int32_t* block, void* logits, int32_t logits_dtype, void* ws,
                          size_t ws_bytes, void* stream) {
+  return dpara_target_forward_hidden(cfg, w, ctx, batch, block, logits, logits_dtype, nullptr, 0, nullptr, ws,
+                                     ws_bytes, stream);
+}
+
+int dpara_target_forward_hidden(const dpara_config_t* cfg, const dpara_target_weights_t* w, const dpara_ctx_t* ctx,
+                                int32_t batch, const int32_t* block, void* logits, int32_t logits_dtype,
+                                const int32_t* feat_layers, int32_t n_feat, void* hidden, void* ws,
+                                size_t ws_bytes, void* stream) {
   if (!cfg) return fail(DPARA_E_INVALID, "cfg is NULL");
+  if (n_feat < 0 || n_feat > 8) return fail(DPARA_E_INVALID, "n_feat must be in [0, 8]");
+  if (n_feat > 0) {
+    if (!feat_layers) return fail(DPARA_E_INVALID, "feat_layers is NULL");
+    CHECK_PTR(hidden, "hidden");
+    if (!aligned16(hidden)) return fail(DPARA_E_INVALID, "hidden is not 16-byte aligned");
+    for (int j = 0; j < n_feat; ++j)
+      if (feat_layers[j] < 0 || feat_layers[j] >= cfg->n_layers)
+        return fail(DPARA_E_INVALID, "feat_layers[%d] = %d outside [0, n_layers)", j, feat_layers[j]);
+  }
   dpara_config_t c = *cfg;
   c.ar_rank = 64;  // the target has no AR head
   int rc = check_cfg(&c);
@@ -593,7 +616,9 @@ int dpara_target_forward(const dpara_config_t* cfg, const dpara_target_weights_t
   if ((rc = check_device())) return rc;
   hipStream_t st = (hipStream_t)stream;
   int pend = 0;
-  if ((rc = run_decoder(&c, w->layers, w->embed, w->embed, ctx, batch, block, 1, p, ws, st, &pend))) return rc;
+  if ((rc = run_decoder(&c, w->layers, w->embed, w->embed, ctx, batch, block, 1, p, ws, st, &pend, feat_layers,
+                        n_feat, hidden)))
+    return rc;
   const int H = c.hidden, M = p.M;
   {
     Phase ph("final_norm", st);

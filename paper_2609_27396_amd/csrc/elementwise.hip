@@ -303,6 +303,25 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
     if (lane + 64 * q < hd) st_f(Vc + (kvb * hd + lane + 64 * q) * cap + pos, v[q]);
 }
 
+// Hidden state of every row after a layer: bf16(X + the S pending split-K planes), written
+// to out[m * n_out + j] (rows of H entries), 4 entries per thread.
+__global__ __launch_bounds__(256) void emit_hidden(int H, const float* X, const float* P, int S, int64_t pstride,
+                                                   bf16_t* out, int n_out, int j) {
+  const int m = blockIdx.y;
+  const int i = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= H) return;
+  float4 v = *(const float4*)(X + (int64_t)m * H + i);
+  for (int s = 0; s < S; ++s) {
+    const float4 q = *(const float4*)(P + s * pstride + (int64_t)m * H + i);
+    v.x += q.x;
+    v.y += q.y;
+    v.z += q.z;
+    v.w += q.w;
+  }
+  bf16_t* o = out + ((int64_t)m * n_out + j) * H + i;
+  *(uint2*)o = make_uint2(f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16), f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+}
+
 __global__ void ctx_len_update_kernel(int B, int n_max, int cap, const int* n_new, int* ctx_len, int* status) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
@@ -439,6 +458,15 @@ hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv
     hipLaunchKernelGGL(kv_store<float>, grid, dim3(256), 0, st, CH, c0, n_max, n_kv, hd, qk_norm, eps,
                        rope, KV, S, pstride, kn, n_new, ctx_len, cap, (float*)Kc, (float*)Vc,
                        (int64_t)layer_elems);
+  return hipGetLastError();
+}
+
+hipError_t launch_emit_hidden(int rows, int H, const float* X, const float* P, int S, int64_t pstride, void* out,
+                              int n_out, int j, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (H % 4 || S < 0 || S > kMaxPlanes || j < 0 || j >= n_out) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(emit_hidden, dim3((H / 4 + 255) / 256, rows), dim3(256), 0, st, H, X, P, S, pstride,
+                     (bf16_t*)out, n_out, j);
   return hipGetLastError();
 }
 

@@ -25,8 +25,8 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_verify_greedy", "dpara_select_and_head", "dpara_branch_candidates_bytes",
            "dpara_branch_candidates", "dpara_select_and_head_cand", "dpara_clear_status",
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
-           "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_fuse_workspace_bytes",
-           "dpara_fuse_features")
+           "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_target_forward_hidden",
+           "dpara_fuse_workspace_bytes", "dpara_fuse_features")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -101,6 +101,8 @@ def lib():
         L.dpara_target_workspace_bytes.restype = SZ
         L.dpara_target_forward.argtypes = [P(DparaConfig), P(DparaTargetWeights), P(DparaCtx), I32, VP, VP, I32,
                                            VP, SZ, VP]
+        L.dpara_target_forward_hidden.argtypes = [P(DparaConfig), P(DparaTargetWeights), P(DparaCtx), I32, VP, VP,
+                                                  I32, P(I32), I32, VP, VP, SZ, VP]
         L.dpara_fuse_workspace_bytes.argtypes = [P(DparaConfig), I32, I32]
         L.dpara_fuse_workspace_bytes.restype = SZ
         L.dpara_fuse_features.argtypes = [P(DparaConfig), P(DparaFusionWeights), I32, VP, VP, VP, SZ, VP]
@@ -111,7 +113,8 @@ def lib():
         for name in ("dpara_ctx_append", "dpara_backbone_all_boundaries", "dpara_verify_greedy",
                      "dpara_select_and_head", "dpara_branch_candidates", "dpara_select_and_head_cand",
                      "dpara_clear_status", "dpara_profile_enable",
-                     "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features"):
+                     "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features",
+                     "dpara_target_forward_hidden"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -414,6 +417,18 @@ def fuse_features(f: DeviceFusion, hidden, feats, ws, stream=None):
     of at least dpara_fuse_workspace_bytes bytes."""
     n = int(hidden.shape[0])
     dpara_fuse_features(f.cfg, f.w, n, _ptr(hidden), _ptr(feats), _ptr(ws), int(ws.numel()), _stream(stream))
+
+
+def target_forward_hidden(t: DeviceTarget, ctx: DeviceContext, block, logits, feat_layers, hidden, ws: Workspace,
+                          stream=None):
+    """target_forward that also writes hidden [B, gamma+1, n_feat, H] (bf16): the block rows'
+    residual stream after each layer of feat_layers."""
+    import torch
+    ldt = DPARA_BF16 if logits.dtype == torch.bfloat16 else DPARA_F32
+    fl = (ctypes.c_int32 * len(feat_layers))(*[int(x) for x in feat_layers])
+    _check(lib().dpara_target_forward_hidden(_ref(t.cfg), _ref(t.w), _ref(ctx.c), int(block.shape[0]), _ptr(block),
+                                             _ptr(logits), ldt, fl, len(feat_layers), _ptr(hidden), ws.ptr,
+                                             ws.nbytes, _stream(stream)))
 
 
 def target_forward(t: DeviceTarget, ctx: DeviceContext, block, logits, ws: Workspace, stream=None):

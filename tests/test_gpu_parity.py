@@ -418,6 +418,19 @@ def test_target_forward_parity():
     assert d.max() <= TOL["bf16"]
     # bf16 logits are the float32 logits rounded once
     np.testing.assert_allclose(lb.float().cpu().numpy(), lf.cpu().numpy(), rtol=2 ** -8, atol=0)
+    # emitting hidden states leaves the logits bit for bit as they were; the hidden states
+    # are the oracle's residual stream after those layers, within the bf16 bar
+    fl = [1, 0]
+    hid = torch.empty((len(ctx_lens), s.gamma + 1, len(fl), s.hidden), dtype=torch.bfloat16, device="cuda")
+    lh = torch.empty_like(lf)
+    D.target_forward_hidden(t, ctx, blk, lh, fl, hid, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(lh, lf)
+    for b in range(len(ctx_lens)):
+        _, th = O.target_forward(s, w, [k[l][b] for l in range(s.n_layers)], [v[l][b] for l in range(s.n_layers)],
+                                 block[b], "bf16", fl)
+        got = hid[b].float().cpu().numpy()
+        assert np.all(np.abs(got - th) <= 2.0 ** -8 * np.abs(th) + TOL["bf16"]), b
 
 
 def test_backbone_and_target_on_concurrent_streams():
@@ -562,3 +575,130 @@ def test_fuse_features_parity(case):
             _say("fusion mismatch", n, tuple(i), float(got[tuple(i)]), float(ref[tuple(i)]))
         assert not bad.any(), (n, int(bad.sum()))
     _say(case, "fusion: worst relative |gpu - oracle|", worst)
+
+
+# ----------------------------------------------------------------------------- Algorithm 1 iterated
+LOOP_DRAFTER = synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=512,
+                                  vocab=3001, gamma=5, ar_rank=64, qk_norm=True, dtype="bf16")
+LOOP_TARGET = synth.DrafterShape(n_layers=4, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=512,
+                                 vocab=3001, gamma=5, ar_rank=64, qk_norm=True, dtype="bf16")
+FEAT_LAYERS = [0, 1, 3]
+LOOP_PLANT = [0, 3, 5]   # leading drafts of each round's block replaced by the target's own greedy chain
+
+
+def _greedy_chain(st_, wt, tk, tv, b, t0, k):
+    """t_0 followed by k tokens of the oracle target's greedy continuation (causal, so the
+    block's verdict accepts at least those k drafts)."""
+    blk = [int(t0)]
+    for _ in range(k):
+        lg = O.target_forward(st_, wt, [tk[l][b] for l in range(st_.n_layers)],
+                              [tv[l][b] for l in range(st_.n_layers)], np.array(blk, np.int32), "bf16")
+        blk.append(int(np.argmax(lg[-1])))
+    return blk
+
+
+def test_iterated_rounds_with_fused_target_features():
+    """Algorithm 1 iterated over three rounds on random weights.  Each round the target
+    forwards the block and emits its hidden states after layers 0, 1 and 3; greedy verify;
+    the drafter's all-boundary backbone and select + head; the hidden states of the block are
+    fused and the rows of t_0..t_r are appended to the drafter's cache (C <- [C, C_new]).
+    The loop is driven by the oracle: every round's block is the oracle's next spine (with
+    a planted number of leading drafts replaced by the target's greedy chain, so the accepted
+    length varies from 0 to gamma) and the append count is the oracle's r + 1; the GPU's
+    hidden states, logits, verdict, reps, drafts and fused rows are checked against the
+    oracle's, wherever the oracle's argmax margins make them unique.  The oracle's context
+    grows by its own fused rows, the GPU's by the GPU's.  The target's own cache stays fixed."""
+    from paper_2609_27396_amd import dpara as D
+    from paper_2609_27396_amd.harness import upload_cache
+    sd, st_ = LOOP_DRAFTER, LOOP_TARGET
+    ctx_lens, B, g, H = [30, 90], 2, LOOP_DRAFTER.gamma, LOOP_DRAFTER.hidden
+    nf = len(FEAT_LAYERS)
+    wd = synth.make_weights(sd, seed=31, gain_jitter=0.1, ar_e_std=1.0)
+    wt = synth.make_target_weights(st_, seed=32, gain_jitter=0.1)
+    wf = synth.make_fusion_weights(sd, n_feat=nf, seed=33, gain_jitter=0.1)
+    wl = synth.Workload("loop", sd, batch=B, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=34)
+    ri = synth.make_round(wl, ctx_lens=ctx_lens)
+    dr = _harness()(sd, wd, ri, ctx_cap=256)
+    tk, tv = synth.make_target_cache(st_, ctx_lens, seed=35)
+    t = D.DeviceTarget(st_, wt)
+    tctx = D.DeviceContext(st_, B, 256)
+    upload_cache(tctx, tk, tv, ctx_lens, torch.bfloat16)
+    tws = D.Workspace(t.cfg, B, 256, target=True)
+    fus = D.DeviceFusion(sd, wf, nf)
+    fws = torch.empty(D.dpara_fuse_workspace_bytes(fus.cfg, B * (g + 1), nf), dtype=torch.uint8, device="cuda")
+    hid = torch.empty((B, g + 1, nf, H), dtype=torch.bfloat16, device="cuda")
+    fused = torch.empty((B, g + 1, H), dtype=torch.bfloat16, device="cuda")
+    feats = [np.asarray(f, np.float32) for f in ri.ctx_feats]  # the oracle's drafter context
+    spine = ri.spine.astype(np.int32).copy()
+    worst = {"hidden": 0.0, "logits": 0.0, "reps": 0.0, "fused": 0.0}
+    compared = {"verdicts": 0, "drafts": 0, "n_new": []}
+    for rnd in range(len(LOOP_PLANT)):
+        for b in range(B):
+            chain = _greedy_chain(st_, wt, tk, tv, b, spine[b, 0], LOOP_PLANT[rnd])
+            spine[b, :len(chain)] = chain
+        _say(f"round {rnd}: planted {LOOP_PLANT[rnd]}, spine {spine.tolist()}")
+        dr.spine.copy_(torch.from_numpy(spine))
+        D.target_forward_hidden(t, tctx, dr.spine, dr.logits, FEAT_LAYERS, hid, tws)
+        dr.backbone()
+        dr.verify()
+        dr.head()
+        D.fuse_features(fus, hid.view(B * (g + 1), nf * H), fused.view(B * (g + 1), H), fws)
+        torch.cuda.synchronize()
+        assert dr.status() == 0
+        acc, bonus = dr.accept.cpu().numpy(), dr.bonus.cpu().numpy()
+        drafts = dr.drafts.cpu().numpy()
+        logits_h = dr.logits.float().cpu().numpy()
+        hid_h, fused_h = hid.float().cpu().numpy(), fused.float().cpu().numpy()
+        nxt, n_new = np.zeros_like(spine), np.zeros(B, np.int32)
+        for b in range(B):
+            tl, th = O.target_forward(st_, wt, [tk[l][b] for l in range(st_.n_layers)],
+                                      [tv[l][b] for l in range(st_.n_layers)], spine[b], "bf16", FEAT_LAYERS)
+            # the GPU's hidden states and logits are rounded once to bf16 from float32 values
+            # within the bf16 bar of the oracle's
+            e = np.abs(hid_h[b] - th)
+            worst["hidden"] = max(worst["hidden"], float(e.max()))
+            assert np.all(e <= 2.0 ** -8 * np.abs(th) + TOL["bf16"]), (rnd, b)
+            e = np.abs(logits_h[b] - tl)
+            worst["logits"] = max(worst["logits"], float(e.max()))
+            assert np.all(e <= 2.0 ** -8 * np.abs(tl) + TOL["bf16"]), (rnd, b)
+            r_ref, bonus_ref, _ = O.verify_greedy(tl, spine[b])
+            assert r_ref >= LOOP_PLANT[rnd]
+            if min(O.argmax_margin(tl[j])[1] for j in range(r_ref + 1)) > MARGIN:
+                assert (int(acc[b]), int(bonus[b])) == (r_ref, bonus_ref), (rnd, b)
+                compared["verdicts"] += 1
+            # from the second round on, the two contexts also differ by the appended rows
+            # (each side's own fused rows, up to the fused bar apart): the reps bar then adds
+            # the worst fused deviation seen so far to the single-round bar
+            ref = O.backbone_all_boundaries(sd, wd, feats[b], spine[b], "bf16")["reps"]
+            e = np.abs(dr.reps[b].cpu().numpy() - ref)
+            worst["reps"] = max(worst["reps"], float(e.max()))
+            assert e.max() <= TOL["bf16"] + worst["fused"], (rnd, b)
+            check_head(sd, wd, dr, "bf16", b)
+            hd = O.select_and_head(sd, wd, ref, r_ref, bonus_ref, "bf16")
+            if int(acc[b]) == r_ref:
+                for i in range(g):           # the oracle's own chain, up to its first near-tie
+                    if hd["margins"][i] <= MARGIN:
+                        break
+                    assert int(drafts[b, i]) == int(hd["drafts"][i]), (rnd, b, i)
+                    compared["drafts"] += 1
+            # C_new: the fused target features of t_0..t_r.  The GPU fuses its own hidden
+            # states, which already sit within the bf16 bar of the oracle's, so the fused rows
+            # are held to that end-to-end bar (the fusion kernel's own bar, on identical
+            # inputs, is checked by the fusion parity test)
+            k = r_ref + 1
+            f_ref = O.fuse_features(sd, wf, th[:k].reshape(k, nf * H), "bf16")
+            e = np.abs(fused_h[b, :k] - f_ref)
+            worst["fused"] = max(worst["fused"], float(e.max()))
+            assert np.all(e <= 2.0 ** -7 * np.abs(f_ref) + TOL["bf16"]), (rnd, b)
+            feats[b] = np.concatenate([feats[b], f_ref.astype(np.float32)])
+            nxt[b], n_new[b] = hd["next_spine"], k
+        before = dr.ctx.ctx_len[:B].clone()
+        nn = torch.from_numpy(n_new).cuda()
+        dr.append(nn, fused)
+        torch.cuda.synchronize()
+        assert torch.equal(dr.ctx.ctx_len[:B], before + nn)
+        assert dr.status() == 0
+        compared["n_new"].append(n_new.tolist())
+        spine = nxt
+    _say("iterated rounds: worst |gpu - oracle|", worst, "compared", compared)
+    assert compared["verdicts"] >= 4

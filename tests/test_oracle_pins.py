@@ -433,6 +433,13 @@ def test_target_forward_matches_hf_causal_lm_with_cache():
         vs = [cache.layers[l].values[0].permute(1, 0, 2).numpy() for l in range(s.n_layers)]
     got = O.target_forward(s, w, ks, vs, block, "exact")
     np.testing.assert_allclose(got, full[len(prefix):].numpy(), rtol=2e-5, atol=2e-5)
+    # the hidden state after layer 0 (the input of layer 1 in transformers' hidden_states)
+    with torch.no_grad():
+        hs = model(torch.from_numpy(np.concatenate([prefix, block]))[None], use_cache=False,
+                   output_hidden_states=True).hidden_states
+    logits2, hid = O.target_forward(s, w, ks, vs, block, "exact", feat_layers=[0])
+    np.testing.assert_array_equal(logits2, got)
+    np.testing.assert_allclose(hid[:, 0], hs[1][0, len(prefix):].numpy(), rtol=1e-6, atol=1e-6)
 
 
 def test_fuse_features_matches_torch_linear_rms_norm():
