@@ -134,3 +134,20 @@ def test_fusion_validation_without_gpu():
     assert "n_feat" in D.dpara_last_error()
     bad = D.DparaFusionWeights(fc=None, norm=FAKE, n_feat=3)
     assert _rc("dpara_fuse_features", R(cfg), R(bad), 17, FAKE, FAKE, ws, need, None) == D.DPARA_E_INVALID
+
+
+def test_target_hidden_validation_without_gpu():
+    """dpara_target_forward_hidden rejects a bad feature-layer list on the host, before any launch."""
+    cfg = D.make_config(synth.QWEN3_8B)
+    R = ctypes.byref
+    fl = (ctypes.c_int32 * 9)(*range(9))
+    args = lambda fl, n, hid: (R(cfg), None, None, 1, FAKE, FAKE, D.DPARA_BF16, fl, n, hid, FAKE, 1 << 20, None)
+    assert _rc("dpara_target_forward_hidden", *args(fl, 9, FAKE)) == D.DPARA_E_INVALID
+    assert "n_feat" in D.dpara_last_error()
+    assert _rc("dpara_target_forward_hidden", *args(fl, -1, FAKE)) == D.DPARA_E_INVALID
+    assert _rc("dpara_target_forward_hidden", *args(None, 3, FAKE)) == D.DPARA_E_INVALID
+    assert _rc("dpara_target_forward_hidden", *args(fl, 3, None)) == D.DPARA_E_INVALID
+    assert _rc("dpara_target_forward_hidden", *args(fl, 3, FAKE + 8)) == D.DPARA_E_INVALID
+    out = (ctypes.c_int32 * 3)(0, cfg.n_layers - 1, cfg.n_layers)
+    assert _rc("dpara_target_forward_hidden", *args(out, 3, FAKE)) == D.DPARA_E_INVALID
+    assert "feat_layers[2]" in D.dpara_last_error()
