@@ -23,10 +23,9 @@ Decoding"):
 
 The paper does not spell out the drafter layer internals; the readings used
 here (Qwen3-shaped pre-norm blocks, mask-token positions, how cached features
-enter each layer, bf16 rounding points) are listed in the design doc and restated
-at each function.  Parity unpinned: agreement with a trained DSpark/M-DFlash
-checkpoint (none is available); everything else is pinned by tests under
-``tests/test_oracle_*.py``.
+enter each layer, bf16 rounding points) are restated at each function.
+Parity unpinned: agreement with a trained DSpark/M-DFlash checkpoint (none is
+available); everything else is pinned by tests under ``tests/test_oracle_*.py``.
 
 Precision modes (``mode``):
   "exact" - no rounding anywhere (float64 throughout);

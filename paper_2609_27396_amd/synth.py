@@ -16,7 +16,8 @@ bit-identical weights.
 Shapes follow the paper's setting (Section 4.1: Qwen3-8B and Qwen3-14B
 targets, drafts of length d scored per round, batch 1..16); the acceptance
 regime (accepted length ~ Geometric, capped at the draft length) and the
-planted target logits are a reading documented in the design doc.
+planted target logits are a reading of this module: the paper reports mean
+accepted lengths but not their distribution.
 """
 from __future__ import annotations
 
