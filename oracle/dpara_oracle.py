@@ -367,6 +367,139 @@ def select_and_head(shape, w, reps, r: int, bonus: int, mode: str = "bf16", teac
 
 
 # ----------------------------------------------------------------------------
+# sampling variant (Section 2.1 rejection sampling; Algorithm 1 head with
+# y_i ~ softmax(z_i); the sampling appendix: temperature 1.0, top-p 1.0)
+# ----------------------------------------------------------------------------
+# Random numbers: Philox4x32-10, the counter-based generator of Salmon, Moraes, Dror and Shaw,
+# "Parallel random numbers: as easy as 1, 2, 3" (SC 2011).  Ten rounds; each round multiplies
+# words 0 and 2 by the two Philox multipliers, mixes the high halves with words 1 and 3 and the
+# round key, and the key advances by the two Weyl constants between rounds.
+PHILOX_M0, PHILOX_M1 = 0xD2511F53, 0xCD9E8D57
+PHILOX_W0, PHILOX_W1 = 0x9E3779B9, 0xBB67AE85
+# counter word 3 names what a number is drawn for
+TAG_HEAD, TAG_ACCEPT, TAG_BONUS = 1, 2, 3
+_M32 = 0xFFFFFFFF
+
+
+def philox4x32_10(ctr, key):
+    """Philox4x32-10 of counter (c0, c1, c2, c3) under key (k0, k1); every counter word may be
+    an integer array (broadcast).  Returns the four output words as uint64 arrays."""
+    c0, c1, c2, c3 = (np.asarray(c, np.uint64) & np.uint64(_M32) for c in ctr)
+    k0, k1 = int(key[0]) & _M32, int(key[1]) & _M32
+    for _ in range(10):
+        p0 = np.uint64(PHILOX_M0) * c0          # < 2^64: exact in uint64
+        p1 = np.uint64(PHILOX_M1) * c2
+        c0, c1, c2, c3 = ((p1 >> np.uint64(32)) ^ c1 ^ np.uint64(k0), p1 & np.uint64(_M32),
+                          (p0 >> np.uint64(32)) ^ c3 ^ np.uint64(k1), p0 & np.uint64(_M32))
+        k0, k1 = (k0 + PHILOX_W0) & _M32, (k1 + PHILOX_W1) & _M32
+    return c0, c1, c2, c3
+
+
+def u01(word):
+    """A 32-bit word to a uniform in (0, 1): its top 23 bits k give (2k + 1) / 2^24, exact in
+    float32 and float64 and never 0 or 1."""
+    k = np.asarray(word, np.uint64) >> np.uint64(9)
+    return (k.astype(np.float64) * 2.0 + 1.0) * 2.0 ** -24
+
+
+def uniforms(seed: int, tag: int, b: int, i: int, v):
+    """U(seed; tag, request b, position i, index v): word 0 of Philox4x32-10 with counter
+    (v, i, b, tag) and key (seed mod 2^32, seed div 2^32)."""
+    key = (int(seed) & _M32, (int(seed) >> 32) & _M32)
+    w0 = philox4x32_10((np.asarray(v), int(i), int(b), int(tag)), key)[0]
+    return u01(w0)
+
+
+def gumbel(u):
+    """Standard Gumbel variate from a uniform: -log(-log u)."""
+    return -np.log(-np.log(u))
+
+
+def gumbel_argmax(scores, seed: int, tag: int, b: int, i: int):
+    """A draw from softmax(scores) by the Gumbel-max rule: argmax_v scores[v] + G_v, G_v the
+    Gumbel transform of U(seed; tag, b, i, v).  Entries at -inf never win.  Returns (index,
+    top1 - top2 of the perturbed scores)."""
+    s = np.asarray(scores, np.float64)
+    keys = s + gumbel(uniforms(seed, tag, b, i, np.arange(s.size)))
+    return argmax_margin(keys)
+
+
+def head_step_sampled(w, ell_i, y_prev: int, temperature: float, seed: int, b: int, i: int,
+                      mode: str = "bf16"):
+    """Sampled head step: s_i = z_i / T with z_i = l_i + W E(y_{i-1}), then y_i ~ softmax(s_i)
+    drawn with the head's random numbers (tag TAG_HEAD, request b, step i).  Returns (y_i,
+    margin of the perturbed scores, s_i)."""
+    _, _, z = head_step(w, ell_i, y_prev, mode)
+    s = Rounding(mode).r32(z / float(temperature))
+    y, m = gumbel_argmax(s, seed, TAG_HEAD, b, i)
+    return y, m, s
+
+
+def select_and_head_sampled(shape, w, reps, r: int, bonus: int, temperature: float, seed: int, b: int,
+                            mode: str = "bf16", teacher=None):
+    """select_and_head with y_i ~ softmax(z_i / T) (Algorithm 1's head loop as printed).
+    Returns dict(drafts, margins, scores [gamma, V] (the tempered draft scores s_i the next
+    round's verification reads), next_spine)."""
+    g = shape.gamma
+    ell = base_logits(w, _f64(reps[r]), mode)
+    drafts = np.zeros(g, np.int64)
+    margins = np.zeros(g, np.float64)
+    scores = np.zeros((g, ell.shape[1]), np.float64)
+    y_prev = int(bonus)
+    for i in range(1, g + 1):
+        y, m, s = head_step_sampled(w, ell[i - 1], y_prev, temperature, seed, b, i, mode)
+        drafts[i - 1], margins[i - 1], scores[i - 1] = y, m, s
+        y_prev = y if teacher is None else int(teacher[i - 1])
+    return {"drafts": drafts, "margins": margins, "scores": scores,
+            "next_spine": np.concatenate([[int(bonus)], drafts])}
+
+
+def log_softmax(x):
+    x = np.asarray(x, np.float64)
+    m = np.max(x)
+    return x - (m + np.log(np.sum(np.exp(x - m))))
+
+
+def verify_sampled(target_logits, draft_scores, spine, temperature: float, seed: int, b: int):
+    """Speculative-sampling verification of one request's block (Section 2.1; the sampling
+    appendix's standard rejection rule).
+
+    target_logits [gamma+1, V]: row j scores the token after t_j; p_j = softmax(row / T).
+    draft_scores [gamma, V]: the tempered scores s the drafts were drawn from (draft t_i was
+    drawn from q_i = softmax(s[i-1])).  Draft t_i (i = 1..gamma) is accepted while
+    U(seed; TAG_ACCEPT, b, i, 0) < p_{i-1}(t_i) / q_i(t_i); r = number of leading accepted
+    drafts.  The bonus is drawn (tag TAG_BONUS, position 0) from the residual
+    max(0, p_r - q_{r+1}) renormalised when r < gamma (from p_r itself should rounding leave
+    the residual empty), and from p_gamma after full acceptance.  The test runs in log space:
+    log p - log q - log u > 0.  Returns (r, bonus, dict(accept_margins, bonus_margin))."""
+    L = np.asarray(target_logits, np.float64)
+    S = np.asarray(draft_scores, np.float64)
+    gam = L.shape[0] - 1
+    logp = np.stack([log_softmax(L[j] / float(temperature)) for j in range(gam + 1)])
+    logq = np.stack([log_softmax(S[j]) for j in range(gam)])
+    r, am = 0, []
+    for i in range(1, gam + 1):
+        t = int(spine[i])
+        u = float(uniforms(seed, TAG_ACCEPT, b, i, 0))
+        a = logp[i - 1][t] - logq[i - 1][t] - np.log(u)
+        am.append(a)
+        if a > 0:
+            r += 1
+        else:
+            break
+    if r < gam:
+        d = np.exp(logp[r]) - np.exp(logq[r])
+        with np.errstate(divide="ignore"):
+            keys = np.where(d > 0, np.log(np.where(d > 0, d, 1.0)), -np.inf)
+        if not np.isfinite(keys).any():
+            keys = logp[r]
+    else:
+        keys = logp[gam]
+    bonus, bm = gumbel_argmax(keys, seed, TAG_BONUS, b, 0)
+    return r, bonus, {"accept_margins": np.array(am), "bonus_margin": bm}
+
+
+# ----------------------------------------------------------------------------
 # target verification forward (Algorithm 1, Verify; Section 4.3.2 colocation)
 # ----------------------------------------------------------------------------
 def target_forward(shape, w, ctx_k, ctx_v, block, mode: str = "bf16", feat_layers=None):
