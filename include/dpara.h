@@ -187,6 +187,47 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
                           float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
                           void* ws, size_t ws_bytes, void* stream);
 
+/* Sampling variant (Algorithm 1's head loop draws y_i ~ softmax(z_i); Section 2.1's
+ * distribution-preserving rejection sampling; the sampling appendix: temperature 1.0 for
+ * target and drafter, top-p 1.0).
+ *
+ * Random numbers: U(seed; tag, b, i, v) = (2k + 1) / 2^24, k = the top 23 bits of word 0 of
+ * Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011) with counter (v, i, b, tag) and key
+ * (seed mod 2^32, seed div 2^32); b is the request's index in the call's batch.  Tags: 1 head
+ * draws (i = step, v = vocabulary id), 2 acceptance tests (i = draft index, v = 0), 3 bonus
+ * draws (i = 0, v = vocabulary id).  A draw from softmax(x) is argmax_v x_v - log(-log U_v)
+ * (Gumbel-max).  Callers pass a fresh seed per round; reusing one repeats the draws.
+ *
+ * dpara_select_and_head_sampled: dpara_select_and_head with y_i drawn from softmax(z_i / T)
+ * (tag 1, step i) instead of argmax z_i; margins are top1 - top2 of z_i / T plus the noise.
+ * draft_scores: [batch, gamma, vocab] float32 (device, may be NULL): s_i = z_i / T, the
+ * tempered scores each draft was drawn from (the input of dpara_verify_sampled in the next
+ * round).  The bound-pruned steps do not apply; the full head runs (same launch rules).
+ *
+ * dpara_verify_sampled: speculative-sampling verification of the block t_0..t_gamma.
+ * target_logits: [batch, gamma+1, vocab] (device, logits_dtype DPARA_F32 or DPARA_BF16,
+ *                finite), row j scores the token after t_j; p_j = softmax(row j / T).
+ * draft_scores:  [batch, gamma, vocab] float32 (device, finite): row i-1 holds the scores s
+ *                draft t_i was drawn from; q_i = softmax(s).
+ * Draft t_i (i = 1..gamma) is accepted while U(seed; 2, b, i, 0) < p_{i-1}(t_i) / q_i(t_i)
+ * (tested in log space); accept_len[b] = r = the number of leading accepted drafts.  The
+ * bonus is drawn (tag 3) from max(0, p_r - q_{r+1}) renormalised when r < gamma (from p_r
+ * should rounding leave that empty) and from p_gamma when every draft is accepted.
+ * Outputs (device, int32): accept_len [batch], bonus [batch].  Out-of-range draft ids set
+ * DPARA_STATUS_TOKEN_RANGE and are never accepted.  ws: a workspace of
+ * dpara_workspace_bytes(cfg, batch, ctx_cap) bytes; the call uses a region of its own, so it
+ * may run concurrently with dpara_backbone_all_boundaries on the same workspace.
+ * Both calls: temperature must be positive and finite (else DPARA_E_INVALID). */
+int dpara_select_and_head_sampled(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
+                                  const float* reps, const int32_t* accept_len, const int32_t* bonus,
+                                  float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
+                                  float temperature, uint64_t seed, float* draft_scores, void* ws,
+                                  size_t ws_bytes, void* stream);
+int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* target_logits,
+                         int32_t logits_dtype, const float* draft_scores, const int32_t* spine,
+                         float temperature, uint64_t seed, int32_t* accept_len, int32_t* bonus,
+                         void* ws, size_t ws_bytes, void* stream);
+
 /* Head variant with every branch's base logits computed off the serial path (Algorithm 1
  * computes the base logits during Precompute).
  * dpara_branch_candidates, issued after the backbone (for instance on its stream, where it

@@ -1,5 +1,7 @@
 // Persistent AR head (head equation of Section 3.2, Algorithm 1's head loop) for bf16
-// drafters: one launch runs all gamma serial steps.
+// drafters: one launch runs all gamma serial steps.  The sampling variant draws
+// y_i ~ softmax(z_i / T) by ranking z_i / T plus Gumbel noise from the counter-based
+// generator (request, step and vocabulary index in the counter) instead of z_i.
 //
 // Each step computes z_i = l_i + W E(y_{i-1}) over the vocabulary and y_i = argmax z_i.
 // Reading the V x r matrix W from HBM at every step dominates the per-step kernels; here
@@ -157,13 +159,15 @@ __device__ __forceinline__ void top2_join(Top2& t, const Top2& o) {
   t.k1 = better ? o.k1 : t.k1;
 }
 
-template <int NKB, int NRB, int NW>
+// SAMPLE: the sampling variant ranks s + Gumbel noise, s = z * inv_t (and stores s when asked).
+template <int NKB, int NRB, int NW, bool SAMPLE>
 __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, int B, const float* logits,
                                                                      const bf16_t* E, const bf16_t* W,
                                                                      const int* bonus, int* drafts,
                                                                      int* next_spine, float* margins,
                                                                      uint64_t* part, int* status,
-                                                                     uint32_t spin_limit, const int* only_if) {
+                                                                     uint32_t spin_limit, const int* only_if,
+                                                                     Sampling smp) {
   // Every workgroup reads the same flag, so all of them leave together.
   if (only_if && *only_if == 0) return;
   constexpr int RANK = NKB * 32;
@@ -174,6 +178,7 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
   static_assert((kArpMaxB * LCH) % (64 * NW) == 0, "logit staging must split into whole DMA rounds");
   __shared__ __attribute__((aligned(16))) bf16_t es[kArpMaxB * ESTRIDE];
   __shared__ __attribute__((aligned(16))) float lgs[kArpMaxB * ROWS_WG];  // this step's logits of the slice
+  __shared__ float gs[SAMPLE ? kArpMaxB * ROWS_WG : 1];                    // this step's Gumbel noise of the slice
   __shared__ int ys[kArpMaxB];
   __shared__ float ms[kArpMaxB];
   __shared__ uint64_t rk[NW][kArpMaxB];
@@ -216,6 +221,14 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
       const int v = min(v0 + 4 * (c % LCH), V - 4);
       __builtin_amdgcn_global_load_lds((const void*)(logits + ((int64_t)b * gamma + s - 1) * V + v),
                                        (lds_void_t*)(lgs + 4 * (c0 + wave * 64)), 16, 0, 0);
+    }
+    if constexpr (SAMPLE) {
+      // the noise does not depend on y: drawn here, it overlaps the wait for the partials
+#pragma unroll 1
+      for (int e = tid; e < B * ROWS_WG; e += 64 * NW) {
+        const int v = v0 + e % ROWS_WG;
+        gs[e] = v < V ? rng_gumbel(smp.k0, smp.k1, kTagHead, e / ROWS_WG, s, v) : 0.f;
+      }
     }
     if (s > 1) {
       const bool okp = arp_poll(part, s - 1, B, G, V, spin_limit, ys, ms, &rk[0][0], &rv[0][0]);
@@ -264,7 +277,14 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
         if (i >= IMAX) break;
         const int b = 4 * lg + i;
         const bool valid = v < V && b < B;
-        const float z = lgs[min(b, B - 1) * ROWS_WG + vl] + acc[i];
+        float z = lgs[min(b, B - 1) * ROWS_WG + vl] + acc[i];
+        if constexpr (SAMPLE) {
+          if (valid) {
+            z *= smp.inv_t;
+            lgs[b * ROWS_WG + vl] = z;  // read once above: now the score, copied out below
+            z += gs[b * ROWS_WG + vl];
+          }
+        }
         top2_add(t2[i], valid ? arp_key(z, (uint32_t)v) : 0ull, valid ? z : -INFINITY);
       }
     }
@@ -294,6 +314,15 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
       store_dev(e + 1, ((uint64_t)__float_as_uint(V2) << 32) | (uint32_t)s);
       store_dev(e, K | ((uint32_t)s & ((1u << kArpTagBits) - 1)));
     }
+    if constexpr (SAMPLE) {
+      if (smp.scores) {  // the slice's scores z / T, row by row (the barrier above ordered them)
+        for (int e = tid; e < B * ROWS_WG; e += 64 * NW) {
+          const int v = v0 + e % ROWS_WG;
+          if (v < V) smp.scores[((int64_t)(e / ROWS_WG) * gamma + s - 1) * V + v] = lgs[e];
+        }
+        __syncthreads();  // before the next step's logit DMA overwrites lgs
+      }
+    }
   }
   // y_gamma: only workgroup 0 needs it
   if (wg != 0) return;
@@ -310,10 +339,10 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
   }
 }
 
-template <int NKB, int NRB, int NW>
+template <int NKB, int NRB, int NW, bool SAMPLE>
 hipError_t arp_launch(int B, int gamma, int V, const float* logits, const void* E, const void* W, const int* bonus,
                       int* drafts, int* next_spine, float* margins, uint64_t* part, int part_grid, int* status,
-                      const int* only_if, hipStream_t st) {
+                      const int* only_if, hipStream_t st, const Sampling& smp) {
   constexpr int ROWS_WG = NW * 16 * NRB;
   const int G = (V + ROWS_WG - 1) / ROWS_WG;
   if (G > part_grid || G > kArpMaxGrid) return hipErrorNotSupported;
@@ -321,14 +350,14 @@ hipError_t arp_launch(int B, int gamma, int V, const float* logits, const void* 
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e == hipSuccess)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ar_head_persistent<NKB, NRB, NW>, 64 * NW, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ar_head_persistent<NKB, NRB, NW, SAMPLE>, 64 * NW, 0);
   if (e != hipSuccess) return e;
   if (G > per_cu * cus) return hipErrorNotSupported;  // not co-resident: the caller falls back
   const uint32_t spin_limit = 1u << 17;  // polls of ~2 us: ~0.3 s before a workgroup gives up
   Phase ph("ar_step", st);
-  hipLaunchKernelGGL((ar_head_persistent<NKB, NRB, NW>), dim3(G), dim3(64 * NW), 0, st, gamma, V, B, logits,
+  hipLaunchKernelGGL((ar_head_persistent<NKB, NRB, NW, SAMPLE>), dim3(G), dim3(64 * NW), 0, st, gamma, V, B, logits,
                      (const bf16_t*)E, (const bf16_t*)W, bonus, drafts, next_spine, margins, part, status,
-                     spin_limit, only_if);
+                     spin_limit, only_if, smp);
   return hipGetLastError();
 }
 
@@ -345,16 +374,23 @@ int ar_persistent_grid(int rank, int V) {
 
 hipError_t launch_ar_head_persistent(int B, int gamma, int V, int rank, const float* logits, const void* E,
                                      const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                                     uint64_t* part, int part_grid, int* status, const int* only_if, hipStream_t st) {
+                                     uint64_t* part, int part_grid, int* status, const int* only_if, hipStream_t st,
+                                     const Sampling& smp) {
   if (B < 1 || B > kArpMaxB || V > (int)kArpIdxMask + 1 || V % 4 || V < 4 || gamma < 1 ||
       gamma >= (1 << kArpTagBits) || (uintptr_t)logits % 16)
     return hipErrorNotSupported;
+#define DPARA_ARP(NKB)                                                                                         \
+  (smp.on ? arp_launch<NKB, 5, 8, true>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part,     \
+                                        part_grid, status, only_if, st, smp)                                     \
+          : arp_launch<NKB, 5, 8, false>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part,    \
+                                         part_grid, status, only_if, st, smp))
   switch (rank) {
-    case 64: return arp_launch<2, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, only_if, st);
-    case 128: return arp_launch<4, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, only_if, st);
-    case 256: return arp_launch<8, 5, 8>(B, gamma, V, logits, E, W, bonus, drafts, next_spine, margins, part, part_grid, status, only_if, st);
+    case 64: return DPARA_ARP(2);
+    case 128: return DPARA_ARP(4);
+    case 256: return DPARA_ARP(8);
     default: return hipErrorNotSupported;
   }
+#undef DPARA_ARP
 }
 
 }  // namespace dpara

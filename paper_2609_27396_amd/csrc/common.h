@@ -182,6 +182,37 @@ struct Top3 {
 // Status word (int32 at byte offset 0 of the workspace).
 __device__ __forceinline__ void raise_status(int* status, int bit) { atomicOr(status, bit); }
 
+// Counter-based random numbers for the sampling variant: word 0 of Philox4x32-10 (Salmon,
+// Moraes, Dror and Shaw, SC 2011) of counter (c0, c1, c2, c3) under key (k0, k1).  Each round
+// multiplies words 0 and 2 by the two Philox multipliers, xors the high halves into words 1
+// and 3 with the round key, and the key advances by the two Weyl constants.
+__device__ __forceinline__ uint32_t philox_word0(uint32_t k0, uint32_t k1, uint32_t c0, uint32_t c1, uint32_t c2,
+                                                 uint32_t c3) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t h0 = __umulhi(0xD2511F53u, c0), l0 = 0xD2511F53u * c0;
+    const uint32_t h2 = __umulhi(0xCD9E8D57u, c2), l2 = 0xCD9E8D57u * c2;
+    c0 = h2 ^ c1 ^ k0;
+    c1 = l2;
+    c2 = h0 ^ c3 ^ k1;
+    c3 = l0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c0;
+}
+// Random-number purposes (counter word 3).
+constexpr uint32_t kTagHead = 1, kTagAccept = 2, kTagBonus = 3;
+// Uniform in (0, 1) from the top 23 bits k of a word: (2k + 1) / 2^24, exact in float32.
+__device__ __forceinline__ float u01_of(uint32_t w) { return (float)((w >> 9) * 2u + 1u) * 0x1p-24f; }
+// U(key; tag, request b, position i, index v) and its Gumbel transform -log(-log u).
+__device__ __forceinline__ float rng_uniform(uint32_t k0, uint32_t k1, uint32_t tag, int b, int i, int v) {
+  return u01_of(philox_word0(k0, k1, (uint32_t)v, (uint32_t)i, (uint32_t)b, tag));
+}
+__device__ __forceinline__ float rng_gumbel(uint32_t k0, uint32_t k1, uint32_t tag, int b, int i, int v) {
+  return -logf(-logf(rng_uniform(k0, k1, tag, b, i, v)));
+}
+
 // RoPE angle for position `pos`, rotation pair p of head_dim hd, in float64 so that large
 // positions keep full float32 accuracy in cos/sin.
 __device__ __forceinline__ void rope_cs(int pos, int p, int hd, double base, float* c, float* s) {

@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <cmath>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -116,7 +117,7 @@ struct Plan {
   bool afrag;              // normed activations in MFMA fragment order (QKV and gate/up GEMMs)
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
-      hflag, F, KV32, rope_app, csplit, cpart;
+      hflag, F, KV32, rope_app, csplit, cpart, spart;
   int ar_grid;  // persistent AR head grid (0: step kernels only)
   size_t total;
 };
@@ -199,6 +200,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   const size_t crows = (size_t)B * (c->gamma + 1) * c->gamma;
   p.csplit = take(c->dtype == DPARA_BF16 ? 2 * crows * H * 2 : 0);
   p.cpart = take(c->dtype == DPARA_BF16 ? head_cand_part_bytes(B, c->gamma, c->vocab) : 0);
+  p.spart = take(verify_sampled_bytes(B, c->gamma, p.v_chunks));  // sampled verify: lse partials, bonus keys
   p.total = off;
   return p;
 }
@@ -664,9 +666,13 @@ int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* ta
   return DPARA_OK;
 }
 
-int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch, const float* reps,
-                          const int32_t* accept_len, const int32_t* bonus, float* gathered, int32_t* drafts,
-                          int32_t* next_spine, float* margins, void* ws, size_t ws_bytes, void* stream) {
+namespace {
+// Gather, LM head, then the AR head: greedy (smp == nullptr: bound-pruned steps first, the
+// full head only where a step is not proven) or sampled (the full head with Gumbel noise).
+int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch, const float* reps,
+                         const int32_t* accept_len, const int32_t* bonus, float* gathered, int32_t* drafts,
+                         int32_t* next_spine, float* margins, void* ws, size_t ws_bytes, void* stream,
+                         const Sampling* smp) {
   int rc = check_cfg(cfg);
   if (rc) return rc;
   if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
@@ -706,6 +712,13 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
     Phase ph("lm_head", st);
     HIP_TRY(launch_gemm(bf ? A_BF16_DUAL : A_F32, EPI_STORE_F32, lm, st), "lm head gemm");
   }
+  if (smp) {
+    HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
+                           drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
+                           p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status, nullptr, st, *smp),
+            "sampled ar head");
+    return DPARA_OK;
+  }
   // Exact bound-pruned steps first; the full head then runs only if some step could not be
   // decided from the candidates (its kernels return at once otherwise).
   int* hflag = at<int>(ws, p.hflag);
@@ -718,6 +731,64 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
                          p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status,
                          pe == hipSuccess ? hflag : nullptr, st),
           "ar head");
+  return DPARA_OK;
+}
+
+// Temperature and seed of the sampling variant: the generator's key is the seed's two
+// 32-bit halves.
+int make_sampling(float temperature, uint64_t seed, float* scores, Sampling* smp) {
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(1.0f / temperature))
+    return fail(DPARA_E_INVALID, "temperature must be positive and finite, got %g", (double)temperature);
+  smp->on = 1;
+  smp->inv_t = 1.0f / temperature;
+  smp->k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  smp->k1 = (uint32_t)(seed >> 32);
+  smp->scores = scores;
+  return DPARA_OK;
+}
+}  // namespace
+
+int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch, const float* reps,
+                          const int32_t* accept_len, const int32_t* bonus, float* gathered, int32_t* drafts,
+                          int32_t* next_spine, float* margins, void* ws, size_t ws_bytes, void* stream) {
+  return select_and_head_impl(cfg, w, batch, reps, accept_len, bonus, gathered, drafts, next_spine, margins, ws,
+                              ws_bytes, stream, nullptr);
+}
+
+int dpara_select_and_head_sampled(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
+                                  const float* reps, const int32_t* accept_len, const int32_t* bonus,
+                                  float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
+                                  float temperature, uint64_t seed, float* draft_scores, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  Sampling smp{};
+  const int rc = make_sampling(temperature, seed, draft_scores, &smp);
+  if (rc) return rc;
+  return select_and_head_impl(cfg, w, batch, reps, accept_len, bonus, gathered, drafts, next_spine, margins, ws,
+                              ws_bytes, stream, &smp);
+}
+
+int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* target_logits, int32_t logits_dtype,
+                         const float* draft_scores, const int32_t* spine, float temperature, uint64_t seed,
+                         int32_t* accept_len, int32_t* bonus, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if (logits_dtype != DPARA_F32 && logits_dtype != DPARA_BF16)
+    return fail(DPARA_E_UNSUPPORTED, "logits_dtype must be F32 or BF16");
+  if (!target_logits || !draft_scores || !spine || !accept_len || !bonus)
+    return fail(DPARA_E_INVALID, "target_logits, draft_scores, spine, accept_len and bonus must be non-NULL");
+  Sampling smp{};
+  if ((rc = make_sampling(temperature, seed, nullptr, &smp))) return rc;
+  const Plan p = make_plan(cfg, batch, 64);
+  if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
+  const size_t need = p.spart + verify_sampled_bytes(batch, cfg->gamma, p.v_chunks);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if ((rc = check_device())) return rc;
+  HIP_TRY(launch_verify_sampled(logits_dtype, batch, cfg->gamma, cfg->vocab, target_logits, draft_scores, spine,
+                                smp.inv_t, smp.k0, smp.k1, accept_len, bonus, at<void>(ws, p.spart), p.v_chunks,
+                                p.v_chunk, at<int>(ws, 0), (hipStream_t)stream),
+          "sampled verify");
   return DPARA_OK;
 }
 

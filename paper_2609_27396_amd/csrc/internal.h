@@ -134,9 +134,27 @@ hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, in
 hipError_t launch_clear_status(int* status, hipStream_t st);
 
 // ---------------------------------------------------------------- verify / head
+// Sampled head (sampling variant): with on != 0 every head step scores s = z * inv_t, writes
+// s to scores[b][step-1][v] when scores is non-NULL, and ranks s + Gumbel(key; head tag, b,
+// step, v) instead of z; margins are then those of the perturbed scores.
+struct Sampling {
+  int on;
+  float inv_t;
+  uint32_t k0, k1;
+  float* scores;
+};
 hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits,
                          const int* spine, int* accept_len, int* bonus, int* target_argmax,
                          uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st);
+// Speculative-sampling verification (sampling variant): per request, the logsumexp of every
+// target row (scaled by inv_t) and draft-score row in vocabulary chunks, one wave for the
+// acceptance test of each draft, then the bonus drawn by Gumbel-max from the residual
+// max(0, p_r - q_{r+1}) (from p_r if rounding leaves it empty) or, after full acceptance,
+// from p_gamma.  verify_sampled_bytes gives the scratch bytes it needs.
+size_t verify_sampled_bytes(int B, int gamma, int n_chunks);
+hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, const void* logits, const float* scores,
+                                 const int* spine, float inv_t, uint32_t k0, uint32_t k1, int* accept_len,
+                                 int* bonus, void* scratch, int n_chunks, int chunk, int* status, hipStream_t st);
 // G (fp32, optional copy G_out) and its bf16 hi/lo split planes Ghi, Glo = Ghi + M*H.
 // Also zeroes n_clear uint64 words at `clear` (the persistent AR head's step tags).
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
@@ -151,7 +169,7 @@ int ar_persistent_grid(int rank, int V);
 hipError_t launch_ar_head_persistent(int B, int gamma, int V, int rank, const float* logits, const void* E,
                                      const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                                      uint64_t* part, int part_grid, int* status, const int* only_if,
-                                     hipStream_t st);
+                                     hipStream_t st, const Sampling& smp = Sampling{});
 // bf16 with ppart (zero tags, ppart_grid = ar_persistent_grid) runs the persistent head when
 // the device allows it; otherwise gamma+1 step kernels with partials in `part`.  With a
 // non-NULL only_if, every kernel returns at once unless *only_if != 0 when it runs.
@@ -159,7 +177,7 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
                           const void* E, const void* W, const int* bonus, int* drafts,
                           int* next_spine, float* margins, uint64_t* part, int n_chunks,
                           int chunk, uint64_t* ppart, int ppart_grid, int* status, const int* only_if,
-                          hipStream_t st);
+                          hipStream_t st, const Sampling& smp = Sampling{});
 // Exact bound-pruned head (head_prune.hip): top candidates per logit row, the largest W row
 // norm, then all gamma steps over the candidates only.  Where a row or a step cannot be
 // decided exactly it sets *flag != 0 (the flag is cleared first), and the caller runs

@@ -6,6 +6,10 @@
 // gives the accepted length r = index of the first mismatch (gamma if none) and the
 // bonus g_r (Section 2.1; Algorithm 1, Verify).
 //
+// Sampling variant: the acceptance test and bonus draw of speculative sampling (Section 2.1)
+// over log-sum-exp partials of the target and draft-score rows; the head steps rank
+// z / T plus Gumbel noise.
+//
 // head: y_0 = bonus; step i computes z_i = l_i + W E(y_{i-1}) over the vocabulary in
 // chunks (8 lanes per vocabulary row, E(y_{i-1}) staged in LDS) and keeps a per-chunk
 // top-2; the next step's workgroups reduce those partials to y_i and the top1 - top2
@@ -196,7 +200,8 @@ template <typename T>
 __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int rank, const float* logits,
                                                const T* E, const T* W, const int* bonus, int* drafts,
                                                int* next_spine, float* margins, uint64_t* part,
-                                               int n_chunks, int chunk, int B, int* status, const int* only_if) {
+                                               int n_chunks, int chunk, int B, int* status, const int* only_if,
+                                               Sampling smp) {
   if (only_if && *only_if == 0) return;
   __shared__ float e[1024];
   __shared__ uint64_t rk[4];
@@ -234,7 +239,12 @@ __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int r
     d += __shfl_xor(d, 2, kWave);
     d += __shfl_xor(d, 4, kWave);
     if (j == 0) {
-      const float z = lrow[v] + d;
+      float z = lrow[v] + d;
+      if (smp.on) {
+        z *= smp.inv_t;
+        if (smp.scores) smp.scores[((int64_t)b * gamma + step - 1) * V + v] = z;
+        z += rng_gumbel(smp.k0, smp.k1, kTagHead, b, step, v);
+      }
       top2_merge(k1, v2, argmax_key(z, (uint32_t)v), -INFINITY);
     }
   }
@@ -269,7 +279,8 @@ template <typename T, int P>
 __global__ __launch_bounds__(256) void ar_step_pf(int step, int gamma, int V, int rank, const float* logits,
                                                   const T* E, const T* W, const int* bonus, int* drafts,
                                                   int* next_spine, float* margins, uint64_t* part,
-                                                  int n_chunks, int chunk, int B, int* status, const int* only_if) {
+                                                  int n_chunks, int chunk, int B, int* status, const int* only_if,
+                                                  Sampling smp) {
   if (only_if && *only_if == 0) return;
   constexpr int NR = ar_rows_per_group(P);
   __shared__ __attribute__((aligned(16))) float e[1024];
@@ -343,6 +354,11 @@ __global__ __launch_bounds__(256) void ar_step_pf(int step, int gamma, int V, in
     if (j == i) zmine = lg + d;
   }
   const int vmine = v0 + grp + 32 * j;
+  if (smp.on && j < NR && vmine < V) {
+    zmine *= smp.inv_t;
+    if (smp.scores) smp.scores[((int64_t)b * gamma + step - 1) * V + vmine] = zmine;
+    zmine += rng_gumbel(smp.k0, smp.k1, kTagHead, b, step, vmine);
+  }
   uint64_t k1 = (j < NR && vmine < V) ? argmax_key(zmine, (uint32_t)vmine) : 0;
   float v2 = -INFINITY;
 #pragma unroll
@@ -366,6 +382,189 @@ __global__ __launch_bounds__(256) void ar_step_pf(int step, int gamma, int V, in
   }
 }
 
+
+// ------------------------------------------------------------ speculative-sampling verify
+// Online (max, sum of exp(x - max)) over one row chunk; -inf sums are empty.
+__device__ __forceinline__ void ms_add(float& m, float& s, float x) {
+  if (x > m) {
+    s = s * expf(m - x) + 1.f;
+    m = x;
+  } else {
+    s += expf(x - m);
+  }
+}
+__device__ __forceinline__ void ms_merge(float& m, float& s, float om, float os) {
+  if (os == 0.f) return;
+  if (s == 0.f) {
+    m = om;
+    s = os;
+    return;
+  }
+  const float M = fmaxf(m, om);
+  s = s * expf(m - M) + os * expf(om - M);
+  m = M;
+}
+
+// Row r < n_trows: target row (times inv_t); otherwise draft-score row r - n_trows.  Every
+// workgroup writes (max, sum) of its chunk to part[row][chunk].
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void lse_partial(const T* tl, const float* sc, int V, int chunk, int n_chunks,
+                                                   int n_trows, float inv_t, float2* part) {
+  __shared__ float rm[4], rs[4];
+  const int row = blockIdx.y, c = blockIdx.x;
+  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  float m = -INFINITY, s = 0.f;
+  if (row < n_trows) {
+    const T* x = tl + (int64_t)row * V;
+    if constexpr (VEC) {
+      constexpr int EPP = 16 / sizeof(T);
+      for (int v = v0 + threadIdx.x * EPP; v < v1; v += 256 * EPP) {
+        const uint4 u = *(const uint4*)(x + v);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int q = 0; q < EPP; ++q) {
+          float f;
+          if constexpr (sizeof(T) == 2) f = __uint_as_float(q & 1 ? (w[q >> 1] & 0xFFFF0000u) : (w[q >> 1] << 16));
+          else f = __uint_as_float(w[q]);
+          if (v + q < v1) ms_add(m, s, f * inv_t);
+        }
+      }
+    } else {
+      for (int v = v0 + threadIdx.x; v < v1; v += 256) ms_add(m, s, ld_f(x + v) * inv_t);
+    }
+  } else {
+    const float* x = sc + (int64_t)(row - n_trows) * V;
+    if constexpr (VEC) {
+      for (int v = v0 + threadIdx.x * 4; v < v1; v += 1024) {
+        const float4 f = *(const float4*)(x + v);
+        ms_add(m, s, f.x);
+        if (v + 1 < v1) ms_add(m, s, f.y);
+        if (v + 2 < v1) ms_add(m, s, f.z);
+        if (v + 3 < v1) ms_add(m, s, f.w);
+      }
+    } else {
+      for (int v = v0 + threadIdx.x; v < v1; v += 256) ms_add(m, s, x[v]);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, kWave), os = __shfl_xor(s, o, kWave);
+    ms_merge(m, s, om, os);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    rm[threadIdx.x >> 6] = m;
+    rs[threadIdx.x >> 6] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 4; ++i) ms_merge(m, s, rm[i], rs[i]);
+    part[(int64_t)row * n_chunks + c] = make_float2(m, s);
+  }
+}
+
+__device__ __forceinline__ float lse_of(const float2* p, int n_chunks) {
+  float m = -INFINITY, s = 0.f;
+  for (int c = 0; c < n_chunks; ++c) ms_merge(m, s, p[c].x, p[c].y);
+  return m + logf(s);
+}
+
+// One wave per request: lane j (1..gamma) tests draft t_j against p_{j-1} (target row j-1)
+// and q_j (draft-score row j-1) in log space: accepted iff log p - log q - log u > 0.  An
+// out-of-range draft is flagged and never accepted.  info[b] = (r, lse of target row r, lse
+// of draft-score row r (the residual's q), 0).
+template <typename T>
+__global__ __launch_bounds__(64) void spec_accept(int B, int gamma, int V, int n_chunks, const float2* part,
+                                                  const T* tl, const float* sc, const int* spine, float inv_t,
+                                                  uint32_t k0, uint32_t k1, int* accept_len, float4* info,
+                                                  int* status) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int64_t trow0 = (int64_t)b * (gamma + 1);
+  const float lse_p = lane <= gamma ? lse_of(part + (trow0 + lane) * n_chunks, n_chunks) : 0.f;
+  const float lse_q =
+      (lane >= 1 && lane <= gamma)
+          ? lse_of(part + ((int64_t)B * (gamma + 1) + (int64_t)b * gamma + lane - 1) * n_chunks, n_chunks)
+          : 0.f;
+  const float lse_prev = __shfl(lse_p, lane > 0 ? lane - 1 : 0, kWave);
+  bool reject = false;
+  if (lane >= 1 && lane <= gamma) {
+    const int t = spine[trow0 + lane];
+    if (t < 0 || t >= V) {
+      raise_status(status, 1);
+      reject = true;
+    } else {
+      const float lp = ld_f(tl + (trow0 + lane - 1) * V + t) * inv_t - lse_prev;
+      const float lq = sc[((int64_t)b * gamma + lane - 1) * V + t] - lse_q;
+      const float u = rng_uniform(k0, k1, kTagAccept, b, lane, 0);
+      reject = !(lp - lq - logf(u) > 0.f);
+    }
+  }
+  const uint64_t mask = __ballot(reject);
+  const int r = mask ? (__ffsll((unsigned long long)mask) - 2) : gamma;
+  const float lp_r = __shfl(lse_p, r, kWave);
+  const float lq_r = __shfl(lse_q, r < gamma ? r + 1 : 0, kWave);
+  if (lane == 0) {
+    accept_len[b] = r;
+    info[b] = make_float4((float)r, lp_r, lq_r, 0.f);
+  }
+}
+
+// Bonus candidates of one chunk: keys of log(p - q) + G where p > q (the residual) and of
+// log p + G (used after full acceptance, or should rounding leave the residual empty).
+template <typename T>
+__global__ __launch_bounds__(256) void spec_bonus_partial(int gamma, int V, int chunk, int n_chunks, const T* tl,
+                                                          const float* sc, const float4* info, float inv_t,
+                                                          uint32_t k0, uint32_t k1, uint64_t* bpart) {
+  __shared__ uint64_t red[2][4];
+  const int c = blockIdx.x, b = blockIdx.y;
+  const float4 in = info[b];
+  const int r = (int)in.x;
+  const T* prow = tl + ((int64_t)b * (gamma + 1) + r) * V;
+  const float* qrow = r < gamma ? sc + ((int64_t)b * gamma + r) * V : nullptr;
+  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  uint64_t kres = 0, kp = 0;
+  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+    const float lp = ld_f(prow + v) * inv_t - in.y;
+    const float g = rng_gumbel(k0, k1, kTagBonus, b, 0, v);
+    const uint64_t a = argmax_key(lp + g, (uint32_t)v);
+    kp = a > kp ? a : kp;
+    if (qrow) {
+      const float d = expf(lp) - expf(qrow[v] - in.z);
+      if (d > 0.f) {
+        const uint64_t k = argmax_key(logf(d) + g, (uint32_t)v);
+        kres = k > kres ? k : kres;
+      }
+    }
+  }
+  kres = wave_max_u64(kres);
+  kp = wave_max_u64(kp);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = kres;
+    red[1][threadIdx.x >> 6] = kp;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    uint64_t m = red[threadIdx.x][0];
+    for (int i = 1; i < 4; ++i) m = red[threadIdx.x][i] > m ? red[threadIdx.x][i] : m;
+    bpart[((int64_t)b * n_chunks + c) * 2 + threadIdx.x] = m;
+  }
+}
+
+__global__ __launch_bounds__(64) void spec_bonus_final(int gamma, int n_chunks, const float4* info,
+                                                       const uint64_t* bpart, int* bonus) {
+  const int b = blockIdx.x;
+  uint64_t kres = 0, kp = 0;
+  for (int c = threadIdx.x; c < n_chunks; c += 64) {
+    const uint64_t a = bpart[((int64_t)b * n_chunks + c) * 2], p = bpart[((int64_t)b * n_chunks + c) * 2 + 1];
+    kres = a > kres ? a : kres;
+    kp = p > kp ? p : kp;
+  }
+  kres = wave_max_u64(kres);
+  kp = wave_max_u64(kp);
+  if (threadIdx.x == 0) {
+    const int r = (int)info[b].x;
+    bonus[b] = (int)key_index((r < gamma && kres != 0) ? kres : kp);
+  }
+}
 }  // namespace
 
 hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits, const int* spine,
@@ -397,6 +596,56 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
   return hipGetLastError();
 }
 
+size_t verify_sampled_bytes(int B, int gamma, int n_chunks) {
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  return up((size_t)B * (2 * gamma + 1) * n_chunks * 8) + up((size_t)B * 16) + up((size_t)B * n_chunks * 16);
+}
+
+hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, const void* logits, const float* scores,
+                                 const int* spine, float inv_t, uint32_t k0, uint32_t k1, int* accept_len,
+                                 int* bonus, void* scratch, int n_chunks, int chunk, int* status, hipStream_t st) {
+  Phase ph("verify", st);
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  char* base = (char*)scratch;
+  float2* part = (float2*)base;
+  float4* info = (float4*)(base + up((size_t)B * (2 * gamma + 1) * n_chunks * 8));
+  uint64_t* bpart = (uint64_t*)((char*)info + up((size_t)B * 16));
+  const size_t esz = logits_dtype == 1 ? 2 : 4;
+  const bool vec = ((uintptr_t)logits % 16 == 0) && ((uintptr_t)scores % 16 == 0) && ((size_t)V * esz % 16 == 0) &&
+                   (V % 4 == 0) && ((size_t)chunk * esz % 16 == 0);
+  const int n_trows = B * (gamma + 1);
+  dim3 g1(n_chunks, n_trows + B * gamma);
+#define DPARA_LSE(TT, VV)                                                                                        \
+  hipLaunchKernelGGL((lse_partial<TT, VV>), g1, dim3(256), 0, st, (const TT*)logits, scores, V, chunk, n_chunks, \
+                     n_trows, inv_t, part)
+  if (logits_dtype == 1) {
+    if (vec) DPARA_LSE(bf16_t, true);
+    else DPARA_LSE(bf16_t, false);
+  } else {
+    if (vec) DPARA_LSE(float, true);
+    else DPARA_LSE(float, false);
+  }
+#undef DPARA_LSE
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (logits_dtype == 1) {
+    hipLaunchKernelGGL(spec_accept<bf16_t>, dim3(B), dim3(64), 0, st, B, gamma, V, n_chunks, part,
+                       (const bf16_t*)logits, scores, spine, inv_t, k0, k1, accept_len, info, status);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(spec_bonus_partial<bf16_t>, dim3(n_chunks, B), dim3(256), 0, st, gamma, V, chunk, n_chunks,
+                       (const bf16_t*)logits, scores, info, inv_t, k0, k1, bpart);
+  } else {
+    hipLaunchKernelGGL(spec_accept<float>, dim3(B), dim3(64), 0, st, B, gamma, V, n_chunks, part,
+                       (const float*)logits, scores, spine, inv_t, k0, k1, accept_len, info, status);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(spec_bonus_partial<float>, dim3(n_chunks, B), dim3(256), 0, st, gamma, V, chunk, n_chunks,
+                       (const float*)logits, scores, info, inv_t, k0, k1, bpart);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(spec_bonus_final, dim3(B), dim3(64), 0, st, gamma, n_chunks, info, bpart, bonus);
+  return hipGetLastError();
+}
+
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, const int* accept_len, float* G,
                                 float* G_out, bf16_t* Ghi, uint64_t* clear, int64_t n_clear, int* status,
                                 hipStream_t st) {
@@ -416,19 +665,20 @@ template <typename T, int P>
 hipError_t launch_ar_pf(dim3 grid, hipStream_t st, int step, int gamma, int V, int rank, const float* logits,
                         const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
                         float* margins, uint64_t* part, int n_chunks, int chunk, int B, int* status,
-                        const int* only_if) {
+                        const int* only_if, const Sampling& smp) {
   hipLaunchKernelGGL((ar_step_pf<T, P>), grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const T*)E,
-                     (const T*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status, only_if);
+                     (const T*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status, only_if,
+                     smp);
   return hipGetLastError();
 }
 
 hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                           const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                           uint64_t* part, int n_chunks, int chunk, uint64_t* ppart, int ppart_grid, int* status,
-                          const int* only_if, hipStream_t st) {
+                          const int* only_if, hipStream_t st, const Sampling& smp) {
   if (dtype == 1 && ppart && ppart_grid > 0) {
     const hipError_t e = launch_ar_head_persistent(B, gamma, V, rank, logits, E, W, bonus, drafts, next_spine,
-                                                   margins, ppart, ppart_grid, status, only_if, st);
+                                                   margins, ppart, ppart_grid, status, only_if, st, smp);
     if (e != hipErrorNotSupported) return e;
   }
   if (chunk != ar_head_chunk(dtype, rank) || n_chunks != (V + chunk - 1) / chunk) return hipErrorInvalidValue;
@@ -439,7 +689,7 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
     hipError_t e = hipErrorInvalidValue;
 #define DPARA_AR_PF(TT, PP) \
   e = launch_ar_pf<TT, PP>(grid, st, step, gamma, V, rank, logits, E, W, bonus, drafts, next_spine, margins, part, \
-                           n_chunks, chunk, B, status, only_if)
+                           n_chunks, chunk, B, status, only_if, smp)
     if (dtype == 1) {
       switch (P) {
         case 1: DPARA_AR_PF(bf16_t, 1); break;
@@ -453,7 +703,7 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
         default:
           hipLaunchKernelGGL(ar_step<bf16_t>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const bf16_t*)E,
                              (const bf16_t*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status,
-                             only_if);
+                             only_if, smp);
           e = hipGetLastError();
       }
     } else {
@@ -465,7 +715,7 @@ hipError_t launch_ar_head(int dtype, int B, int gamma, int V, int rank, const fl
         default:
           hipLaunchKernelGGL(ar_step<float>, grid, dim3(256), 0, st, step, gamma, V, rank, logits, (const float*)E,
                              (const float*)W, bonus, drafts, next_spine, margins, part, n_chunks, chunk, B, status,
-                             only_if);
+                             only_if, smp);
           e = hipGetLastError();
       }
     }

@@ -26,7 +26,8 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_branch_candidates", "dpara_select_and_head_cand", "dpara_clear_status",
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
            "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_target_forward_hidden",
-           "dpara_fuse_workspace_bytes", "dpara_fuse_features")
+           "dpara_fuse_workspace_bytes", "dpara_fuse_features", "dpara_select_and_head_sampled",
+           "dpara_verify_sampled")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -106,6 +107,10 @@ def lib():
         L.dpara_fuse_workspace_bytes.argtypes = [P(DparaConfig), I32, I32]
         L.dpara_fuse_workspace_bytes.restype = SZ
         L.dpara_fuse_features.argtypes = [P(DparaConfig), P(DparaFusionWeights), I32, VP, VP, VP, SZ, VP]
+        F32, U64 = ctypes.c_float, ctypes.c_uint64
+        L.dpara_select_and_head_sampled.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP,
+                                                    VP, F32, U64, VP, VP, SZ, VP]
+        L.dpara_verify_sampled.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, F32, U64, VP, VP, VP, SZ, VP]
         L.dpara_last_error.restype = ctypes.c_char_p
         L.dpara_version.restype = I32
         L.dpara_profile_enable.argtypes = [I32]
@@ -114,7 +119,7 @@ def lib():
                      "dpara_select_and_head", "dpara_branch_candidates", "dpara_select_and_head_cand",
                      "dpara_clear_status", "dpara_profile_enable",
                      "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features",
-                     "dpara_target_forward_hidden"):
+                     "dpara_target_forward_hidden", "dpara_select_and_head_sampled", "dpara_verify_sampled"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -361,6 +366,27 @@ def select_and_head(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts,
     dpara_select_and_head(d.cfg, d.w, int(accept_len.shape[0]), _ptr(reps), _ptr(accept_len), _ptr(bonus),
                           _ptr(gathered), _ptr(drafts), _ptr(next_spine), _ptr(margins), ws.ptr, ws.nbytes,
                           _stream(stream))
+
+
+def select_and_head_sampled(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts, next_spine, margins,
+                            temperature: float, seed: int, scores, ws: Workspace, stream=None):
+    """The sampled head: y_i ~ softmax(z_i / T) from the library's counter-based generator;
+    scores [B, gamma, V] float32 (or None) receives z_i / T."""
+    _check(lib().dpara_select_and_head_sampled(_ref(d.cfg), _ref(d.w), int(accept_len.shape[0]), _ptr(reps),
+                                               _ptr(accept_len), _ptr(bonus), _ptr(gathered), _ptr(drafts),
+                                               _ptr(next_spine), _ptr(margins), float(temperature), int(seed),
+                                               _ptr(scores), ws.ptr, ws.nbytes, _stream(stream)))
+
+
+def verify_sampled(d: DeviceDrafter, logits, scores, spine, temperature: float, seed: int, accept_len, bonus,
+                   ws: Workspace, stream=None):
+    """Speculative-sampling verification: logits [B, gamma+1, V] (bf16 or float32), scores
+    [B, gamma, V] float32 (the drafts' tempered scores), spine [B, gamma+1] int32."""
+    import torch
+    ldt = DPARA_BF16 if logits.dtype == torch.bfloat16 else DPARA_F32
+    _check(lib().dpara_verify_sampled(_ref(d.cfg), int(spine.shape[0]), _ptr(logits), ldt, _ptr(scores),
+                                      _ptr(spine), float(temperature), int(seed), _ptr(accept_len), _ptr(bonus),
+                                      ws.ptr, ws.nbytes, _stream(stream)))
 
 
 def branch_candidates_buffer(d: DeviceDrafter, batch: int, device="cuda"):

@@ -78,6 +78,14 @@ class DeviceRound:
         D.select_and_head(self.d, self.reps, self.accept, self.bonus, self.gathered, self.drafts,
                           self.next_spine, self.margins, self.ws, stream)
 
+    def head_sampled(self, temperature: float, seed: int, scores=None, stream=None):
+        D.select_and_head_sampled(self.d, self.reps, self.accept, self.bonus, self.gathered, self.drafts,
+                                  self.next_spine, self.margins, temperature, seed, scores, self.ws, stream)
+
+    def verify_sampled(self, scores, temperature: float, seed: int, stream=None):
+        D.verify_sampled(self.d, self.logits, scores, self.spine, temperature, seed, self.accept, self.bonus,
+                         self.ws, stream)
+
     def candidates(self, stream=None):
         """Every branch row's head candidates (the off-serial-path head variant)."""
         if getattr(self, "cand", None) is None:

@@ -1,0 +1,199 @@
+"""GPU parity of the sampling variant (speculative-sampling verification and the sampled AR
+head) against the oracle, through the C ABI.
+
+Both sides draw from the same counter-based generator, so the draws are the same wherever
+floating point cannot flip them: an acceptance test is compared where the oracle's log-ratio
+margin |log p - log q - log u| exceeds 1e-4 (the float32 log-sum-exp over the vocabulary is
+good to about 1e-6 there), a bonus or head draw where the oracle's top1 - top2 of the
+perturbed scores exceeds 1e-3 (bonus) or 1e-2 (head, whose scores carry the bf16 model's
+rounding); the tests also require that almost every decision was compared."""
+import types
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import dpara_oracle as O  # noqa: E402
+from paper_2609_27396_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+ACC_MARGIN, BONUS_MARGIN, HEAD_MARGIN = 1e-4, 1e-3, 1e-2
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _round_bf16(x):
+    return torch.from_numpy(np.asarray(x, np.float32)).to(torch.bfloat16).float().numpy()
+
+
+def _verify_inputs(B, gamma, V, T, dtype, seed):
+    """Target logits N(0, 2); draft scores close to the target's tempered logits for even
+    requests (long acceptances) and unrelated for odd ones; drafts drawn from q."""
+    rng = np.random.default_rng(seed)
+    L = rng.standard_normal((B, gamma + 1, V)).astype(np.float32) * 2.0
+    if dtype == "bf16":
+        L = _round_bf16(L)
+    S = np.empty((B, gamma, V), np.float32)
+    for b in range(B):
+        if b % 2 == 0:
+            S[b] = L[b, :gamma] / T + rng.standard_normal((gamma, V)).astype(np.float32) * 0.3
+        else:
+            S[b] = rng.standard_normal((gamma, V)).astype(np.float32) * 2.0
+    spine = np.empty((B, gamma + 1), np.int32)
+    spine[:, 0] = rng.integers(0, V, B)
+    for b in range(B):
+        for i in range(gamma):
+            q = np.exp(S[b, i].astype(np.float64) - S[b, i].max())
+            spine[b, i + 1] = rng.choice(V, p=q / q.sum())
+    return L, S, spine
+
+
+VERIFY_CASES = {
+    "v3001_bf16_t1": (6, 5, 3001, 1.0, "bf16"),     # odd vocabulary: element loads
+    "v8192_f32_t07": (5, 7, 8192, 0.7, "f32"),      # 16-byte loads, temperature 0.7
+    "v151936_bf16_t1": (2, 16, 151936, 1.0, "bf16"),  # Qwen3 vocabulary, draft length 16
+}
+
+
+@pytest.mark.parametrize("case", sorted(VERIFY_CASES))
+def test_verify_sampled_parity(case):
+    from paper_2609_27396_amd import dpara as D
+    B, gamma, V, T, dtype = VERIFY_CASES[case]
+    shape = synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
+                               vocab=V, gamma=gamma, ar_rank=64, qk_norm=True, dtype="bf16")
+    _say("case", case)
+    cfg = D.make_config(shape)
+    d = types.SimpleNamespace(cfg=cfg)
+    ws = D.Workspace(cfg, B, 64)
+    L, S, spine = _verify_inputs(B, gamma, V, T, dtype, seed=len(case))
+    tl = torch.from_numpy(L).cuda().to(torch.bfloat16 if dtype == "bf16" else torch.float32)
+    sc = torch.from_numpy(S).cuda()
+    sp = torch.from_numpy(spine).cuda()
+    acc = torch.empty(B, dtype=torch.int32, device="cuda")
+    bon = torch.empty(B, dtype=torch.int32, device="cuda")
+    compared, total, accepted = 0, 0, []
+    for seed in (1, 2, 0xDEADBEEF12345):
+        D.dpara_clear_status(ws.ptr, D._stream(None))
+        D.verify_sampled(d, tl, sc, sp, T, seed, acc, bon, ws)
+        torch.cuda.synchronize()
+        assert ws.status() == 0
+        ga, gb = acc.cpu().numpy(), bon.cpu().numpy()
+        for b in range(B):
+            r, bonus, info = O.verify_sampled(L[b], S[b], spine[b], T, seed, b)
+            am = np.abs(info["accept_margins"])
+            total += 1
+            accepted.append(int(ga[b]))
+            if am.min() > ACC_MARGIN:
+                assert int(ga[b]) == r, (seed, b, ga[b], r, info["accept_margins"])
+                if info["bonus_margin"] > BONUS_MARGIN:
+                    assert int(gb[b]) == bonus, (seed, b, gb[b], bonus, info["bonus_margin"])
+                    compared += 1
+    _say(f"{case}: accepted lengths {accepted}; compared {compared} of {total} verdicts")
+    assert compared >= total - 1
+    assert max(accepted) >= 2 and min(accepted) == 0
+
+
+def test_verify_sampled_full_acceptance_and_token_range():
+    """q == p accepts every draft and draws the bonus from p_gamma; an out-of-range draft is
+    flagged and never accepted."""
+    from paper_2609_27396_amd import dpara as D
+    B, gamma, V, T = 3, 4, 1000, 1.0
+    shape = synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
+                               vocab=V, gamma=gamma, ar_rank=64, qk_norm=True, dtype="bf16")
+    cfg = D.make_config(shape)
+    d = types.SimpleNamespace(cfg=cfg)
+    ws = D.Workspace(cfg, B, 64)
+    L = np.random.default_rng(3).standard_normal((B, gamma + 1, V)).astype(np.float32)
+    S = np.ascontiguousarray(L[:, :gamma])
+    spine = np.random.default_rng(4).integers(0, V, (B, gamma + 1)).astype(np.int32)
+    acc = torch.empty(B, dtype=torch.int32, device="cuda")
+    bon = torch.empty(B, dtype=torch.int32, device="cuda")
+    D.verify_sampled(d, torch.from_numpy(L).cuda(), torch.from_numpy(S).cuda(), torch.from_numpy(spine).cuda(), T,
+                     9, acc, bon, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    for b in range(B):
+        r, bonus, info = O.verify_sampled(L[b], S[b], spine[b], T, 9, b)
+        assert r == gamma and int(acc[b]) == gamma
+        if info["bonus_margin"] > BONUS_MARGIN:
+            assert int(bon[b]) == bonus
+    spine[1, 2] = V + 7
+    D.verify_sampled(d, torch.from_numpy(L).cuda(), torch.from_numpy(S).cuda(), torch.from_numpy(spine).cuda(), T,
+                     9, acc, bon, ws)
+    torch.cuda.synchronize()
+    assert ws.status() & D.STATUS_TOKEN_RANGE
+    assert int(acc[1]) == 1 and int(acc[0]) == gamma
+
+
+def _check_head_sampled(shape, w, dr, scores, T, seed, mode):
+    """Teacher-forced: step i of the oracle is fed the GPU's y_{i-1} and the GPU's gathered
+    rows (copied bit for bit from its reps); scores within 1e-3 + 1e-3 |s|."""
+    compared = 0
+    for b in range(dr.B):
+        gathered = dr.gathered[b].cpu().numpy()
+        r = int(dr.accept[b].item())
+        np.testing.assert_array_equal(gathered, dr.reps[b, r].cpu().numpy())
+        drafts, bonus = dr.drafts[b].cpu().numpy(), int(dr.bonus[b].item())
+        assert dr.next_spine[b, 0].item() == bonus
+        np.testing.assert_array_equal(dr.next_spine[b, 1:].cpu().numpy(), drafts)
+        sg = scores[b].cpu().numpy()
+        ell = O.base_logits(w, gathered, mode)
+        y_prev = bonus
+        for i in range(1, shape.gamma + 1):
+            y, m, s = O.head_step_sampled(w, ell[i - 1], y_prev, T, seed, b, i, mode)
+            assert np.all(np.abs(sg[i - 1] - s) <= 1e-3 + 1e-3 * np.abs(s)), (b, i)
+            if m > HEAD_MARGIN:
+                assert int(drafts[i - 1]) == y, (b, i, drafts[i - 1], y, m)
+                compared += 1
+            y_prev = int(drafts[i - 1])
+    return compared
+
+
+HEAD_CASES = {
+    # bf16, rank 64, 3 requests: the persistent head
+    "bf16_persistent": ("h256_hd128_g5", [0, 77, 300], 1.0),
+    # bf16, 18 requests (more than one persistent launch holds): the step kernels
+    "bf16_steps_b18": ("h256_hd128_g5", [5 * i for i in range(18)], 0.8),
+    # float32 model: the step kernels
+    "f32_steps": ("f32_h256_g7", [33, 150], 1.0),
+}
+
+
+@pytest.mark.parametrize("case", sorted(HEAD_CASES))
+def test_head_sampled_parity(case):
+    from test_gpu_parity import SMALL_CASES
+    from paper_2609_27396_amd.harness import DeviceRound
+    name, ctx, T = HEAD_CASES[case]
+    shape = SMALL_CASES[name][0]
+    mode = shape.dtype
+    _say("case", case)
+    wl = synth.Workload("hs", shape, batch=len(ctx), ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=21,
+                        logits_dtype="bf16" if mode == "bf16" else "f32")
+    w = synth.make_weights(shape, seed=22, gain_jitter=0.1, ar_e_std=1.0, ar_w_std=0.3)
+    ri = synth.make_round(wl, ctx_lens=ctx)
+    dr = DeviceRound(shape, w, ri)
+    dr.backbone()
+    dr.verify()
+    scores = torch.empty((len(ctx), shape.gamma, shape.vocab), dtype=torch.float32, device="cuda")
+    total = 0
+    for seed in (5, 77):
+        dr.head_sampled(T, seed, scores)
+        torch.cuda.synchronize()
+        assert dr.status() == 0
+        compared = _check_head_sampled(shape, w, dr, scores, T, seed, mode)
+        total += len(ctx) * shape.gamma
+        _say(f"{case} seed {seed}: drafts {dr.drafts.cpu().numpy().tolist()[:3]}, compared {compared}")
+        assert compared >= len(ctx) * shape.gamma - 2
+    # the draws are not the greedy tokens (the noise is there) and differ between seeds
+    dr.head_sampled(T, 5, scores)
+    d5 = dr.drafts.clone()
+    dr.head_sampled(T, 6, scores)
+    assert not torch.equal(d5, dr.drafts)
+    # scores may be NULL
+    dr.head_sampled(T, 5, None)
+    torch.cuda.synchronize()
+    assert torch.equal(d5, dr.drafts)
