@@ -247,14 +247,16 @@ def fuse_timing(shape, rows=(17, 2048), n_feat=3, iters=20):
 def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
     """Select + AR head alone at several batch sizes, on synthetic branch representations
     (microseconds per call): the plain call (gather, LM head over gamma rows, gamma AR
-    steps), and the off-serial-path variant: the branch-candidates call (every branch row's
-    LM head with top-2 tiles, timed on its own) and the serial call that uses them."""
+    steps), the off-serial-path variant: the branch-candidates call (every branch row's
+    LM head with top-2 tiles, timed on its own) and the serial call that uses them, and the
+    sampling variant: the sampled head and the speculative-sampling verification."""
     import torch
     from paper_2609_27396_amd import dpara as D
     g, H, V = shape.gamma, shape.hidden, shape.vocab
     gen = torch.Generator(device="cuda")
     gen.manual_seed(1234)
-    out = {"plain_us": {}, "plain_fallback": {}, "candidates_us": {}, "cand_serial_us": {}, "cand_fallback": {}}
+    out = {"plain_us": {}, "plain_fallback": {}, "candidates_us": {}, "cand_serial_us": {}, "cand_fallback": {},
+           "sampled_head_us": {}, "sampled_verify_us": {}}
 
     def timed(call):
         for _ in range(3):
@@ -283,8 +285,15 @@ def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
         out["cand_serial_us"][k] = timed(
             lambda: D.select_and_head_cand(dr.d, reps, cand, acc, bon, None, drafts, nspine, None, ws))
         out["cand_fallback"][k] = ws.head_fallback()
+        # sampling variant: the sampled head (full head with Gumbel noise, draft scores out)
+        # and the speculative-sampling verification of a block
+        scores = torch.randn((B, g, V), generator=gen, device="cuda", dtype=torch.float32)
+        out["sampled_head_us"][k] = timed(lambda: D.select_and_head_sampled(
+            dr.d, reps, acc, bon, None, drafts, nspine, None, 1.0, 77, scores, ws))
+        tl = torch.randn((B, g + 1, V), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+        out["sampled_verify_us"][k] = timed(lambda: D.verify_sampled(dr.d, tl, scores, nspine, 1.0, 78, acc, bon, ws))
         assert ws.status() == 0, f"device status {ws.status()}"
-        del ws, reps, cand
+        del ws, reps, cand, scores, tl
     return out
 
 
