@@ -151,3 +151,27 @@ def test_target_hidden_validation_without_gpu():
     out = (ctypes.c_int32 * 3)(0, cfg.n_layers - 1, cfg.n_layers)
     assert _rc("dpara_target_forward_hidden", *args(out, 3, FAKE)) == D.DPARA_E_INVALID
     assert "feat_layers[2]" in D.dpara_last_error()
+
+
+def test_sampling_validation_without_gpu():
+    """The sampled head and verification reject a non-positive or non-finite temperature and
+    missing buffers on the host, before any launch."""
+    shape = synth.QWEN3_8B
+    cfg = D.make_config(shape)
+    w, _layers = _fake_weights(shape)
+    R = ctypes.byref
+    ws, nb = FAKE, D.dpara_workspace_bytes(cfg, 1, 64)
+    for t in (0.0, -1.0, float("inf"), float("nan"), 1e-45):
+        rc = _rc("dpara_select_and_head_sampled", R(cfg), R(w), 1, FAKE, FAKE, FAKE, None, FAKE, FAKE, None,
+                 t, 1, None, ws, nb, None)
+        assert rc == D.DPARA_E_INVALID, t
+        assert "temperature" in D.dpara_last_error()
+        rc = _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, t, 1, FAKE, FAKE, ws, nb, None)
+        assert rc == D.DPARA_E_INVALID, t
+    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, None, FAKE, 1.0, 1, FAKE, FAKE, ws, nb,
+               None) == D.DPARA_E_INVALID
+    assert "draft_scores" in D.dpara_last_error()
+    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, 7, FAKE, FAKE, 1.0, 1, FAKE, FAKE, ws, nb,
+               None) == D.DPARA_E_UNSUPPORTED
+    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, 1.0, 1, FAKE, FAKE, ws, 1024,
+               None) == D.DPARA_E_WORKSPACE
