@@ -305,6 +305,8 @@ def main():
     ap.add_argument("--workload", default="qwen3_8b_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-head-sweep", action="store_true")
+    ap.add_argument("--head-sweep-batches", default="1,2,4,8,16",
+                    help="comma-separated batch sizes of the head sweep")
     ap.add_argument("--no-graph", action="store_true", help="skip timing the step as HIP graph replays")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run a plain 256 MiB device copy 3 times (known HBM bytes, to scale "
@@ -449,7 +451,7 @@ def main():
         "graph_ms_per_step": graph_ms,
     }
     if shape.dtype == "bf16" and not args.no_head_sweep:
-        hs = head_sweep(dr, shape)
+        hs = head_sweep(dr, shape, batches=tuple(int(x) for x in args.head_sweep_batches.split(",")))
         out["head_us_by_batch"] = hs.pop("plain_us")
         out["head_variants_by_batch"] = hs
     if shape.dtype == "bf16" and not args.no_head_sweep:

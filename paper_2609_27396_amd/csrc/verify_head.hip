@@ -67,16 +67,27 @@ __global__ __launch_bounds__(256) void verify_partial(const T* logits, int V, in
   }
 }
 
-__global__ __launch_bounds__(64) void verify_finalize(int gamma, int V, int n_chunks, const uint64_t* part,
-                                                      const int* spine, int* accept_len, int* bonus,
-                                                      int* target_argmax, int* status) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+// One workgroup of 16 waves per request: wave w reduces rows w, w + 16, ... with one chunk
+// partial per lane (all loads of a row in flight at once), then wave 0 compares the drafts.
+constexpr int kFinWaves = 16;
+__global__ __launch_bounds__(64 * kFinWaves) void verify_finalize(int gamma, int V, int n_chunks,
+                                                                  const uint64_t* part, const int* spine,
+                                                                  int* accept_len, int* bonus, int* target_argmax,
+                                                                  int* status) {
+  __shared__ int gs[64];
+  const int b = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int j = wave; j <= gamma; j += kFinWaves) {
+    const uint64_t* p = part + ((int64_t)b * (gamma + 1) + j) * n_chunks;
+    uint64_t best = 0;
+    for (int c = lane; c < n_chunks; c += 64) best = p[c] > best ? p[c] : best;
+    best = wave_max_u64(best);
+    if (lane == 0) gs[j] = (int)key_index(best);
+  }
+  __syncthreads();
+  if (wave != 0) return;
   int g = 0;
   if (lane <= gamma) {
-    const uint64_t* p = part + ((int64_t)b * (gamma + 1) + lane) * n_chunks;
-    uint64_t best = 0;
-    for (int c = 0; c < n_chunks; ++c) best = p[c] > best ? p[c] : best;
-    g = (int)key_index(best);
+    g = gs[lane];
     if (target_argmax) target_argmax[b * (gamma + 1) + lane] = g;
   }
   bool mismatch = false;
@@ -93,6 +104,7 @@ __global__ __launch_bounds__(64) void verify_finalize(int gamma, int V, int n_ch
     bonus[b] = bon;
   }
 }
+
 
 __global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const float* reps, const int* accept_len,
                                                      float* G, float* G_out, bf16_t* Ghi, int64_t lo_off,
@@ -406,28 +418,41 @@ __device__ __forceinline__ void ms_merge(float& m, float& s, float om, float os)
 }
 
 // Row r < n_trows: target row (times inv_t); otherwise draft-score row r - n_trows.  Every
-// workgroup writes (max, sum) of its chunk to part[row][chunk].
+// workgroup writes (max, sum) of its chunk of kLseChunk entries to part[row][chunk]; the
+// 16-byte form loads all of a thread's entries into registers, takes their max, then sums
+// one exponential per entry.
+constexpr int kLseChunk = 4096;
 template <typename T, bool VEC>
-__global__ __launch_bounds__(256) void lse_partial(const T* tl, const float* sc, int V, int chunk, int n_chunks,
-                                                   int n_trows, float inv_t, float2* part) {
+__global__ __launch_bounds__(256) void lse_partial(const T* tl, const float* sc, int V, int n_chunks, int n_trows,
+                                                   float inv_t, float2* part) {
   __shared__ float rm[4], rs[4];
   const int row = blockIdx.y, c = blockIdx.x;
-  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  const int v0 = c * kLseChunk, v1 = min(V, v0 + kLseChunk);
   float m = -INFINITY, s = 0.f;
   if (row < n_trows) {
     const T* x = tl + (int64_t)row * V;
     if constexpr (VEC) {
-      constexpr int EPP = 16 / sizeof(T);
-      for (int v = v0 + threadIdx.x * EPP; v < v1; v += 256 * EPP) {
-        const uint4 u = *(const uint4*)(x + v);
+      constexpr int EPP = 16 / sizeof(T), NL = kLseChunk / (256 * EPP);
+      float f[NL * EPP];
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int v = v0 + (k * 256 + (int)threadIdx.x) * EPP;
+        const uint4 u = v < v1 ? *(const uint4*)(x + v) : make_uint4(0, 0, 0, 0);
         const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
         for (int q = 0; q < EPP; ++q) {
-          float f;
-          if constexpr (sizeof(T) == 2) f = __uint_as_float(q & 1 ? (w[q >> 1] & 0xFFFF0000u) : (w[q >> 1] << 16));
-          else f = __uint_as_float(w[q]);
-          if (v + q < v1) ms_add(m, s, f * inv_t);
+          float e;
+          if constexpr (sizeof(T) == 2) e = __uint_as_float(q & 1 ? (w[q >> 1] & 0xFFFF0000u) : (w[q >> 1] << 16));
+          else e = __uint_as_float(w[q]);
+          f[k * EPP + q] = v + q < v1 ? e * inv_t : -INFINITY;
         }
+      }
+      // the thread's entries are in registers: max first, then one exponential each
+#pragma unroll
+      for (int i = 0; i < NL * EPP; ++i) m = fmaxf(m, f[i]);
+      if (m > -INFINITY) {
+#pragma unroll
+        for (int i = 0; i < NL * EPP; ++i) s += expf(f[i] - m);
       }
     } else {
       for (int v = v0 + threadIdx.x; v < v1; v += 256) ms_add(m, s, ld_f(x + v) * inv_t);
@@ -435,12 +460,22 @@ __global__ __launch_bounds__(256) void lse_partial(const T* tl, const float* sc,
   } else {
     const float* x = sc + (int64_t)(row - n_trows) * V;
     if constexpr (VEC) {
-      for (int v = v0 + threadIdx.x * 4; v < v1; v += 1024) {
-        const float4 f = *(const float4*)(x + v);
-        ms_add(m, s, f.x);
-        if (v + 1 < v1) ms_add(m, s, f.y);
-        if (v + 2 < v1) ms_add(m, s, f.z);
-        if (v + 3 < v1) ms_add(m, s, f.w);
+      constexpr int NL = kLseChunk / 1024;
+      float f[NL * 4];
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int v = v0 + (k * 256 + (int)threadIdx.x) * 4;
+        const float4 q = v < v1 ? *(const float4*)(x + v) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        f[4 * k] = q.x;
+        f[4 * k + 1] = q.y;
+        f[4 * k + 2] = q.z;
+        f[4 * k + 3] = q.w;
+      }
+#pragma unroll
+      for (int i = 0; i < NL * 4; ++i) m = fmaxf(m, f[i]);
+      if (m > -INFINITY) {
+#pragma unroll
+        for (int i = 0; i < NL * 4; ++i) s += expf(f[i] - m);
       }
     } else {
       for (int v = v0 + threadIdx.x; v < v1; v += 256) ms_add(m, s, x[v]);
@@ -462,29 +497,35 @@ __global__ __launch_bounds__(256) void lse_partial(const T* tl, const float* sc,
   }
 }
 
-__device__ __forceinline__ float lse_of(const float2* p, int n_chunks) {
-  float m = -INFINITY, s = 0.f;
-  for (int c = 0; c < n_chunks; ++c) ms_merge(m, s, p[c].x, p[c].y);
-  return m + logf(s);
-}
-
-// One wave per request: lane j (1..gamma) tests draft t_j against p_{j-1} (target row j-1)
-// and q_j (draft-score row j-1) in log space: accepted iff log p - log q - log u > 0.  An
-// out-of-range draft is flagged and never accepted.  info[b] = (r, lse of target row r, lse
-// of draft-score row r (the residual's q), 0).
+// One workgroup of 16 waves per request.  The waves first reduce the chunk partials of the
+// request's 2 gamma + 1 rows (one partial per lane, then a shuffle merge) to log-sum-exps:
+// target rows 0..gamma and draft-score rows 1..gamma.  Then wave 0, lane j (1..gamma), tests
+// draft t_j against p_{j-1} (target row j-1) and q_j in log space: accepted iff
+// log p - log q - log u > 0.  An out-of-range draft is flagged and never accepted.
+// info[b] = (r, lse of target row r, lse of draft-score row r+1 (the residual's q), 0).
 template <typename T>
-__global__ __launch_bounds__(64) void spec_accept(int B, int gamma, int V, int n_chunks, const float2* part,
-                                                  const T* tl, const float* sc, const int* spine, float inv_t,
-                                                  uint32_t k0, uint32_t k1, int* accept_len, float4* info,
-                                                  int* status) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+__global__ __launch_bounds__(64 * kFinWaves) void spec_accept(int B, int gamma, int V, int n_chunks,
+                                                              const float2* part, const T* tl, const float* sc,
+                                                              const int* spine, float inv_t, uint32_t k0,
+                                                              uint32_t k1, int* accept_len, float4* info,
+                                                              int* status) {
+  __shared__ float lse[128];  // [0, gamma]: target rows; gamma + i: draft-score row of draft i
+  const int b = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t trow0 = (int64_t)b * (gamma + 1);
-  const float lse_p = lane <= gamma ? lse_of(part + (trow0 + lane) * n_chunks, n_chunks) : 0.f;
-  const float lse_q =
-      (lane >= 1 && lane <= gamma)
-          ? lse_of(part + ((int64_t)B * (gamma + 1) + (int64_t)b * gamma + lane - 1) * n_chunks, n_chunks)
-          : 0.f;
-  const float lse_prev = __shfl(lse_p, lane > 0 ? lane - 1 : 0, kWave);
+  for (int j = wave; j < 2 * gamma + 1; j += kFinWaves) {
+    const int64_t row = j <= gamma ? trow0 + j : (int64_t)B * (gamma + 1) + (int64_t)b * gamma + (j - gamma - 1);
+    const float2* p = part + row * n_chunks;
+    float m = -INFINITY, s = 0.f;
+    for (int c = lane; c < n_chunks; c += 64) ms_merge(m, s, p[c].x, p[c].y);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float om = __shfl_xor(m, o, kWave), os = __shfl_xor(s, o, kWave);
+      ms_merge(m, s, om, os);
+    }
+    if (lane == 0) lse[j] = m + logf(s);
+  }
+  __syncthreads();
+  if (wave != 0) return;
   bool reject = false;
   if (lane >= 1 && lane <= gamma) {
     const int t = spine[trow0 + lane];
@@ -492,46 +533,57 @@ __global__ __launch_bounds__(64) void spec_accept(int B, int gamma, int V, int n
       raise_status(status, 1);
       reject = true;
     } else {
-      const float lp = ld_f(tl + (trow0 + lane - 1) * V + t) * inv_t - lse_prev;
-      const float lq = sc[((int64_t)b * gamma + lane - 1) * V + t] - lse_q;
+      const float lp = ld_f(tl + (trow0 + lane - 1) * V + t) * inv_t - lse[lane - 1];
+      const float lq = sc[((int64_t)b * gamma + lane - 1) * V + t] - lse[gamma + lane];
       const float u = rng_uniform(k0, k1, kTagAccept, b, lane, 0);
       reject = !(lp - lq - logf(u) > 0.f);
     }
   }
   const uint64_t mask = __ballot(reject);
   const int r = mask ? (__ffsll((unsigned long long)mask) - 2) : gamma;
-  const float lp_r = __shfl(lse_p, r, kWave);
-  const float lq_r = __shfl(lse_q, r < gamma ? r + 1 : 0, kWave);
   if (lane == 0) {
     accept_len[b] = r;
-    info[b] = make_float4((float)r, lp_r, lq_r, 0.f);
+    info[b] = make_float4((float)r, lse[r], r < gamma ? lse[gamma + r + 1] : 0.f, 0.f);
   }
 }
 
-// Bonus candidates of one chunk: keys of log(p - q) + G where p > q (the residual) and of
-// log p + G (used after full acceptance, or should rounding leave the residual empty).
+// Bonus candidates of one chunk of kBonusChunk entries (4 per thread, loads first): keys of
+// log(p - q) + G where p > q (the residual) and of log p + G (used after full acceptance, or
+// should rounding leave the residual empty).
+constexpr int kBonusChunk = 1024;
 template <typename T>
-__global__ __launch_bounds__(256) void spec_bonus_partial(int gamma, int V, int chunk, int n_chunks, const T* tl,
+__global__ __launch_bounds__(256) void spec_bonus_partial(int gamma, int V, int n_bchunks, const T* tl,
                                                           const float* sc, const float4* info, float inv_t,
                                                           uint32_t k0, uint32_t k1, uint64_t* bpart) {
+  constexpr int PER = kBonusChunk / 256;
   __shared__ uint64_t red[2][4];
   const int c = blockIdx.x, b = blockIdx.y;
   const float4 in = info[b];
   const int r = (int)in.x;
   const T* prow = tl + ((int64_t)b * (gamma + 1) + r) * V;
   const float* qrow = r < gamma ? sc + ((int64_t)b * gamma + r) * V : nullptr;
-  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  float x[PER], y[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int v = c * kBonusChunk + k * 256 + (int)threadIdx.x;
+    x[k] = v < V ? ld_f(prow + v) : 0.f;
+    y[k] = (qrow && v < V) ? qrow[v] : 0.f;
+  }
   uint64_t kres = 0, kp = 0;
-  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const float lp = ld_f(prow + v) * inv_t - in.y;
-    const float g = rng_gumbel(k0, k1, kTagBonus, b, 0, v);
-    const uint64_t a = argmax_key(lp + g, (uint32_t)v);
-    kp = a > kp ? a : kp;
-    if (qrow) {
-      const float d = expf(lp) - expf(qrow[v] - in.z);
-      if (d > 0.f) {
-        const uint64_t k = argmax_key(logf(d) + g, (uint32_t)v);
-        kres = k > kres ? k : kres;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int v = c * kBonusChunk + k * 256 + (int)threadIdx.x;
+    if (v < V) {
+      const float lp = x[k] * inv_t - in.y;
+      const float g = rng_gumbel(k0, k1, kTagBonus, b, 0, v);
+      const uint64_t a = argmax_key(lp + g, (uint32_t)v);
+      kp = a > kp ? a : kp;
+      if (qrow) {
+        const float d = expf(lp) - expf(y[k] - in.z);
+        if (d > 0.f) {
+          const uint64_t kk = argmax_key(logf(d) + g, (uint32_t)v);
+          kres = kk > kres ? kk : kres;
+        }
       }
     }
   }
@@ -545,16 +597,16 @@ __global__ __launch_bounds__(256) void spec_bonus_partial(int gamma, int V, int 
   if (threadIdx.x < 2) {
     uint64_t m = red[threadIdx.x][0];
     for (int i = 1; i < 4; ++i) m = red[threadIdx.x][i] > m ? red[threadIdx.x][i] : m;
-    bpart[((int64_t)b * n_chunks + c) * 2 + threadIdx.x] = m;
+    bpart[((int64_t)b * n_bchunks + c) * 2 + threadIdx.x] = m;
   }
 }
 
-__global__ __launch_bounds__(64) void spec_bonus_final(int gamma, int n_chunks, const float4* info,
+__global__ __launch_bounds__(64) void spec_bonus_final(int gamma, int n_bchunks, const float4* info,
                                                        const uint64_t* bpart, int* bonus) {
   const int b = blockIdx.x;
   uint64_t kres = 0, kp = 0;
-  for (int c = threadIdx.x; c < n_chunks; c += 64) {
-    const uint64_t a = bpart[((int64_t)b * n_chunks + c) * 2], p = bpart[((int64_t)b * n_chunks + c) * 2 + 1];
+  for (int c = threadIdx.x; c < n_bchunks; c += 64) {
+    const uint64_t a = bpart[((int64_t)b * n_bchunks + c) * 2], p = bpart[((int64_t)b * n_bchunks + c) * 2 + 1];
     kres = a > kres ? a : kres;
     kp = p > kp ? p : kp;
   }
@@ -591,32 +643,35 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(verify_finalize, dim3(B), dim3(64), 0, st, gamma, V, n_chunks, part, spine, accept_len,
+  hipLaunchKernelGGL(verify_finalize, dim3(B), dim3(64 * kFinWaves), 0, st, gamma, V, n_chunks, part, spine, accept_len,
                      bonus, target_argmax, status);
   return hipGetLastError();
 }
 
 size_t verify_sampled_bytes(int B, int gamma, int n_chunks) {
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
-  return up((size_t)B * (2 * gamma + 1) * n_chunks * 8) + up((size_t)B * 16) + up((size_t)B * n_chunks * 16);
+  const size_t n_bchunks = (size_t)n_chunks * (kLseChunk / kBonusChunk);
+  return up((size_t)B * (2 * gamma + 1) * n_chunks * 8) + up((size_t)B * 16) + up((size_t)B * n_bchunks * 16);
 }
 
 hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, const void* logits, const float* scores,
                                  const int* spine, float inv_t, uint32_t k0, uint32_t k1, int* accept_len,
                                  int* bonus, void* scratch, int n_chunks, int chunk, int* status, hipStream_t st) {
+  if (chunk != kLseChunk || n_chunks != (V + kLseChunk - 1) / kLseChunk || gamma > 63) return hipErrorInvalidValue;
   Phase ph("verify", st);
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  const int n_bchunks = (V + kBonusChunk - 1) / kBonusChunk;
   char* base = (char*)scratch;
   float2* part = (float2*)base;
   float4* info = (float4*)(base + up((size_t)B * (2 * gamma + 1) * n_chunks * 8));
   uint64_t* bpart = (uint64_t*)((char*)info + up((size_t)B * 16));
   const size_t esz = logits_dtype == 1 ? 2 : 4;
   const bool vec = ((uintptr_t)logits % 16 == 0) && ((uintptr_t)scores % 16 == 0) && ((size_t)V * esz % 16 == 0) &&
-                   (V % 4 == 0) && ((size_t)chunk * esz % 16 == 0);
+                   (V % 4 == 0);
   const int n_trows = B * (gamma + 1);
   dim3 g1(n_chunks, n_trows + B * gamma);
-#define DPARA_LSE(TT, VV)                                                                                        \
-  hipLaunchKernelGGL((lse_partial<TT, VV>), g1, dim3(256), 0, st, (const TT*)logits, scores, V, chunk, n_chunks, \
+#define DPARA_LSE(TT, VV)                                                                                 \
+  hipLaunchKernelGGL((lse_partial<TT, VV>), g1, dim3(256), 0, st, (const TT*)logits, scores, V, n_chunks, \
                      n_trows, inv_t, part)
   if (logits_dtype == 1) {
     if (vec) DPARA_LSE(bf16_t, true);
@@ -628,21 +683,22 @@ hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, cons
 #undef DPARA_LSE
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const dim3 fin(64 * kFinWaves);
   if (logits_dtype == 1) {
-    hipLaunchKernelGGL(spec_accept<bf16_t>, dim3(B), dim3(64), 0, st, B, gamma, V, n_chunks, part,
-                       (const bf16_t*)logits, scores, spine, inv_t, k0, k1, accept_len, info, status);
+    hipLaunchKernelGGL(spec_accept<bf16_t>, dim3(B), fin, 0, st, B, gamma, V, n_chunks, part, (const bf16_t*)logits,
+                       scores, spine, inv_t, k0, k1, accept_len, info, status);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(spec_bonus_partial<bf16_t>, dim3(n_chunks, B), dim3(256), 0, st, gamma, V, chunk, n_chunks,
+    hipLaunchKernelGGL(spec_bonus_partial<bf16_t>, dim3(n_bchunks, B), dim3(256), 0, st, gamma, V, n_bchunks,
                        (const bf16_t*)logits, scores, info, inv_t, k0, k1, bpart);
   } else {
-    hipLaunchKernelGGL(spec_accept<float>, dim3(B), dim3(64), 0, st, B, gamma, V, n_chunks, part,
-                       (const float*)logits, scores, spine, inv_t, k0, k1, accept_len, info, status);
+    hipLaunchKernelGGL(spec_accept<float>, dim3(B), fin, 0, st, B, gamma, V, n_chunks, part, (const float*)logits,
+                       scores, spine, inv_t, k0, k1, accept_len, info, status);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(spec_bonus_partial<float>, dim3(n_chunks, B), dim3(256), 0, st, gamma, V, chunk, n_chunks,
+    hipLaunchKernelGGL(spec_bonus_partial<float>, dim3(n_bchunks, B), dim3(256), 0, st, gamma, V, n_bchunks,
                        (const float*)logits, scores, info, inv_t, k0, k1, bpart);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(spec_bonus_final, dim3(B), dim3(64), 0, st, gamma, n_chunks, info, bpart, bonus);
+  hipLaunchKernelGGL(spec_bonus_final, dim3(B), dim3(64), 0, st, gamma, n_bchunks, info, bpart, bonus);
   return hipGetLastError();
 }
 
