@@ -197,3 +197,92 @@ def test_head_sampled_parity(case):
     dr.head_sampled(T, 5, None)
     torch.cuda.synchronize()
     assert torch.equal(d5, dr.drafts)
+
+
+def test_iterated_sampled_rounds():
+    """Algorithm 1 with sampling, iterated over three rounds on random weights: target forward
+    of the block (hidden states after layers 0, 1 and 3), speculative-sampling verification
+    against the draft scores the previous round's sampled head wrote, the all-boundary
+    backbone, the sampled head (next block and its scores), fusion and the append of
+    t_0..t_r.  The loop is driven by the oracle's own decisions (block, append count); the
+    GPU's verdict, bonus and drafts are compared with the oracle's wherever its margins make
+    them unique, its scores within the head's bar.  Round 0 starts from synthetic scores."""
+    from test_gpu_parity import LOOP_DRAFTER, LOOP_TARGET, FEAT_LAYERS, TOL
+    from paper_2609_27396_amd import dpara as D
+    from paper_2609_27396_amd.harness import DeviceRound, upload_cache
+    sd, st_ = LOOP_DRAFTER, LOOP_TARGET
+    ctx_lens, B, g, H, V, T = [40, 75], 2, sd.gamma, sd.hidden, sd.vocab, 1.0
+    nf = len(FEAT_LAYERS)
+    wd = synth.make_weights(sd, seed=41, gain_jitter=0.1, ar_e_std=1.0, ar_w_std=0.3)
+    wt = synth.make_target_weights(st_, seed=42, gain_jitter=0.1)
+    wf = synth.make_fusion_weights(sd, n_feat=nf, seed=43, gain_jitter=0.1)
+    wl = synth.Workload("sloop", sd, batch=B, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=44)
+    ri = synth.make_round(wl, ctx_lens=ctx_lens)
+    dr = DeviceRound(sd, wd, ri, ctx_cap=256)
+    tk, tv = synth.make_target_cache(st_, ctx_lens, seed=45)
+    t = D.DeviceTarget(st_, wt)
+    tctx = D.DeviceContext(st_, B, 256)
+    upload_cache(tctx, tk, tv, ctx_lens, torch.bfloat16)
+    tws = D.Workspace(t.cfg, B, 256, target=True)
+    fus = D.DeviceFusion(sd, wf, nf)
+    fws = torch.empty(D.dpara_fuse_workspace_bytes(fus.cfg, B * (g + 1), nf), dtype=torch.uint8, device="cuda")
+    hid = torch.empty((B, g + 1, nf, H), dtype=torch.bfloat16, device="cuda")
+    fused = torch.empty((B, g + 1, H), dtype=torch.bfloat16, device="cuda")
+    scores_in = torch.empty((B, g, V), dtype=torch.float32, device="cuda")
+    scores_out = torch.empty_like(scores_in)
+    feats = [np.asarray(f, np.float32) for f in ri.ctx_feats]
+    spine = ri.spine.astype(np.int32).copy()
+    s_ref = np.random.default_rng(46).standard_normal((B, g, V)).astype(np.float32)  # round 0's q
+    scores_in.copy_(torch.from_numpy(s_ref))
+    stats = {"verdicts": 0, "bonus": 0, "drafts": 0, "accepted": []}
+    for rnd in range(3):
+        seed = 1000 + rnd
+        dr.spine.copy_(torch.from_numpy(spine))
+        D.target_forward_hidden(t, tctx, dr.spine, dr.logits, FEAT_LAYERS, hid, tws)
+        dr.verify_sampled(scores_in, T, seed)
+        dr.backbone()
+        dr.head_sampled(T, seed, scores_out)
+        D.fuse_features(fus, hid.view(B * (g + 1), nf * H), fused.view(B * (g + 1), H), fws)
+        torch.cuda.synchronize()
+        assert dr.status() == 0
+        acc, bon, drafts = dr.accept.cpu().numpy(), dr.bonus.cpu().numpy(), dr.drafts.cpu().numpy()
+        sc_gpu = scores_out.cpu().numpy()
+        nxt, n_new, s_next = np.zeros_like(spine), np.zeros(B, np.int32), np.zeros((B, g, V), np.float32)
+        for b in range(B):
+            tl, th = O.target_forward(st_, wt, [tk[l][b] for l in range(st_.n_layers)],
+                                      [tv[l][b] for l in range(st_.n_layers)], spine[b], "bf16", FEAT_LAYERS)
+            r, bonus, info = O.verify_sampled(tl, s_ref[b], spine[b], T, seed, b)
+            if np.abs(info["accept_margins"]).min() > 2e-2:   # the GPU's logits and scores carry bf16 error
+                assert int(acc[b]) == r, (rnd, b, acc[b], r)
+                stats["verdicts"] += 1
+                if info["bonus_margin"] > 5e-2:
+                    assert int(bon[b]) == bonus, (rnd, b)
+                    stats["bonus"] += 1
+            stats["accepted"].append(int(acc[b]))
+            ref = O.backbone_all_boundaries(sd, wd, feats[b], spine[b], "bf16")["reps"]
+            hd = O.select_and_head_sampled(sd, wd, ref, r, bonus, T, seed, b, "bf16")
+            if (int(acc[b]), int(bon[b])) == (r, bonus):
+                for i in range(g):               # the oracle's own chain, up to its first near-tie
+                    if hd["margins"][i] <= 5e-2:
+                        break
+                    assert int(drafts[b, i]) == int(hd["drafts"][i]), (rnd, b, i)
+                    stats["drafts"] += 1
+                    # the score row the draw came from
+                    assert np.all(np.abs(sc_gpu[b, i] - hd["scores"][i]) <= 2e-2 + 2e-2 * np.abs(hd["scores"][i]))
+            k = r + 1
+            f_ref = O.fuse_features(sd, wf, th[:k].reshape(k, nf * H), "bf16")
+            feats[b] = np.concatenate([feats[b], f_ref.astype(np.float32)])
+            nxt[b], n_new[b], s_next[b] = hd["next_spine"], k, hd["scores"]
+        nn = torch.from_numpy(n_new).cuda()
+        dr.append(nn, fused)
+        # the next round's verification reads the scores of the block it verifies: the GPU's
+        # own when its block is the GPU's, else the oracle's (the loop follows the oracle)
+        same = [bool(np.array_equal(nxt[b], dr.next_spine[b].cpu().numpy())) for b in range(B)]
+        for b in range(B):
+            if not same[b]:
+                scores_out[b].copy_(torch.from_numpy(s_next[b]))
+        scores_in.copy_(scores_out)
+        s_ref, spine = s_next, nxt
+        _say(f"sampled round {rnd}: accepted {acc.tolist()} (oracle-driven), same next block {same}")
+    _say("iterated sampled rounds:", stats)
+    assert stats["verdicts"] >= 4 and stats["drafts"] >= 4
