@@ -464,13 +464,17 @@ def test_backbone_and_target_on_concurrent_streams():
 
 
 # ----------------------------------------------------------------------------- HIP graph of a round
-@pytest.mark.parametrize("case", ["h256_hd128_g5", "qwen3_8b_b1"])
+@pytest.mark.parametrize("case", ["h256_hd128_g5", "qwen3_8b_b1", "h256_hd128_g5_sampled", "qwen3_8b_b1_sampled"])
 def test_round_graph_replays(case):
     """One steady-state round (context rewind, append of the accepted rows' features,
     all-boundary backbone, greedy verify, select + head) captured into a HIP graph: every
     replay, with eager work that overwrites the outputs and synchronisations between the
     replays, gives the eager round's results bit for bit (the library takes all scratch from
-    the caller's workspace and launches only kernels on the caller's stream)."""
+    the caller's workspace and launches only kernels on the caller's stream).  The sampled
+    cases capture the sampling variant's verification and head instead (fixed seed and draft
+    scores), and also compare the scores the head writes."""
+    sampled = case.endswith("_sampled")
+    case = case[:-len("_sampled")] if sampled else case
     if case == "qwen3_8b_b1":
         wl = synth.WORKLOADS[case]
         w = synth.make_weights(wl.shape, seed=wl.seed_w)
@@ -488,13 +492,25 @@ def test_round_graph_replays(case):
     n_new = torch.from_numpy(n_new_h).cuda()
     base_len = torch.from_numpy((ri.ctx_lens - n_new_h).astype(np.int32)).cuda()
     outs = ("reps", "accept", "bonus", "targmax", "gathered", "drafts", "next_spine", "margins")
+    if sampled:
+        g_, V_ = wl.shape.gamma, wl.shape.vocab
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(5)
+        dr.scores_in = torch.randn((B, g_, V_), generator=gen, device="cuda", dtype=torch.float32)
+        dr.scores_out = torch.empty((B, g_, V_), dtype=torch.float32, device="cuda")
+        dr.targmax.zero_()  # not written by the sampled verification
+        outs = ("reps", "accept", "bonus", "gathered", "drafts", "next_spine", "margins", "scores_out")
 
     def step():
         dr.ctx.ctx_len[:B].copy_(base_len)
         dr.append(n_new)
         dr.backbone()
-        dr.verify()
-        dr.head()
+        if sampled:
+            dr.verify_sampled(dr.scores_in, 1.0, 1234)
+            dr.head_sampled(1.0, 1234, dr.scores_out)
+        else:
+            dr.verify()
+            dr.head()
 
     step()  # eager (also the first call of every launcher outside the capture)
     torch.cuda.synchronize()
@@ -522,7 +538,7 @@ def test_round_graph_replays(case):
         assert torch.equal(dr.ctx.ctx_len, ref_len)
         assert torch.equal(dr.ctx.k, ref_k) and torch.equal(dr.ctx.v, ref_v)
         assert dr.status() == 0
-    _say(case, "graph replays identical to the eager round: 4")
+    _say(case, "sampled" if sampled else "greedy", "graph replays identical to the eager round: 4")
 
 
 

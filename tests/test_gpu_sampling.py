@@ -56,6 +56,7 @@ VERIFY_CASES = {
     "v3001_bf16_t1": (6, 5, 3001, 1.0, "bf16"),     # odd vocabulary: element loads
     "v8192_f32_t07": (5, 7, 8192, 0.7, "f32"),      # 16-byte loads, temperature 0.7
     "v151936_bf16_t1": (2, 16, 151936, 1.0, "bf16"),  # Qwen3 vocabulary, draft length 16
+    "v1000_bf16_g63": (3, 63, 1000, 1.0, "bf16"),   # the longest draft the library takes
 }
 
 
