@@ -167,6 +167,10 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
     off += up256(bytes);
     return o;
   };
+  // The verification regions come first: their offsets depend only on (cfg, B), never on
+  // ctx_cap, so a verification may run beside the backbone on the same workspace.
+  p.vpart = take((size_t)B * (c->gamma + 1) * p.v_chunks * 8);
+  p.spart = take(verify_sampled_bytes(B, c->gamma, p.v_chunks));  // sampled verify: lse partials, bonus keys
   p.X = take(M * H * 4);
   p.A = take((p.afrag ? (M + 15) / 16 * 16 : M) * H * p.esz);
   p.QKV = take((size_t)p.s_qkv * M * (nq + 2 * nkv) * hd * 4);
@@ -179,7 +183,6 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   p.Hmid = take(M * (size_t)c->ffn * p.esz);
   p.P = take((size_t)(p.s_o > p.s_down ? p.s_o : p.s_down) * M * H * 4);  // O / down partial planes
   p.rope = take((size_t)B * (2 * c->gamma + 1) * (hd / 2) * 8);
-  p.vpart = take((size_t)B * (c->gamma + 1) * p.v_chunks * 8);
   p.G = take((size_t)B * c->gamma * H * 4);
   p.Gsplit = take((size_t)2 * B * c->gamma * H * 2);  // bf16 hi and lo planes of G
   p.logits = take((size_t)B * c->gamma * c->vocab * 4);
@@ -200,7 +203,6 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   const size_t crows = (size_t)B * (c->gamma + 1) * c->gamma;
   p.csplit = take(c->dtype == DPARA_BF16 ? 2 * crows * H * 2 : 0);
   p.cpart = take(c->dtype == DPARA_BF16 ? head_cand_part_bytes(B, c->gamma, c->vocab) : 0);
-  p.spart = take(verify_sampled_bytes(B, c->gamma, p.v_chunks));  // sampled verify: lse partials, bonus keys
   p.total = off;
   return p;
 }

@@ -463,6 +463,45 @@ def test_backbone_and_target_on_concurrent_streams():
         assert torch.equal(l1, l2)
 
 
+def test_verification_beside_backbone_on_one_workspace():
+    """Greedy and sampled verification on a second stream, concurrent with the backbone on the
+    same workspace (context capacity 512, so the backbone splits its attention over more key
+    ranges than a 64-capacity plan would): every output equals the sequential run's bit for bit."""
+    from paper_2609_27396_amd import dpara as D
+    DeviceRound = _harness()
+    shape, _ = SMALL_CASES["h256_hd128_g5"]
+    wl = synth.Workload("vb", shape, batch=3, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=15)
+    wd = synth.make_weights(shape, seed=16)
+    ri = synth.make_round(wl, ctx_lens=[300, 17, 450])
+    dr = DeviceRound(shape, wd, ri, ctx_cap=512)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(3)
+    scores = torch.randn((3, shape.gamma, shape.vocab), generator=gen, device="cuda", dtype=torch.float32)
+    acc2, bon2 = torch.empty_like(dr.accept), torch.empty_like(dr.bonus)
+
+    def verify_both(stream=None):
+        dr.verify(stream=stream)
+        D.verify_sampled(dr.d, dr.logits, scores, dr.spine, 1.0, 99, acc2, bon2, dr.ws, stream)
+
+    dr.backbone()
+    verify_both()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (dr.reps, dr.accept, dr.bonus, dr.targmax, acc2, bon2)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for _ in range(3):
+        for t in (dr.reps, dr.accept, dr.bonus, dr.targmax, acc2, bon2):
+            t.zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            dr.backbone(stream=s1)
+        with torch.cuda.stream(s2):
+            verify_both(stream=s2)
+        torch.cuda.synchronize()
+        for a_, b_ in zip(ref, (dr.reps, dr.accept, dr.bonus, dr.targmax, acc2, bon2)):
+            assert torch.equal(a_, b_)
+    assert dr.status() == 0
+
+
 # ----------------------------------------------------------------------------- HIP graph of a round
 @pytest.mark.parametrize("case", ["h256_hd128_g5", "qwen3_8b_b1", "h256_hd128_g5_sampled", "qwen3_8b_b1_sampled"])
 def test_round_graph_replays(case):
