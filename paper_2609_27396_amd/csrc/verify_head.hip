@@ -1,10 +1,11 @@
 // Greedy verification, branch gather and the Markov AR head.
 //
 // verify: per (row, vocab chunk) a workgroup reduces its slice to one packed 64-bit
-// (value, lowest index) key; one wave per request then takes each row's argmax g_j
-// (lane j), compares the drafts t_{j+1} with g_j, and a wave ballot of the mismatches
-// gives the accepted length r = index of the first mismatch (gamma if none) and the
-// bonus g_r (Section 2.1; Algorithm 1, Verify).
+// (value, lowest index) key; one workgroup per request then reduces each row's chunk keys
+// (one wave per row, one key per lane) to its argmax g_j, and one wave compares the
+// drafts t_{j+1} with g_j (lane j): a ballot of the mismatches gives the accepted length
+// r = index of the first mismatch (gamma if none) and the bonus g_r (Section 2.1;
+// Algorithm 1, Verify).
 //
 // Sampling variant: the acceptance test and bonus draw of speculative sampling (Section 2.1)
 // over log-sum-exp partials of the target and draft-score rows; the head steps rank
