@@ -196,7 +196,10 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
  * (seed mod 2^32, seed div 2^32); b is the request's index in the call's batch.  Tags: 1 head
  * draws (i = step, v = vocabulary id), 2 acceptance tests (i = draft index, v = 0), 3 bonus
  * draws (i = 0, v = vocabulary id).  A draw from softmax(x) is argmax_v x_v - log(-log U_v)
- * (Gumbel-max).  Callers pass a fresh seed per round; reusing one repeats the draws.
+ * (Gumbel-max).  Callers pass a fresh seed per round; reusing one repeats the draws.  With
+ * seed_dev non-NULL (device, one uint64, 8-byte aligned) the seed is read from there when the
+ * kernels run and `seed` is ignored: a captured graph then takes a fresh seed per replay from
+ * whatever the caller writes there between replays.
  *
  * dpara_select_and_head_sampled: dpara_select_and_head with y_i drawn from softmax(z_i / T)
  * (tag 1, step i) instead of argmax z_i; margins are top1 - top2 of z_i / T plus the noise.
@@ -221,12 +224,12 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
 int dpara_select_and_head_sampled(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
                                   const float* reps, const int32_t* accept_len, const int32_t* bonus,
                                   float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
-                                  float temperature, uint64_t seed, float* draft_scores, void* ws,
-                                  size_t ws_bytes, void* stream);
+                                  float temperature, uint64_t seed, const uint64_t* seed_dev,
+                                  float* draft_scores, void* ws, size_t ws_bytes, void* stream);
 int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* target_logits,
                          int32_t logits_dtype, const float* draft_scores, const int32_t* spine,
-                         float temperature, uint64_t seed, int32_t* accept_len, int32_t* bonus,
-                         void* ws, size_t ws_bytes, void* stream);
+                         float temperature, uint64_t seed, const uint64_t* seed_dev,
+                         int32_t* accept_len, int32_t* bonus, void* ws, size_t ws_bytes, void* stream);
 
 /* Head variant with every branch's base logits computed off the serial path (Algorithm 1
  * computes the base logits during Precompute).

@@ -211,6 +211,8 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
   }
 
   const int v0 = wg * ROWS_WG;
+  uint32_t sk0 = 0, sk1 = 0;
+  if constexpr (SAMPLE) sampling_key(smp, sk0, sk1);
   for (int s = 1; s <= gamma; ++s) {
     // this step's logits of the slice -> LDS by DMA (independent of y): LDS chunk c holds
     // request c / LCH, rows v0 + 4*(c % LCH) .. +3 (chunks past V re-read the last full
@@ -227,7 +229,7 @@ __global__ __launch_bounds__(64 * NW) void ar_head_persistent(int gamma, int V, 
 #pragma unroll 1
       for (int e = tid; e < B * ROWS_WG; e += 64 * NW) {
         const int v = v0 + e % ROWS_WG;
-        gs[e] = v < V ? rng_gumbel(smp.k0, smp.k1, kTagHead, e / ROWS_WG, s, v) : 0.f;
+        gs[e] = v < V ? rng_gumbel(sk0, sk1, kTagHead, e / ROWS_WG, s, v) : 0.f;
       }
     }
     if (s > 1) {

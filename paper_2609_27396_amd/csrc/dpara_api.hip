@@ -738,13 +738,15 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
 
 // Temperature and seed of the sampling variant: the generator's key is the seed's two
 // 32-bit halves.
-int make_sampling(float temperature, uint64_t seed, float* scores, Sampling* smp) {
+int make_sampling(float temperature, uint64_t seed, const uint64_t* seed_dev, float* scores, Sampling* smp) {
   if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(1.0f / temperature))
     return fail(DPARA_E_INVALID, "temperature must be positive and finite, got %g", (double)temperature);
+  if ((uintptr_t)seed_dev % 8 != 0) return fail(DPARA_E_INVALID, "seed_dev is not 8-byte aligned");
   smp->on = 1;
   smp->inv_t = 1.0f / temperature;
   smp->k0 = (uint32_t)(seed & 0xFFFFFFFFu);
   smp->k1 = (uint32_t)(seed >> 32);
+  smp->seed_dev = seed_dev;
   smp->scores = scores;
   return DPARA_OK;
 }
@@ -760,10 +762,10 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
 int dpara_select_and_head_sampled(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
                                   const float* reps, const int32_t* accept_len, const int32_t* bonus,
                                   float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
-                                  float temperature, uint64_t seed, float* draft_scores, void* ws, size_t ws_bytes,
-                                  void* stream) {
+                                  float temperature, uint64_t seed, const uint64_t* seed_dev, float* draft_scores,
+                                  void* ws, size_t ws_bytes, void* stream) {
   Sampling smp{};
-  const int rc = make_sampling(temperature, seed, draft_scores, &smp);
+  const int rc = make_sampling(temperature, seed, seed_dev, draft_scores, &smp);
   if (rc) return rc;
   return select_and_head_impl(cfg, w, batch, reps, accept_len, bonus, gathered, drafts, next_spine, margins, ws,
                               ws_bytes, stream, &smp);
@@ -771,7 +773,8 @@ int dpara_select_and_head_sampled(const dpara_config_t* cfg, const dpara_weights
 
 int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* target_logits, int32_t logits_dtype,
                          const float* draft_scores, const int32_t* spine, float temperature, uint64_t seed,
-                         int32_t* accept_len, int32_t* bonus, void* ws, size_t ws_bytes, void* stream) {
+                         const uint64_t* seed_dev, int32_t* accept_len, int32_t* bonus, void* ws, size_t ws_bytes,
+                         void* stream) {
   int rc = check_cfg(cfg);
   if (rc) return rc;
   if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
@@ -780,7 +783,7 @@ int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* t
   if (!target_logits || !draft_scores || !spine || !accept_len || !bonus)
     return fail(DPARA_E_INVALID, "target_logits, draft_scores, spine, accept_len and bonus must be non-NULL");
   Sampling smp{};
-  if ((rc = make_sampling(temperature, seed, nullptr, &smp))) return rc;
+  if ((rc = make_sampling(temperature, seed, seed_dev, nullptr, &smp))) return rc;
   const Plan p = make_plan(cfg, batch, 64);
   if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
@@ -788,7 +791,7 @@ int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* t
   if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
   if ((rc = check_device())) return rc;
   HIP_TRY(launch_verify_sampled(logits_dtype, batch, cfg->gamma, cfg->vocab, target_logits, draft_scores, spine,
-                                smp.inv_t, smp.k0, smp.k1, accept_len, bonus, at<void>(ws, p.spart), p.v_chunks,
+                                smp, accept_len, bonus, at<void>(ws, p.spart), p.v_chunks,
                                 p.v_chunk, at<int>(ws, 0), (hipStream_t)stream),
           "sampled verify");
   return DPARA_OK;

@@ -137,12 +137,25 @@ hipError_t launch_clear_status(int* status, hipStream_t st);
 // Sampled head (sampling variant): with on != 0 every head step scores s = z * inv_t, writes
 // s to scores[b][step-1][v] when scores is non-NULL, and ranks s + Gumbel(key; head tag, b,
 // step, v) instead of z; margins are then those of the perturbed scores.
+// The generator's key is (k0, k1), or the 64-bit seed at seed_dev read when the kernel runs
+// (so a captured graph can draw a fresh seed per replay).
 struct Sampling {
   int on;
   float inv_t;
   uint32_t k0, k1;
+  const uint64_t* seed_dev;
   float* scores;
 };
+__device__ __forceinline__ void sampling_key(const Sampling& s, uint32_t& k0, uint32_t& k1) {
+  if (s.seed_dev) {
+    const uint64_t v = *s.seed_dev;
+    k0 = (uint32_t)v;
+    k1 = (uint32_t)(v >> 32);
+  } else {
+    k0 = s.k0;
+    k1 = s.k1;
+  }
+}
 hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* logits,
                          const int* spine, int* accept_len, int* bonus, int* target_argmax,
                          uint64_t* part, int n_chunks, int chunk, int* status, hipStream_t st);
@@ -153,7 +166,7 @@ hipError_t launch_verify(int logits_dtype, int B, int gamma, int V, const void* 
 // from p_gamma.  verify_sampled_bytes gives the scratch bytes it needs.
 size_t verify_sampled_bytes(int B, int gamma, int n_chunks);
 hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, const void* logits, const float* scores,
-                                 const int* spine, float inv_t, uint32_t k0, uint32_t k1, int* accept_len,
+                                 const int* spine, const Sampling& smp, int* accept_len,
                                  int* bonus, void* scratch, int n_chunks, int chunk, int* status, hipStream_t st);
 // G (fp32, optional copy G_out) and its bf16 hi/lo split planes Ghi, Glo = Ghi + M*H.
 // Also zeroes n_clear uint64 words at `clear` (the persistent AR head's step tags).

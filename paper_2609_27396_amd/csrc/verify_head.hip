@@ -241,6 +241,8 @@ __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int r
   if (step > gamma) return;
   for (int k = threadIdx.x; k < rank; k += 256) e[k] = ld_f(E + (int64_t)y_prev * rank + k);
   __syncthreads();
+  uint32_t sk0 = 0, sk1 = 0;
+  if (smp.on) sampling_key(smp, sk0, sk1);
   const float* lrow = logits + ((int64_t)b * gamma + step - 1) * V;
   const int j = threadIdx.x & 7, grp = threadIdx.x >> 3;
   const int v0 = c * chunk, v1 = min(V, v0 + chunk);
@@ -256,7 +258,7 @@ __global__ __launch_bounds__(256) void ar_step(int step, int gamma, int V, int r
       if (smp.on) {
         z *= smp.inv_t;
         if (smp.scores) smp.scores[((int64_t)b * gamma + step - 1) * V + v] = z;
-        z += rng_gumbel(smp.k0, smp.k1, kTagHead, b, step, v);
+        z += rng_gumbel(sk0, sk1, kTagHead, b, step, v);
       }
       top2_merge(k1, v2, argmax_key(z, (uint32_t)v), -INFINITY);
     }
@@ -370,7 +372,9 @@ __global__ __launch_bounds__(256) void ar_step_pf(int step, int gamma, int V, in
   if (smp.on && j < NR && vmine < V) {
     zmine *= smp.inv_t;
     if (smp.scores) smp.scores[((int64_t)b * gamma + step - 1) * V + vmine] = zmine;
-    zmine += rng_gumbel(smp.k0, smp.k1, kTagHead, b, step, vmine);
+    uint32_t sk0, sk1;
+    sampling_key(smp, sk0, sk1);
+    zmine += rng_gumbel(sk0, sk1, kTagHead, b, step, vmine);
   }
   uint64_t k1 = (j < NR && vmine < V) ? argmax_key(zmine, (uint32_t)vmine) : 0;
   float v2 = -INFINITY;
@@ -507,9 +511,8 @@ __global__ __launch_bounds__(256) void lse_partial(const T* tl, const float* sc,
 template <typename T>
 __global__ __launch_bounds__(64 * kFinWaves) void spec_accept(int B, int gamma, int V, int n_chunks,
                                                               const float2* part, const T* tl, const float* sc,
-                                                              const int* spine, float inv_t, uint32_t k0,
-                                                              uint32_t k1, int* accept_len, float4* info,
-                                                              int* status) {
+                                                              const int* spine, Sampling smp, int* accept_len,
+                                                              float4* info, int* status) {
   __shared__ float lse[128];  // [0, gamma]: target rows; gamma + i: draft-score row of draft i
   const int b = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t trow0 = (int64_t)b * (gamma + 1);
@@ -534,7 +537,9 @@ __global__ __launch_bounds__(64 * kFinWaves) void spec_accept(int B, int gamma, 
       raise_status(status, 1);
       reject = true;
     } else {
-      const float lp = ld_f(tl + (trow0 + lane - 1) * V + t) * inv_t - lse[lane - 1];
+      uint32_t k0, k1;
+      sampling_key(smp, k0, k1);
+      const float lp = ld_f(tl + (trow0 + lane - 1) * V + t) * smp.inv_t - lse[lane - 1];
       const float lq = sc[((int64_t)b * gamma + lane - 1) * V + t] - lse[gamma + lane];
       const float u = rng_uniform(k0, k1, kTagAccept, b, lane, 0);
       reject = !(lp - lq - logf(u) > 0.f);
@@ -554,8 +559,8 @@ __global__ __launch_bounds__(64 * kFinWaves) void spec_accept(int B, int gamma, 
 constexpr int kBonusChunk = 1024;
 template <typename T>
 __global__ __launch_bounds__(256) void spec_bonus_partial(int gamma, int V, int n_bchunks, const T* tl,
-                                                          const float* sc, const float4* info, float inv_t,
-                                                          uint32_t k0, uint32_t k1, uint64_t* bpart) {
+                                                          const float* sc, const float4* info, Sampling smp,
+                                                          uint64_t* bpart) {
   constexpr int PER = kBonusChunk / 256;
   __shared__ uint64_t red[2][4];
   const int c = blockIdx.x, b = blockIdx.y;
@@ -570,6 +575,9 @@ __global__ __launch_bounds__(256) void spec_bonus_partial(int gamma, int V, int 
     x[k] = v < V ? ld_f(prow + v) : 0.f;
     y[k] = (qrow && v < V) ? qrow[v] : 0.f;
   }
+  uint32_t k0, k1;
+  sampling_key(smp, k0, k1);
+  const float inv_t = smp.inv_t;
   uint64_t kres = 0, kp = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -656,8 +664,9 @@ size_t verify_sampled_bytes(int B, int gamma, int n_chunks) {
 }
 
 hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, const void* logits, const float* scores,
-                                 const int* spine, float inv_t, uint32_t k0, uint32_t k1, int* accept_len,
+                                 const int* spine, const Sampling& smp, int* accept_len,
                                  int* bonus, void* scratch, int n_chunks, int chunk, int* status, hipStream_t st) {
+  const float inv_t = smp.inv_t;
   if (chunk != kLseChunk || n_chunks != (V + kLseChunk - 1) / kLseChunk || gamma > 63) return hipErrorInvalidValue;
   Phase ph("verify", st);
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -687,16 +696,16 @@ hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, cons
   const dim3 fin(64 * kFinWaves);
   if (logits_dtype == 1) {
     hipLaunchKernelGGL(spec_accept<bf16_t>, dim3(B), fin, 0, st, B, gamma, V, n_chunks, part, (const bf16_t*)logits,
-                       scores, spine, inv_t, k0, k1, accept_len, info, status);
+                       scores, spine, smp, accept_len, info, status);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(spec_bonus_partial<bf16_t>, dim3(n_bchunks, B), dim3(256), 0, st, gamma, V, n_bchunks,
-                       (const bf16_t*)logits, scores, info, inv_t, k0, k1, bpart);
+                       (const bf16_t*)logits, scores, info, smp, bpart);
   } else {
     hipLaunchKernelGGL(spec_accept<float>, dim3(B), fin, 0, st, B, gamma, V, n_chunks, part, (const float*)logits,
-                       scores, spine, inv_t, k0, k1, accept_len, info, status);
+                       scores, spine, smp, accept_len, info, status);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(spec_bonus_partial<float>, dim3(n_bchunks, B), dim3(256), 0, st, gamma, V, n_bchunks,
-                       (const float*)logits, scores, info, inv_t, k0, k1, bpart);
+                       (const float*)logits, scores, info, smp, bpart);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(spec_bonus_final, dim3(B), dim3(64), 0, st, gamma, n_bchunks, info, bpart, bonus);

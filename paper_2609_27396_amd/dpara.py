@@ -109,8 +109,8 @@ def lib():
         L.dpara_fuse_features.argtypes = [P(DparaConfig), P(DparaFusionWeights), I32, VP, VP, VP, SZ, VP]
         F32, U64 = ctypes.c_float, ctypes.c_uint64
         L.dpara_select_and_head_sampled.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP,
-                                                    VP, F32, U64, VP, VP, SZ, VP]
-        L.dpara_verify_sampled.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, F32, U64, VP, VP, VP, SZ, VP]
+                                                    VP, F32, U64, VP, VP, VP, SZ, VP]
+        L.dpara_verify_sampled.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, F32, U64, VP, VP, VP, VP, SZ, VP]
         L.dpara_last_error.restype = ctypes.c_char_p
         L.dpara_version.restype = I32
         L.dpara_profile_enable.argtypes = [I32]
@@ -369,23 +369,35 @@ def select_and_head(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts,
 
 
 def select_and_head_sampled(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts, next_spine, margins,
-                            temperature: float, seed: int, scores, ws: Workspace, stream=None):
+                            temperature: float, seed, scores, ws: Workspace, stream=None):
     """The sampled head: y_i ~ softmax(z_i / T) from the library's counter-based generator;
-    scores [B, gamma, V] float32 (or None) receives z_i / T."""
+    scores [B, gamma, V] float32 (or None) receives z_i / T.  seed: an int, or a one-element
+    int64 device tensor read when the kernels run."""
+    seed_dev, seed = _seed_args(seed)
     _check(lib().dpara_select_and_head_sampled(_ref(d.cfg), _ref(d.w), int(accept_len.shape[0]), _ptr(reps),
                                                _ptr(accept_len), _ptr(bonus), _ptr(gathered), _ptr(drafts),
-                                               _ptr(next_spine), _ptr(margins), float(temperature), int(seed),
-                                               _ptr(scores), ws.ptr, ws.nbytes, _stream(stream)))
+                                               _ptr(next_spine), _ptr(margins), float(temperature), seed,
+                                               seed_dev, _ptr(scores), ws.ptr, ws.nbytes, _stream(stream)))
 
 
-def verify_sampled(d: DeviceDrafter, logits, scores, spine, temperature: float, seed: int, accept_len, bonus,
+def _seed_args(seed):
+    """(seed_dev pointer, host seed) for an int or a one-element int64 device tensor."""
+    if isinstance(seed, int):
+        return 0, seed & 0xFFFFFFFFFFFFFFFF
+    assert seed.numel() == 1 and seed.element_size() == 8 and seed.is_cuda
+    return _ptr(seed), 0
+
+
+def verify_sampled(d: DeviceDrafter, logits, scores, spine, temperature: float, seed, accept_len, bonus,
                    ws: Workspace, stream=None):
     """Speculative-sampling verification: logits [B, gamma+1, V] (bf16 or float32), scores
-    [B, gamma, V] float32 (the drafts' tempered scores), spine [B, gamma+1] int32."""
+    [B, gamma, V] float32 (the drafts' tempered scores), spine [B, gamma+1] int32; seed as for
+    select_and_head_sampled."""
     import torch
+    seed_dev, seed = _seed_args(seed)
     ldt = DPARA_BF16 if logits.dtype == torch.bfloat16 else DPARA_F32
     _check(lib().dpara_verify_sampled(_ref(d.cfg), int(spine.shape[0]), _ptr(logits), ldt, _ptr(scores),
-                                      _ptr(spine), float(temperature), int(seed), _ptr(accept_len), _ptr(bonus),
+                                      _ptr(spine), float(temperature), seed, seed_dev, _ptr(accept_len), _ptr(bonus),
                                       ws.ptr, ws.nbytes, _stream(stream)))
 
 

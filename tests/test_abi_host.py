@@ -163,15 +163,16 @@ def test_sampling_validation_without_gpu():
     ws, nb = FAKE, D.dpara_workspace_bytes(cfg, 1, 64)
     for t in (0.0, -1.0, float("inf"), float("nan"), 1e-45):
         rc = _rc("dpara_select_and_head_sampled", R(cfg), R(w), 1, FAKE, FAKE, FAKE, None, FAKE, FAKE, None,
-                 t, 1, None, ws, nb, None)
+                 t, 1, None, None, ws, nb, None)
         assert rc == D.DPARA_E_INVALID, t
         assert "temperature" in D.dpara_last_error()
-        rc = _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, t, 1, FAKE, FAKE, ws, nb, None)
+        rc = _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, t, 1, None, FAKE, FAKE, ws, nb,
+                 None)
         assert rc == D.DPARA_E_INVALID, t
-    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, None, FAKE, 1.0, 1, FAKE, FAKE, ws, nb,
+    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, None, FAKE, 1.0, 1, None, FAKE, FAKE, ws, nb,
                None) == D.DPARA_E_INVALID
     assert "draft_scores" in D.dpara_last_error()
-    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, 7, FAKE, FAKE, 1.0, 1, FAKE, FAKE, ws, nb,
+    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, 7, FAKE, FAKE, 1.0, 1, None, FAKE, FAKE, ws, nb,
                None) == D.DPARA_E_UNSUPPORTED
-    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, 1.0, 1, FAKE, FAKE, ws, 1024,
+    assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, 1.0, 1, None, FAKE, FAKE, ws, 1024,
                None) == D.DPARA_E_WORKSPACE

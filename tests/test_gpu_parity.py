@@ -510,8 +510,9 @@ def test_round_graph_replays(case):
     replay, with eager work that overwrites the outputs and synchronisations between the
     replays, gives the eager round's results bit for bit (the library takes all scratch from
     the caller's workspace and launches only kernels on the caller's stream).  The sampled
-    cases capture the sampling variant's verification and head instead (fixed seed and draft
-    scores), and also compare the scores the head writes."""
+    cases capture the sampling variant's verification and head instead, with the seed read
+    from device memory: replays alternate two seeds written there between replays, and each
+    replay matches the eager round with that seed (scores the head writes included)."""
     sampled = case.endswith("_sampled")
     case = case[:-len("_sampled")] if sampled else case
     if case == "qwen3_8b_b1":
@@ -539,22 +540,31 @@ def test_round_graph_replays(case):
         dr.scores_out = torch.empty((B, g_, V_), dtype=torch.float32, device="cuda")
         dr.targmax.zero_()  # not written by the sampled verification
         outs = ("reps", "accept", "bonus", "gathered", "drafts", "next_spine", "margins", "scores_out")
+        seeds = (1234, 987654321987)
+        seed_t = torch.tensor([seeds[0]], dtype=torch.int64, device="cuda")
 
     def step():
         dr.ctx.ctx_len[:B].copy_(base_len)
         dr.append(n_new)
         dr.backbone()
         if sampled:
-            dr.verify_sampled(dr.scores_in, 1.0, 1234)
-            dr.head_sampled(1.0, 1234, dr.scores_out)
+            dr.verify_sampled(dr.scores_in, 1.0, seed_t)
+            dr.head_sampled(1.0, seed_t, dr.scores_out)
         else:
             dr.verify()
             dr.head()
 
-    step()  # eager (also the first call of every launcher outside the capture)
-    torch.cuda.synchronize()
-    assert dr.status() == 0
-    ref = {k: getattr(dr, k).clone() for k in outs}
+    refs = []
+    for sd in (seeds if sampled else (None,)):
+        if sampled:
+            seed_t.fill_(sd)
+        step()  # eager (also the first call of every launcher outside the capture)
+        torch.cuda.synchronize()
+        assert dr.status() == 0
+        refs.append({k: getattr(dr, k).clone() for k in outs})
+    if sampled:
+        assert not torch.equal(refs[0]["drafts"], refs[1]["drafts"])  # the seed reaches the draws
+    ref = refs[-1]
     ref_len = dr.ctx.ctx_len.clone()
     ref_k, ref_v = dr.ctx.k.clone(), dr.ctx.v.clone()
     g = torch.cuda.CUDAGraph()
@@ -565,6 +575,9 @@ def test_round_graph_replays(case):
             step()
     torch.cuda.synchronize()
     for rep in range(4):
+        if sampled:
+            seed_t.fill_(seeds[rep % 2])
+            ref = refs[rep % 2]
         for k in outs:  # eager work between the replays
             t = getattr(dr, k)
             t.fill_(-7 if t.dtype == torch.int32 else float("nan"))
