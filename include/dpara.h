@@ -11,6 +11,14 @@
  *   dpara_select_and_head          select branch r, AR head y_i = argmax(l_i + W E(y_{i-1})),
  *                                  y_0 = b; next block (b, y_1..y_d) (Algorithm 1; the head
  *                                  equation of Section 3.2)
+ * Around it:
+ *   dpara_branch_candidates, dpara_select_and_head_cand   the head with every branch's base
+ *                                  logits scored off the serial path (Algorithm 1, Precompute)
+ *   dpara_verify_sampled, dpara_select_and_head_sampled   the sampling variant: speculative-
+ *                                  sampling acceptance and y_i ~ softmax(z_i / T) (Section 2.1)
+ *   dpara_target_forward[_hidden]  a verifying target on the same GPU (Section 4.3.2), also
+ *                                  emitting the hidden states the drafter fuses
+ *   dpara_fuse_features            C_new = RMSNorm(fc [h_1; ...; h_n]) (Section 3.2)
  * "d" in the paper is `gamma` here (draft length; gamma+1 boundaries).
  *
  * Conventions shared by every call:
@@ -29,7 +37,9 @@
  *  - dtype (DPARA_F32 or DPARA_BF16) applies to matrices, embeddings, context features
  *    and the K/V cache; norm gains are always float32; the residual stream, the
  *    representations, logits and softmax are float32 in both modes.
- *  - Calls on one workspace must not overlap (same stream, or ordered by events).
+ *  - Calls on one workspace must not overlap (same stream, or ordered by events), with one
+ *    exception: a verification (dpara_verify_greedy or dpara_verify_sampled) may run on
+ *    another stream beside dpara_ctx_append and dpara_backbone_all_boundaries.
  */
 #ifndef DPARA_H
 #define DPARA_H
