@@ -287,3 +287,79 @@ def test_iterated_sampled_rounds():
         _say(f"sampled round {rnd}: accepted {acc.tolist()} (oracle-driven), same next block {same}")
     _say("iterated sampled rounds:", stats)
     assert stats["verdicts"] >= 4 and stats["drafts"] >= 4
+
+
+def _freq_ok(counts, p, sig=5.0):
+    n = counts.sum()
+    f = counts / n
+    return np.all(np.abs(f - p) <= sig * np.sqrt(p * (1 - p) / n) + 1.0 / n)
+
+
+def test_verify_sampled_preserves_target_distribution():
+    """The GPU's own draws, as a distribution: 4096 requests share one target and draft
+    distribution (each request index is its own random stream), drafts drawn from q; the first
+    and second emitted tokens follow p_0 and p_1 and t_1 is accepted at rate sum min(p, q)."""
+    from paper_2609_27396_amd import dpara as D
+    B, gamma, V, T = 4096, 2, 8, 1.0
+    shape = synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
+                               vocab=V, gamma=gamma, ar_rank=64, qk_norm=True, dtype="bf16")
+    cfg = D.make_config(shape)
+    d = types.SimpleNamespace(cfg=cfg)
+    ws = D.Workspace(cfg, B, 64)
+    rng = np.random.default_rng(17)
+    L1 = rng.standard_normal((gamma + 1, V)).astype(np.float32) * 1.5
+    S1 = rng.standard_normal((gamma, V)).astype(np.float32) * 1.5
+    p = [np.exp(L1[j] - L1[j].max()) / np.exp(L1[j] - L1[j].max()).sum() for j in range(gamma + 1)]
+    q = [np.exp(S1[j] - S1[j].max()) / np.exp(S1[j] - S1[j].max()).sum() for j in range(gamma)]
+    spine = np.zeros((B, gamma + 1), np.int32)
+    for i in range(gamma):
+        spine[:, i + 1] = rng.choice(V, size=B, p=q[i])
+    L = np.ascontiguousarray(np.broadcast_to(L1, (B, gamma + 1, V)))
+    S = np.ascontiguousarray(np.broadcast_to(S1, (B, gamma, V)))
+    acc = torch.empty(B, dtype=torch.int32, device="cuda")
+    bon = torch.empty(B, dtype=torch.int32, device="cuda")
+    D.verify_sampled(d, torch.from_numpy(L).cuda(), torch.from_numpy(S).cuda(), torch.from_numpy(spine).cuda(), T,
+                     31337, acc, bon, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    r, b = acc.cpu().numpy(), bon.cpu().numpy()
+    e1 = np.where(r >= 1, spine[:, 1], b)
+    e2 = np.where(r >= 2, spine[:, 2], b)[r >= 1]
+    assert _freq_ok(np.bincount(e1, minlength=V), p[0])
+    assert _freq_ok(np.bincount(e2, minlength=V), p[1])
+    a = float(np.minimum(p[0], q[0]).sum())
+    assert abs((r >= 1).mean() - a) <= 5 * np.sqrt(a * (1 - a) / B)
+    _say(f"acceptance of t_1 {(r >= 1).mean():.4f} (sum min(p, q) = {a:.4f}); mean accepted {r.mean():.3f}")
+
+
+@pytest.mark.parametrize("batch", [16, 512])
+def test_head_sampled_draws_follow_softmax(batch):
+    """With the head's correction matrix W zero, each sampled step is a plain draw from
+    softmax(l_i / T): over many requests (16: the single-launch head; 512: the step kernels)
+    the draws of every step follow it."""
+    from paper_2609_27396_amd import dpara as D
+    shape = synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=2, n_kv_heads=1, head_dim=128, ffn=512,
+                               vocab=64, gamma=3, ar_rank=64, qk_norm=True, dtype="bf16")
+    w = synth.make_weights(shape, seed=8, weight_std=0.1)
+    w["ar_W"] = np.zeros_like(w["ar_W"])
+    dd = D.DeviceDrafter(shape, w)
+    B, g, H, V, T = batch, shape.gamma, shape.hidden, shape.vocab, 0.8
+    ws = D.Workspace(dd.cfg, B, 64)
+    rows = np.random.default_rng(9).standard_normal((g, H)).astype(np.float32)
+    reps = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(rows, (B, g + 1, g, H)))).cuda()
+    acc = torch.zeros(B, dtype=torch.int32, device="cuda")
+    bon = torch.zeros(B, dtype=torch.int32, device="cuda")
+    drafts = torch.empty((B, g), dtype=torch.int32, device="cuda")
+    nsp = torch.empty((B, g + 1), dtype=torch.int32, device="cuda")
+    counts = np.zeros((g, V))
+    for seed in range(4096 // B if B < 4096 else 1):
+        D.select_and_head_sampled(dd, reps, acc, bon, None, drafts, nsp, None, T, seed, None, ws)
+        dh = drafts.cpu().numpy()
+        for i in range(g):
+            counts[i] += np.bincount(dh[:, i], minlength=V)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    ell = O.base_logits(w, rows, "bf16") / T
+    for i in range(g):
+        pz = np.exp(ell[i] - ell[i].max())
+        assert _freq_ok(counts[i], pz / pz.sum()), i
