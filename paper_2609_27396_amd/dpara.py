@@ -327,6 +327,7 @@ class Workspace:
         if self.nbytes == 0:
             raise DparaError(DPARA_E_INVALID, "invalid configuration for workspace sizing")
         self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+        self.buf[:256].zero_()  # the header (status word, head flag) starts clear
 
     @property
     def ptr(self) -> int:
