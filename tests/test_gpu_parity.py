@@ -126,6 +126,14 @@ SMALL_CASES = {
     "h512_hd64_g3": (synth.DrafterShape(n_layers=1, hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=64, ffn=640,
                                         vocab=1000, gamma=3, ar_rank=128, qk_norm=False, dtype="bf16"),
                      [64, 129]),
+    # the shortest draft: two boundaries
+    "h256_g1": (synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
+                                   vocab=2000, gamma=1, ar_rank=64, qk_norm=True, dtype="bf16"),
+                [0, 50, 7]),
+    # the longest draft the library takes: 64 boundaries, 4096 block rows per request
+    "h256_g63": (synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
+                                    vocab=2000, gamma=63, ar_rank=64, qk_norm=True, dtype="bf16"),
+                 [100, 3]),
     # float32 model with several tiles, hd 128
     "f32_h256_g7": (synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=1, head_dim=128, ffn=320,
                                        vocab=3001, gamma=7, ar_rank=64, qk_norm=True, dtype="f32"),
