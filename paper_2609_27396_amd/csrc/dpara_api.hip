@@ -117,7 +117,7 @@ struct Plan {
   bool afrag;              // normed activations in MFMA fragment order (QKV and gate/up GEMMs)
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
-      hflag, F, KV32, rope_app, csplit, cpart, spart;
+      hflag, F, KV32, rope_app, csplit, cpart, spart, plogits, erows;
   int ar_grid;  // persistent AR head grid (0: step kernels only)
   size_t total;
 };
@@ -203,6 +203,8 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   const size_t crows = (size_t)B * (c->gamma + 1) * c->gamma;
   p.csplit = take(c->dtype == DPARA_BF16 ? 2 * crows * H * 2 : 0);
   p.cpart = take(c->dtype == DPARA_BF16 ? head_cand_part_bytes(B, c->gamma, c->vocab) : 0);
+  p.plogits = take((size_t)B * c->gamma * c->vocab * 4);  // sampled head: perturbed logits
+  p.erows = take((size_t)B * c->gamma * c->ar_rank * p.esz);  // sampled head: E rows of the previous tokens
   p.total = off;
   return p;
 }
@@ -715,10 +717,28 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
     HIP_TRY(launch_gemm(bf ? A_BF16_DUAL : A_F32, EPI_STORE_F32, lm, st), "lm head gemm");
   }
   if (smp) {
+    // Exact bound-pruned steps over the perturbed logits first; the full sampled head runs only
+    // if some step is not proven (it then writes the scores itself), else the scores kernel does.
+    int* hflag = at<int>(ws, p.hflag);
+    hipError_t pe = hipErrorNotSupported;
+    if (head_prune_supported(cfg->dtype, g, V, cfg->ar_rank)) {
+      HIP_TRY(launch_perturb_logits(batch, g, V, at<float>(ws, p.logits), at<float>(ws, p.plogits), *smp, st),
+              "perturbed logits");
+      pe = launch_head_pruned(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.plogits), w->ar_E, w->ar_W,
+                              bonus, drafts, next_spine, margins, at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart),
+                              hflag, status, st, smp->inv_t);
+      if (pe != hipSuccess && pe != hipErrorNotSupported) return hip_fail(pe, "sampled pruned head");
+    }
     HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                            drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
-                           p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status, nullptr, st, *smp),
+                           p.ar_grid ? at<uint64_t>(ws, p.arpart) : nullptr, p.ar_grid, status,
+                           pe == hipSuccess ? hflag : nullptr, st, *smp),
             "sampled ar head");
+    if (pe == hipSuccess && smp->scores)
+      HIP_TRY(launch_draft_scores(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W,
+                                  bonus, drafts, *smp, hflag, at<void>(ws, p.erows), at<float>(ws, p.plogits),
+                                  at<int>(ws, 8), st),
+              "draft scores");
     return DPARA_OK;
   }
   // Exact bound-pruned steps first; the full head then runs only if some step could not be

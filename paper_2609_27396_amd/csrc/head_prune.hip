@@ -33,6 +33,8 @@
 // (larger value wins, the lower index on ties), as in the full head.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -331,7 +333,7 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
                                                  const float* wpart, int n_wpart, const T* E, const T* W,
                                                  const int* bonus, int* drafts, int* next_spine, float* margins,
                                                  int* flag, int* status, const int* accept_len,
-                                                 const int* pre_flag) {
+                                                 const int* pre_flag, float inv_t) {
   constexpr int EPT = RANK / 16;
   constexpr int D = 4;  // steps of candidate rows in flight, in registers
   __shared__ uint64_t lists[16][kMaxSplits * kKeys];  // the split lists of 16 rows in flight
@@ -389,6 +391,9 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
   }
   if (stop) return;
   const float wmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * (1.0f + 1e-5f);
+  // the sampled head ranks l / T + G + (W_v . e) / T: the correction and its bound scale by 1/T
+  // (exactly 1 for the greedy head)
+  const float wmax_t = wmax * inv_t;
 
   // Step s's (1-based) candidate rows; steps past gamma reload step gamma's (in bounds,
   // never used).  Candidate indices are clamped into the vocabulary (keys of a complete
@@ -418,7 +423,7 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
       d = row16_sum(d);
       ee = row16_sum(ee);
       const uint64_t key = ck[i - 1][kc];
-      if (slice == 0) zs[kc] = key ? key_value(key) + d : -INFINITY;  // fewer than kTopK candidates
+      if (slice == 0) zs[kc] = key ? key_value(key) + d * inv_t : -INFINITY;  // fewer than kTopK candidates
       __syncthreads();
       if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
         uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
@@ -429,7 +434,7 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
         top2_merge(k1, v2, dpp_u64<kDppMirror>(k1), dpp_f<kDppMirror>(v2));
         if (tid == 0) {
           const float lb = key_value(ck[i - 1][kTopK]);
-          const float bound = lb + wmax * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
+          const float bound = lb + wmax_t * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
           const bool ok = v2 > bound;
           const int y = (int)key_index(k1);
           if (ok) {
@@ -454,15 +459,51 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
   }
 }
 
+// Perturbed head logits of the sampling variant: P[row][v] = l[row][v] * inv_t + G, with G
+// the Gumbel noise of head step i = row % gamma + 1 of request row / gamma (the same draw the
+// full sampled head adds).
+__global__ __launch_bounds__(256) void perturb_logits(int gamma, int V, const float* L, float* P, Sampling smp) {
+  const int row = blockIdx.y, b = row / gamma, i = row % gamma + 1;
+  uint32_t k0, k1;
+  sampling_key(smp, k0, k1);
+  const int64_t o = (int64_t)row * V;
+  for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += gridDim.x * 256)
+    P[o + v] = L[o + v] * smp.inv_t + rng_gumbel(k0, k1, kTagHead, b, i, v);
+}
+
+// Draft scores once the drafts are known, as a GEMM: the previous tokens' E rows
+// (row b * gamma + i - 1 holds E(y_{i-1}), y_0 the bonus) times W^T, then
+// s = (l + c) * inv_t.  The gather also turns the pruned head's fallback flag into `ok`
+// (1 when every step was proven: the full head, when it runs, writes the scores itself); c
+// goes to scratch and only the finishing pass, which checks ok, writes the scores.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_prev_e(int gamma, int V, int rank, const T* E, const int* bonus,
+                                                     const int* drafts, T* rows, const int* flag, int* ok) {
+  const int row = blockIdx.x, b = row / gamma, i = row % gamma;  // row's step i + 1 reads y_i
+  if (row == 0 && threadIdx.x == 0) *ok = (*flag == 0) ? 1 : 0;
+  int y = i == 0 ? bonus[b] : drafts[b * gamma + i - 1];
+  y = min(max(y, 0), V - 1);
+  for (int k = threadIdx.x; k < rank; k += 256) rows[(int64_t)row * rank + k] = E[(int64_t)y * rank + k];
+}
+
+__global__ __launch_bounds__(256) void finish_scores(int64_t n, const float* L, const float* C, float* S, float inv_t,
+                                                     const int* ok) {
+  if (*ok == 0) return;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
+    const float z = L[e] + C[e];
+    S[e] = z * inv_t;
+  }
+}
+
 }  // namespace
 
 template <typename T, int RANK>
 hipError_t launch_pruned(int B, int gamma, int V, int S, const uint64_t* cand, const float* wpart, int nw,
                          const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
                          float* margins, int* flag, int* status, const int* accept_len, const int* pre_flag,
-                         hipStream_t st) {
+                         float inv_t, hipStream_t st) {
   hipLaunchKernelGGL((ar_pruned<T, RANK>), dim3(B), dim3(256), 0, st, gamma, V, S, cand, wpart, nw, (const T*)E,
-                     (const T*)W, bonus, drafts, next_spine, margins, flag, status, accept_len, pre_flag);
+                     (const T*)W, bonus, drafts, next_spine, margins, flag, status, accept_len, pre_flag, inv_t);
   return hipGetLastError();
 }
 
@@ -486,10 +527,10 @@ hipError_t launch_wnorm(int dtype, int rank, const void* W, int V, float* wpart,
 hipError_t dispatch_pruned(int dtype, int rank, int B, int gamma, int V, int S, const uint64_t* cand,
                            const float* wpart, int nw, const void* E, const void* W, const int* bonus, int* drafts,
                            int* next_spine, float* margins, int* flag, int* status, const int* accept_len,
-                           const int* pre_flag, hipStream_t st) {
+                           const int* pre_flag, float inv_t, hipStream_t st) {
 #define DPARA_PRUNED(TT, RK)                                                                                   \
   return launch_pruned<TT, RK>(B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag, \
-                               status, accept_len, pre_flag, st)
+                               status, accept_len, pre_flag, inv_t, st)
   if (dtype == 1) {
     if (rank == 64) DPARA_PRUNED(bf16_t, 64);
     if (rank == 128) DPARA_PRUNED(bf16_t, 128);
@@ -555,7 +596,7 @@ hipError_t launch_head_from_candidates(int B, int gamma, int V, int rank, const 
   hipError_t e = launch_clear_status(flag, st);
   if (e != hipSuccess) return e;
   return dispatch_pruned(1, rank, B, gamma, V, 1, keys, wpart, head_prune_wparts(), E, W, bonus, drafts, next_spine,
-                         margins, flag, status, accept_len, overflow, st);
+                         margins, flag, status, accept_len, overflow, 1.0f, st);
 }
 
 bool head_prune_supported(int dtype, int gamma, int V, int rank) {
@@ -567,7 +608,7 @@ size_t head_prune_cand_bytes(int rows, int V) { return (size_t)rows * head_prune
 
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st) {
+                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st, float inv_t) {
   if (!head_prune_supported(dtype, gamma, V, rank) || B < 1) return hipErrorNotSupported;
   const int rows = B * gamma;
   const int S = head_prune_splits(rows, V);
@@ -580,7 +621,44 @@ hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, cons
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return dispatch_pruned(dtype, rank, B, gamma, V, S, cand, wpart, nw, E, W, bonus, drafts, next_spine, margins, flag,
-                         status, nullptr, nullptr, st);
+                         status, nullptr, nullptr, inv_t, st);
+}
+
+hipError_t launch_perturb_logits(int B, int gamma, int V, const float* logits, float* P, const Sampling& smp,
+                                 hipStream_t st) {
+  const int gx = min((V + 255) / 256, 64);
+  hipLaunchKernelGGL(perturb_logits, dim3(gx, B * gamma), dim3(256), 0, st, gamma, V, logits, P, smp);
+  return hipGetLastError();
+}
+
+hipError_t launch_draft_scores(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
+                               const void* W, const int* bonus, const int* drafts, const Sampling& smp,
+                               const int* flag, void* rows, float* cbuf, int* ok, hipStream_t st) {
+  const int R = B * gamma;
+  if (dtype == 1)
+    hipLaunchKernelGGL(gather_prev_e<bf16_t>, dim3(R), dim3(256), 0, st, gamma, V, rank, (const bf16_t*)E, bonus,
+                       drafts, (bf16_t*)rows, flag, ok);
+  else
+    hipLaunchKernelGGL(gather_prev_e<float>, dim3(R), dim3(256), 0, st, gamma, V, rank, (const float*)E, bonus,
+                       drafts, (float*)rows, flag, ok);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  GemmArgs g{};
+  g.A = rows;
+  g.lda = rank;
+  g.B0 = g.B1 = g.B2 = W;
+  g.n1 = g.n2 = V;
+  g.M = R;
+  g.N = V;
+  g.K = rank;
+  g.C = cbuf;
+  g.ldc = V;
+  g.only_if = ok;  // (kernels that ignore it only waste work: the finishing pass checks ok)
+  if ((e = launch_gemm(dtype == 1 ? A_BF16 : A_F32, EPI_STORE_F32, g, st)) != hipSuccess) return e;
+  const int64_t n = (int64_t)R * V;
+  const int grid = (int)std::min<int64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(finish_scores, dim3(grid), dim3(256), 0, st, n, logits, cbuf, smp.scores, smp.inv_t, ok);
+  return hipGetLastError();
 }
 
 }  // namespace dpara

@@ -203,7 +203,19 @@ int head_prune_wparts();
 size_t head_prune_cand_bytes(int rows, int V);
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st);
+                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st,
+                              float inv_t = 1.0f);
+// Sampled head through the pruned steps: P = l * inv_t + Gumbel(key; head tag, b, i, v) for
+// every head row (row b * gamma + i - 1), ranked by launch_head_pruned(..., P, inv_t); then,
+// where the pruned steps decided every step (*flag == 0), the draft scores
+// s_i = (l_i + W E(y_{i-1})) * inv_t of every vocabulary entry from the drafts now known, as a
+// GEMM over the gathered E rows (`rows`: B * gamma * rank elements of the drafter dtype;
+// `cbuf`: B * gamma * V floats of scratch; `ok`: one int of scratch).
+hipError_t launch_perturb_logits(int B, int gamma, int V, const float* logits, float* P, const Sampling& smp,
+                                 hipStream_t st);
+hipError_t launch_draft_scores(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
+                               const void* W, const int* bonus, const int* drafts, const Sampling& smp,
+                               const int* flag, void* rows, float* cbuf, int* ok, hipStream_t st);
 // Candidates of every branch row, off the serial path (bf16): reps [B, gamma+1, gamma, H]
 // fp32 -> `cand` (head_cand_bytes: a 4 KB header with an overflow flag at 0 and the
 // |W_v|^2 maxima at byte 256, then kTopK+1 keys per row); `split` holds 2 * rows * H bf16,

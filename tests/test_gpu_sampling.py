@@ -155,12 +155,17 @@ def _check_head_sampled(shape, w, dr, scores, T, seed, mode):
 
 
 HEAD_CASES = {
-    # bf16, rank 64, 3 requests: the persistent head
-    "bf16_persistent": ("h256_hd128_g5", [0, 77, 300], 1.0),
+    # (shape, contexts, temperature, std of the head's W).  A large W defeats the pruned steps'
+    # bound, so the full sampled head runs: bf16, rank 64, 3 requests: the single-launch head
+    "bf16_persistent": ("h256_hd128_g5", [0, 77, 300], 1.0, 0.3),
     # bf16, 18 requests (more than one persistent launch holds): the step kernels
-    "bf16_steps_b18": ("h256_hd128_g5", [5 * i for i in range(18)], 0.8),
+    "bf16_steps_b18": ("h256_hd128_g5", [5 * i for i in range(18)], 0.8, 0.3),
     # float32 model: the step kernels
-    "f32_steps": ("f32_h256_g7", [33, 150], 1.0),
+    "f32_steps": ("f32_h256_g7", [33, 150], 1.0, 0.3),
+    # a small W: every step is proven over the perturbed logits' candidates, and the scores
+    # come from the scores kernel
+    "bf16_pruned": ("h256_hd128_g5", [0, 77, 300], 1.0, 0.005),
+    "f32_pruned": ("f32_h256_g7", [33, 150], 0.7, 0.005),
 }
 
 
@@ -168,13 +173,13 @@ HEAD_CASES = {
 def test_head_sampled_parity(case):
     from test_gpu_parity import SMALL_CASES
     from paper_2609_27396_amd.harness import DeviceRound
-    name, ctx, T = HEAD_CASES[case]
+    name, ctx, T, w_std = HEAD_CASES[case]
     shape = SMALL_CASES[name][0]
     mode = shape.dtype
     _say("case", case)
     wl = synth.Workload("hs", shape, batch=len(ctx), ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=21,
                         logits_dtype="bf16" if mode == "bf16" else "f32")
-    w = synth.make_weights(shape, seed=22, gain_jitter=0.1, ar_e_std=1.0, ar_w_std=0.3)
+    w = synth.make_weights(shape, seed=22, gain_jitter=0.1, ar_e_std=1.0, ar_w_std=w_std)
     ri = synth.make_round(wl, ctx_lens=ctx)
     dr = DeviceRound(shape, w, ri)
     dr.backbone()
@@ -182,9 +187,11 @@ def test_head_sampled_parity(case):
     scores = torch.empty((len(ctx), shape.gamma, shape.vocab), dtype=torch.float32, device="cuda")
     total = 0
     for seed in (5, 77):
+        scores.fill_(float("nan"))
         dr.head_sampled(T, seed, scores)
         torch.cuda.synchronize()
         assert dr.status() == 0
+        assert (dr.head_fallback() != 0) == (w_std > 0.1), dr.head_fallback()  # which path ran
         compared = _check_head_sampled(shape, w, dr, scores, T, seed, mode)
         total += len(ctx) * shape.gamma
         _say(f"{case} seed {seed}: drafts {dr.drafts.cpu().numpy().tolist()[:3]}, compared {compared}")
