@@ -215,7 +215,12 @@ int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, i
  * (tag 1, step i) instead of argmax z_i; margins are top1 - top2 of z_i / T plus the noise.
  * draft_scores: [batch, gamma, vocab] float32 (device, may be NULL): s_i = z_i / T, the
  * tempered scores each draft was drawn from (the input of dpara_verify_sampled in the next
- * round).  The bound-pruned steps do not apply; the full head runs (same launch rules).
+ * round).  As in the greedy head, the steps first run exactly over candidates: the 16 largest
+ * of l_i / T + G_i (the noise is known before the steps) against the bound
+ * max_v |ar_W[v]| |ar_E[y_{i-1}]| / T; if every step is proven, draft_scores come from one GEMM
+ * over the drafts now known, else the int32 at byte offset 4 of `ws` is left nonzero and the
+ * full head (same launch rules as dpara_select_and_head) recomputes every request and writes
+ * the scores; the draws are the same either way up to float32 rounding.
  *
  * dpara_verify_sampled: speculative-sampling verification of the block t_0..t_gamma.
  * target_logits: [batch, gamma+1, vocab] (device, logits_dtype DPARA_F32 or DPARA_BF16,
