@@ -98,6 +98,7 @@ def full_round(args, wl):
     weights = synth.make_weights(shape, seed=wl.seed_w)
     ri = synth.make_round(wl)
     dr = DeviceRound(shape, weights, ri)
+    prepare_head(dr)
     cap = dr.ctx_cap
     tgt = D.DeviceTarget(tshape, None, seed=100)
     tctx = D.DeviceContext(tshape, B, cap)
@@ -213,6 +214,13 @@ def recorded_traffic(kernel: str):
     if rec.get("kernel") != kernel or rec.get("source_sha256") != digest:
         return None
     return float(rec["bytes_per_launch"])
+
+
+def prepare_head(dr):
+    """Weight preparation at load time (outside every timed region): the AR head's max row
+    norm, a constant of the weights that the bound-pruned head steps use."""
+    if dr.shape.ar_rank in (64, 128, 256):
+        dr.d.prepare_head(dr.ws)
 
 
 def fuse_timing(shape, rows=(17, 2048), n_feat=3, iters=20):
@@ -341,6 +349,7 @@ def main():
     ri = synth.make_round(wl)
     log(f"[bench] inputs generated in {time.time() - t0:.1f} s")
     dr = DeviceRound(shape, weights, ri)
+    prepare_head(dr)
     torch.cuda.synchronize()
     log(f"[bench] weights resident, context prefilled ({time.time() - t0:.1f} s)")
 

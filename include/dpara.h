@@ -115,6 +115,9 @@ typedef struct dpara_weights {
   const void* ar_E;                    /* [vocab, ar_rank] (device) */
   const void* ar_W;                    /* [vocab, ar_rank] (device) */
   const dpara_layer_weights_t* layers; /* [n_layers] (HOST array of device pointers) */
+  const float* ar_w_norm2_max;         /* optional (device, one float): max_v |ar_W[v]|^2 as
+                                          dpara_head_prepare writes it; NULL: every head call
+                                          computes it (one pass over ar_W) */
 } dpara_weights_t;
 
 /* Feature cache C kept as per-layer context K/V (Section 3.3: C over the accepted
@@ -245,6 +248,14 @@ int dpara_verify_sampled(const dpara_config_t* cfg, int32_t batch, const void* t
                          int32_t logits_dtype, const float* draft_scores, const int32_t* spine,
                          float temperature, uint64_t seed, const uint64_t* seed_dev,
                          int32_t* accept_len, int32_t* bonus, void* ws, size_t ws_bytes, void* stream);
+
+/* Weight preparation for the bound-pruned head steps (the Cauchy-Schwarz bound of
+ * dpara_select_and_head): writes max_v |ar_W[v]|^2 into norm2_max (device, one float).  The
+ * value depends on the weights only; set w->ar_w_norm2_max to it and every later head call
+ * skips its own pass over ar_W, with the same results.  ws: a workspace of
+ * dpara_workspace_bytes(cfg, 1, 64) bytes or more (scratch). */
+int dpara_head_prepare(const dpara_config_t* cfg, const dpara_weights_t* w, float* norm2_max, void* ws,
+                       size_t ws_bytes, void* stream);
 
 /* Head variant with every branch's base logits computed off the serial path (Algorithm 1
  * computes the base logits during Precompute).

@@ -726,7 +726,7 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
               "perturbed logits");
       pe = launch_head_pruned(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.plogits), w->ar_E, w->ar_W,
                               bonus, drafts, next_spine, margins, at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart),
-                              hflag, status, st, smp->inv_t);
+                              hflag, status, st, smp->inv_t, w->ar_w_norm2_max);
       if (pe != hipSuccess && pe != hipErrorNotSupported) return hip_fail(pe, "sampled pruned head");
     }
     HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
@@ -746,7 +746,8 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
   int* hflag = at<int>(ws, p.hflag);
   const hipError_t pe = launch_head_pruned(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits),
                                            w->ar_E, w->ar_W, bonus, drafts, next_spine, margins,
-                                           at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart), hflag, status, st);
+                                           at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart), hflag, status, st,
+                                           1.0f, w->ar_w_norm2_max);
   if (pe != hipSuccess && pe != hipErrorNotSupported) return hip_fail(pe, "pruned head");
   HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,
@@ -756,6 +757,28 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
   return DPARA_OK;
 }
 
+}  // namespace
+
+int dpara_head_prepare(const dpara_config_t* cfg, const dpara_weights_t* w, float* norm2_max, void* ws,
+                       size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!w || !w->ar_W) return fail(DPARA_E_INVALID, "weights or ar_W is NULL");
+  CHECK_PTR(norm2_max, "norm2_max");
+  if (!ws || ((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace is NULL or not 256-byte aligned");
+  const Plan p = make_plan(cfg, 1, 64);
+  const size_t need = p.hwpart + up256((size_t)head_prune_wparts() * 4);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if (cfg->ar_rank != 64 && cfg->ar_rank != 128 && cfg->ar_rank != 256)
+    return fail(DPARA_E_UNSUPPORTED, "the pruned head needs ar_rank in {64, 128, 256}");
+  if ((rc = check_device())) return rc;
+  HIP_TRY(launch_head_prepare(cfg->dtype, cfg->ar_rank, w->ar_W, cfg->vocab, at<float>(ws, p.hwpart),
+                              at<int>(ws, 12), norm2_max, (hipStream_t)stream),
+          "head prepare");
+  return DPARA_OK;
+}
+
+namespace {
 // Temperature and seed of the sampling variant: the generator's key is the seed's two
 // 32-bit halves.
 int make_sampling(float temperature, uint64_t seed, const uint64_t* seed_dev, float* scores, Sampling* smp) {

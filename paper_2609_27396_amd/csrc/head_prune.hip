@@ -486,6 +486,16 @@ __global__ __launch_bounds__(256) void gather_prev_e(int gamma, int V, int rank,
   for (int k = threadIdx.x; k < rank; k += 256) rows[(int64_t)row * rank + k] = E[(int64_t)y * rank + k];
 }
 
+__global__ __launch_bounds__(256) void max_of(const float* parts, int n, float* out) {
+  __shared__ float red[4];
+  float m = 0.f;
+  for (int i = threadIdx.x; i < n; i += 256) m = fmaxf(m, parts[i]);
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) *out = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
 __global__ __launch_bounds__(256) void finish_scores(int64_t n, const float* L, const float* C, float* S, float inv_t,
                                                      const int* ok) {
   if (*ok == 0) return;
@@ -608,15 +618,22 @@ size_t head_prune_cand_bytes(int rows, int V) { return (size_t)rows * head_prune
 
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
-                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st, float inv_t) {
+                              uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st, float inv_t,
+                              const float* wnorm_pre) {
   if (!head_prune_supported(dtype, gamma, V, rank) || B < 1) return hipErrorNotSupported;
   const int rows = B * gamma;
   const int S = head_prune_splits(rows, V);
   const int per = ((V + S - 1) / S + 3) / 4 * 4;
-  const int nw = head_prune_wparts();
+  int nw = head_prune_wparts();
   Phase ph("ar_step", st);
-  hipError_t e = launch_wnorm(dtype, rank, W, V, wpart, flag, st);
+  // the weights' max row norm: prepared once (one float), or one pass over W here (which also
+  // clears the fallback flag)
+  hipError_t e = wnorm_pre ? launch_clear_status(flag, st) : launch_wnorm(dtype, rank, W, V, wpart, flag, st);
   if (e != hipSuccess) return e;
+  if (wnorm_pre) {
+    wpart = const_cast<float*>(wnorm_pre);
+    nw = 1;
+  }
   hipLaunchKernelGGL(logit_topk, dim3(S, rows), dim3(256), 0, st, logits, V, S, per, cand, flag);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -658,6 +675,14 @@ hipError_t launch_draft_scores(int dtype, int B, int gamma, int V, int rank, con
   const int64_t n = (int64_t)R * V;
   const int grid = (int)std::min<int64_t>((n + 255) / 256, 4096);
   hipLaunchKernelGGL(finish_scores, dim3(grid), dim3(256), 0, st, n, logits, cbuf, smp.scores, smp.inv_t, ok);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_prepare(int dtype, int rank, const void* W, int V, float* parts, int* scratch_flag, float* out,
+                               hipStream_t st) {
+  hipError_t e = launch_wnorm(dtype, rank, W, V, parts, scratch_flag, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(max_of, dim3(1), dim3(256), 0, st, parts, head_prune_wparts(), out);
   return hipGetLastError();
 }
 

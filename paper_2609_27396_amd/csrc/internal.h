@@ -204,7 +204,11 @@ size_t head_prune_cand_bytes(int rows, int V);
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                               uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st,
-                              float inv_t = 1.0f);
+                              float inv_t = 1.0f, const float* wnorm_pre = nullptr);
+// max_v |W_v|^2 into out (one float); parts: head_prune_wparts() floats of scratch, scratch_flag
+// one int.
+hipError_t launch_head_prepare(int dtype, int rank, const void* W, int V, float* parts, int* scratch_flag, float* out,
+                               hipStream_t st);
 // Sampled head through the pruned steps: P = l * inv_t + Gumbel(key; head tag, b, i, v) for
 // every head row (row b * gamma + i - 1), ranked by launch_head_pruned(..., P, inv_t); then,
 // where the pruned steps decided every step (*flag == 0), the draft scores

@@ -27,7 +27,7 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
            "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_target_forward_hidden",
            "dpara_fuse_workspace_bytes", "dpara_fuse_features", "dpara_select_and_head_sampled",
-           "dpara_verify_sampled")
+           "dpara_verify_sampled", "dpara_head_prepare")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -56,7 +56,7 @@ class DparaLayerWeights(ctypes.Structure):
 class DparaWeights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("mask_emb", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
                 ("ar_E", ctypes.c_void_p), ("ar_W", ctypes.c_void_p),
-                ("layers", ctypes.POINTER(DparaLayerWeights))]
+                ("layers", ctypes.POINTER(DparaLayerWeights)), ("ar_w_norm2_max", ctypes.c_void_p)]
 
 
 class DparaTargetWeights(ctypes.Structure):
@@ -111,6 +111,7 @@ def lib():
         L.dpara_select_and_head_sampled.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP,
                                                     VP, F32, U64, VP, VP, VP, SZ, VP]
         L.dpara_verify_sampled.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, F32, U64, VP, VP, VP, VP, SZ, VP]
+        L.dpara_head_prepare.argtypes = [P(DparaConfig), P(DparaWeights), VP, VP, SZ, VP]
         L.dpara_last_error.restype = ctypes.c_char_p
         L.dpara_version.restype = I32
         L.dpara_profile_enable.argtypes = [I32]
@@ -119,7 +120,8 @@ def lib():
                      "dpara_select_and_head", "dpara_branch_candidates", "dpara_select_and_head_cand",
                      "dpara_clear_status", "dpara_profile_enable",
                      "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features",
-                     "dpara_target_forward_hidden", "dpara_select_and_head_sampled", "dpara_verify_sampled"):
+                     "dpara_target_forward_hidden", "dpara_select_and_head_sampled", "dpara_verify_sampled",
+                     "dpara_head_prepare"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -258,6 +260,18 @@ class DeviceDrafter:
     def mat_dtype(self):
         import torch
         return torch.bfloat16 if self.shape.dtype == "bf16" else torch.float32
+
+    def prepare_head(self, ws, stream=None):
+        """Compute max_v |ar_W[v]|^2 once (dpara_head_prepare) and point the weights at it, so
+        head calls skip their own pass over ar_W."""
+        import torch
+        self.norm2 = torch.empty(1, dtype=torch.float32, device=self.device)
+        _check(lib().dpara_head_prepare(_ref(self.cfg), _ref(self.w), _ptr(self.norm2), ws.ptr, ws.nbytes,
+                                        _stream(stream)))
+        self.w.ar_w_norm2_max = _ptr(self.norm2)
+
+    def unprepare_head(self):
+        self.w.ar_w_norm2_max = None
 
 
 class DeviceTarget:

@@ -189,6 +189,48 @@ def test_head_pruned_bound_and_fallback(regime):
 
 
 @pytest.mark.parametrize("regime", ["pruned", "full"])
+def test_prepared_head_norm_gives_the_same_head(regime):
+    """With the weights' max |W_v|^2 prepared once (dpara_head_prepare), the greedy and the
+    sampled head give the same drafts, next block, margins, scores and fallback flag, bit for
+    bit, as the per-call pass over W, whether every step is proven or the full head runs."""
+    shape = HEAD_SHAPE
+    big = regime == "full"
+    wl = synth.Workload("hp", shape, batch=3, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=12)
+    w = synth.make_weights(shape, seed=5, gain_jitter=0.1, ar_w_std=2.0 if big else 0.005,
+                           ar_e_std=1.0 if big else 0.02)
+    ri = synth.make_round(wl, ctx_lens=[20, 0, 90])
+    dr = _harness()(shape, w, ri)
+    dr.backbone()
+    dr.verify()
+    scores = torch.empty((3, shape.gamma, shape.vocab), dtype=torch.float32, device="cuda")
+    outs = ("drafts", "next_spine", "margins")
+
+    def run():
+        dr.head()
+        torch.cuda.synchronize()
+        greedy = {k: getattr(dr, k).clone() for k in outs}
+        gflag = dr.head_fallback()
+        dr.head_sampled(1.0, 77, scores)
+        torch.cuda.synchronize()
+        sampled = {k: getattr(dr, k).clone() for k in outs}
+        return greedy, gflag, sampled, dr.head_fallback(), scores.clone()
+
+    ref = run()
+    dr.d.prepare_head(dr.ws)
+    assert float(dr.d.norm2.item()) == float((w["ar_W"].astype(np.float32) ** 2).sum(1).max()) or \
+        abs(float(dr.d.norm2.item()) / float((w["ar_W"].astype(np.float64) ** 2).sum(1).max()) - 1) < 1e-6
+    got = run()
+    dr.d.unprepare_head()
+    for r_, g_ in ((ref[0], got[0]), (ref[2], got[2])):
+        for k in outs:
+            assert torch.equal(r_[k], g_[k]), k
+    assert (ref[1], ref[3]) == (got[1], got[3])
+    assert (ref[1] != 0) == big
+    assert torch.equal(ref[4], got[4])
+    assert dr.status() == 0
+
+
+@pytest.mark.parametrize("regime", ["pruned", "full"])
 def test_head_from_branch_candidates(regime):
     """The off-serial-path head variant: candidates of every branch row computed after the
     backbone, then the serial step from the accepted branch's candidates.  Drafts, margins,
