@@ -176,3 +176,22 @@ def test_sampling_validation_without_gpu():
                None) == D.DPARA_E_UNSUPPORTED
     assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, 1.0, 1, None, FAKE, FAKE, ws, 1024,
                None) == D.DPARA_E_WORKSPACE
+
+
+def test_head_prepare_validation_without_gpu():
+    """dpara_head_prepare rejects a missing output, a missing or small workspace and an
+    unsupported rank on the host, before any launch."""
+    shape = synth.QWEN3_8B
+    cfg = D.make_config(shape)
+    w, _layers = _fake_weights(shape)
+    R = ctypes.byref
+    nb = D.dpara_workspace_bytes(cfg, 1, 64)
+    assert _rc("dpara_head_prepare", R(cfg), R(w), None, FAKE, nb, None) == D.DPARA_E_INVALID
+    assert "norm2_max" in D.dpara_last_error()
+    assert _rc("dpara_head_prepare", R(cfg), R(w), FAKE, None, nb, None) == D.DPARA_E_INVALID
+    assert _rc("dpara_head_prepare", R(cfg), R(w), FAKE, FAKE, 1024, None) == D.DPARA_E_WORKSPACE
+    bad = D.make_config(synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=2, n_kv_heads=1, head_dim=128,
+                                           ffn=512, vocab=1000, gamma=4, ar_rank=32, qk_norm=True, dtype="bf16"))
+    assert _rc("dpara_head_prepare", R(bad), R(w), FAKE, FAKE, nb, None) in (D.DPARA_E_INVALID,
+                                                                           D.DPARA_E_UNSUPPORTED)
+    assert "ar_rank" in D.dpara_last_error()
