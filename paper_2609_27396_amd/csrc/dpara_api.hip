@@ -688,7 +688,9 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
   const Plan p = make_plan(cfg, batch, 64);
   if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
-  const size_t need = p.hwpart + up256((size_t)head_prune_wparts() * 4);
+  size_t need = p.hwpart + up256((size_t)head_prune_wparts() * 4);
+  if (smp)  // the sampled head also uses the perturbed-logit and E-row regions at the end
+    need = p.erows + up256((size_t)batch * cfg->gamma * cfg->ar_rank * p.esz);
   if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
   if ((rc = check_device())) return rc;
 

@@ -176,6 +176,9 @@ def test_sampling_validation_without_gpu():
                None) == D.DPARA_E_UNSUPPORTED
     assert _rc("dpara_verify_sampled", R(cfg), 1, FAKE, D.DPARA_BF16, FAKE, FAKE, 1.0, 1, None, FAKE, FAKE, ws, 1024,
                None) == D.DPARA_E_WORKSPACE
+    # the sampled head also needs the perturbed-logit and E-row regions at the end of the plan
+    assert _rc("dpara_select_and_head_sampled", R(cfg), R(w), 1, FAKE, FAKE, FAKE, None, FAKE, FAKE, None,
+               1.0, 1, None, None, ws, nb - 1, None) == D.DPARA_E_WORKSPACE
 
 
 def test_head_prepare_validation_without_gpu():
