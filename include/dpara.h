@@ -162,6 +162,18 @@ int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights
                                   const dpara_ctx_t* ctx, int32_t batch, const int32_t* spine,
                                   float* reps, void* ws, size_t ws_bytes, void* stream);
 
+/* dpara_backbone_all_boundaries that also writes the residual stream of every block row after
+ * every drafter layer, for checking the layers one at a time against a reference (each layer is
+ * the pre-norm block of Section 3.2's backbone; the tree mask is the same).
+ * resid: [n_layers, batch, (gamma+1)^2, hidden] float32 (device, output, 16-byte aligned):
+ *        resid[l][b][m] is row m of request b after layer l (row layout as for spine and reps:
+ *        spine t_j at row j, branch r's mask i at row gamma+1+r*gamma+i-1).
+ * reps and every other argument as for dpara_backbone_all_boundaries; reps come out bit for bit
+ * the same.  Costs one extra write of the rows per layer. */
+int dpara_backbone_trace(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx,
+                         int32_t batch, const int32_t* spine, float* reps, float* resid, void* ws,
+                         size_t ws_bytes, void* stream);
+
 /* Greedy verification (Section 2.1; Algorithm 1, Verify).
  * target_logits: [batch, gamma+1, vocab] (device), logits_dtype DPARA_F32 or DPARA_BF16:
  *                row j scores the token after t_j.

@@ -279,10 +279,12 @@ namespace {
 // Leaves the residual stream in ws[p.X].
 // hid_layers / n_hid / hid: optionally emit the rows' hidden state after those layers
 // (hid[m * n_hid + j] after layer hid_layers[j], bf16).
+// resid: optionally the float32 residual stream of every row after every layer
+// (resid[l][m], [n_layers][M][H]).
 int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, const void* embed,
                 const void* mask_emb, const dpara_ctx_t* ctx, int32_t batch, const int32_t* tokens,
                 int spine_only, const Plan& p, void* ws, hipStream_t st, int* pending,
-                const int32_t* hid_layers = nullptr, int n_hid = 0, void* hid = nullptr) {
+                const int32_t* hid_layers = nullptr, int n_hid = 0, void* hid = nullptr, float* resid = nullptr) {
   const int dt = cfg->dtype, H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q_heads, nkv = cfg->n_kv_heads;
   const int g = cfg->gamma, R = p.R, M = p.M, F = cfg->ffn;
   const int amode = dt == DPARA_BF16 ? A_BF16 : A_F32;
@@ -419,6 +421,9 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     for (int j = 0; j < n_hid; ++j)
       if (hid_layers[j] == l)
         HIP_TRY(launch_emit_hidden(M, H, X, P, pend, (int64_t)M * H, hid, n_hid, j, st), "emit hidden");
+    if (resid)
+      HIP_TRY(launch_emit_hidden(M, H, X, P, pend, (int64_t)M * H, resid + (size_t)l * M * H, 1, 0, st, 1),
+              "emit residual");
   }
   *pending = pend;
   return DPARA_OK;
@@ -540,9 +545,9 @@ int dpara_ctx_append(const dpara_config_t* cfg, const dpara_weights_t* w, const 
   return DPARA_OK;
 }
 
-int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx,
-                                  int32_t batch, const int32_t* spine, float* reps, void* ws, size_t ws_bytes,
-                                  void* stream) {
+namespace {
+int backbone_impl(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx, int32_t batch,
+                  const int32_t* spine, float* reps, float* resid, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_cfg(cfg);
   if (rc) return rc;
   if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
@@ -555,7 +560,9 @@ int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights
   if ((rc = check_device())) return rc;
   hipStream_t st = (hipStream_t)stream;
   int pend = 0;
-  if ((rc = run_decoder(cfg, w->layers, w->embed, w->mask_emb, ctx, batch, spine, 0, p, ws, st, &pend))) return rc;
+  if ((rc = run_decoder(cfg, w->layers, w->embed, w->mask_emb, ctx, batch, spine, 0, p, ws, st, &pend, nullptr, 0,
+                        nullptr, resid)))
+    return rc;
   // reps[b][r][i-1] = final norm of mask rows: input row (m / nmask) * R + (g + 1 + m % nmask), with the
   // last down projection's split-K planes added
   const int g = cfg->gamma, R = p.R, H = cfg->hidden;
@@ -565,6 +572,19 @@ int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights
                          pend, (int64_t)p.M * H, 0, w->final_norm, cfg->rms_eps, reps, st),
           "final_norm");
   return DPARA_OK;
+}
+}  // namespace
+
+int dpara_backbone_all_boundaries(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx,
+                                  int32_t batch, const int32_t* spine, float* reps, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  return backbone_impl(cfg, w, ctx, batch, spine, reps, nullptr, ws, ws_bytes, stream);
+}
+
+int dpara_backbone_trace(const dpara_config_t* cfg, const dpara_weights_t* w, const dpara_ctx_t* ctx, int32_t batch,
+                         const int32_t* spine, float* reps, float* resid, void* ws, size_t ws_bytes, void* stream) {
+  CHECK_PTR(resid, "resid");
+  return backbone_impl(cfg, w, ctx, batch, spine, reps, resid, ws, ws_bytes, stream);
 }
 
 size_t dpara_target_workspace_bytes(const dpara_config_t* cfg, int32_t batch, int32_t ctx_cap) {

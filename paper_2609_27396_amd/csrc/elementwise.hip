@@ -305,8 +305,9 @@ __global__ __launch_bounds__(256) void kv_store(int CH, int c0, int n_max, int n
 
 // Hidden state of every row after a layer: bf16(X + the S pending split-K planes), written
 // to out[m * n_out + j] (rows of H entries), 4 entries per thread.
+template <typename TO>
 __global__ __launch_bounds__(256) void emit_hidden(int H, const float* X, const float* P, int S, int64_t pstride,
-                                                   bf16_t* out, int n_out, int j) {
+                                                   TO* out, int n_out, int j) {
   const int m = blockIdx.y;
   const int i = (blockIdx.x * 256 + threadIdx.x) * 4;
   if (i >= H) return;
@@ -318,8 +319,12 @@ __global__ __launch_bounds__(256) void emit_hidden(int H, const float* X, const 
     v.z += q.z;
     v.w += q.w;
   }
-  bf16_t* o = out + ((int64_t)m * n_out + j) * H + i;
-  *(uint2*)o = make_uint2(f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16), f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+  TO* o = out + ((int64_t)m * n_out + j) * H + i;
+  if constexpr (sizeof(TO) == 4) {
+    *(float4*)o = v;
+  } else {
+    *(uint2*)o = make_uint2(f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16), f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+  }
 }
 
 __global__ void ctx_len_update_kernel(int B, int n_max, int cap, const int* n_new, int* ctx_len, int* status) {
@@ -462,11 +467,14 @@ hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv
 }
 
 hipError_t launch_emit_hidden(int rows, int H, const float* X, const float* P, int S, int64_t pstride, void* out,
-                              int n_out, int j, hipStream_t st) {
+                              int n_out, int j, hipStream_t st, int out_f32) {
   if (rows <= 0) return hipSuccess;
   if (H % 4 || S < 0 || S > kMaxPlanes || j < 0 || j >= n_out) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(emit_hidden, dim3((H / 4 + 255) / 256, rows), dim3(256), 0, st, H, X, P, S, pstride,
-                     (bf16_t*)out, n_out, j);
+  const dim3 grid((H / 4 + 255) / 256, rows);
+  if (out_f32)
+    hipLaunchKernelGGL(emit_hidden<float>, grid, dim3(256), 0, st, H, X, P, S, pstride, (float*)out, n_out, j);
+  else
+    hipLaunchKernelGGL(emit_hidden<bf16_t>, grid, dim3(256), 0, st, H, X, P, S, pstride, (bf16_t*)out, n_out, j);
   return hipGetLastError();
 }
 

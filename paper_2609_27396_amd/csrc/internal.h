@@ -126,9 +126,10 @@ hipError_t launch_kv_store(int dtype, int B, int CH, int c0, int n_max, int n_kv
                            int qk_norm, float eps, const float2* rope, const float* KV, int S,
                            int nl, const KvLayers& kn, const int* n_new, const int* ctx_len, int cap,
                            void* Kc, void* Vc, size_t layer_elems, int* status, hipStream_t st);
-// out[m * n_out + j][0..H) = bf16(X[m] + sum_{s<S} P[s][m]) for rows m < rows (bf16 out).
+// out[m * n_out + j][0..H) = X[m] + sum_{s<S} P[s][m] for rows m < rows, rounded to bf16
+// (out_f32 == 0) or kept float32.
 hipError_t launch_emit_hidden(int rows, int H, const float* X, const float* P, int S, int64_t pstride, void* out,
-                              int n_out, int j, hipStream_t st);
+                              int n_out, int j, hipStream_t st, int out_f32 = 0);
 hipError_t launch_ctx_len_update(int B, int n_max, int cap, const int* n_new, int* ctx_len,
                                  int* status, hipStream_t st);
 hipError_t launch_clear_status(int* status, hipStream_t st);

@@ -27,7 +27,7 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
            "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_target_forward_hidden",
            "dpara_fuse_workspace_bytes", "dpara_fuse_features", "dpara_select_and_head_sampled",
-           "dpara_verify_sampled", "dpara_head_prepare")
+           "dpara_verify_sampled", "dpara_head_prepare", "dpara_backbone_trace")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -89,6 +89,8 @@ def lib():
         L.dpara_ctx_append.argtypes = [P(DparaConfig), P(DparaWeights), P(DparaCtx), I32, VP, VP, I32, VP, SZ, VP]
         L.dpara_backbone_all_boundaries.argtypes = [P(DparaConfig), P(DparaWeights), P(DparaCtx), I32, VP, VP, VP,
                                                     SZ, VP]
+        L.dpara_backbone_trace.argtypes = [P(DparaConfig), P(DparaWeights), P(DparaCtx), I32, VP, VP, VP, VP, SZ,
+                                           VP]
         L.dpara_verify_greedy.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, VP, VP, VP, SZ, VP]
         L.dpara_select_and_head.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP, VP, VP,
                                             SZ, VP]
@@ -121,7 +123,7 @@ def lib():
                      "dpara_clear_status", "dpara_profile_enable",
                      "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features",
                      "dpara_target_forward_hidden", "dpara_select_and_head_sampled", "dpara_verify_sampled",
-                     "dpara_head_prepare"):
+                     "dpara_head_prepare", "dpara_backbone_trace"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -367,6 +369,13 @@ def ctx_append(d: DeviceDrafter, ctx: DeviceContext, feats, n_new, ws: Workspace
 def backbone_all_boundaries(d: DeviceDrafter, ctx: DeviceContext, spine, reps, ws: Workspace, stream=None):
     dpara_backbone_all_boundaries(d.cfg, d.w, ctx.c, int(spine.shape[0]), _ptr(spine), _ptr(reps), ws.ptr,
                                   ws.nbytes, _stream(stream))
+
+
+def backbone_trace(d: DeviceDrafter, ctx: DeviceContext, spine, reps, resid, ws: Workspace, stream=None):
+    """backbone_all_boundaries that also writes resid [n_layers, B, (gamma+1)^2, H] float32: every
+    row's residual stream after every layer."""
+    _check(lib().dpara_backbone_trace(_ref(d.cfg), _ref(d.w), _ref(ctx.c), int(spine.shape[0]), _ptr(spine),
+                                      _ptr(reps), _ptr(resid), ws.ptr, ws.nbytes, _stream(stream)))
 
 
 def verify_greedy(d: DeviceDrafter, logits, spine, accept_len, bonus, target_argmax, ws: Workspace, stream=None):

@@ -5,17 +5,17 @@ representations within 1e-5 (float32 model) or 2e-2 (bf16 model) max-abs; draft
 ids exact wherever the oracle's top1 - top2 margin of z_i exceeds 1e-2, checked
 teacher-forced (the oracle's step i is fed the GPU's y_{i-1}).
 
-Deep bf16 drafters (5 layers at 4096/5120 width): float32 accumulation alone
-(instead of the oracle's float64) flips a fraction of the bf16 roundings and the
-flips compound with depth.  Running the oracle's own GEMMs and attention in
-float32 moves it from itself, at the Qwen3-8B shape, by up to 3.7e-2 max-abs on
-request 0 of the batch-1 round (99.99th percentile 2.9e-2, median 5e-3) and by
-3.4e-2 max-abs on the sampled rows of the batch-16 round (99.99th percentile
-2.8e-2, median 4.8e-3), while one full-width layer stays at 1.1e-2.  Any other
-float32 summation order lands in that envelope only statistically, so the
-5-layer configurations are held to it with a 25% margin: max-abs <= 5e-2,
-99.99th percentile <= 3.5e-2, median <= 1e-2; single-layer and small
-configurations keep the 2e-2 bar.
+Deep bf16 drafters (5 layers at 4096/5120 width): every layer is held to the stated
+2e-2 bar on its own, teacher-forced (test_layerwise_teacher_forced: the oracle's layer
+on the GPU's own input residual, every row of the sampled requests).  End to end,
+float32 accumulation alone (instead of the oracle's float64) flips a fraction of the
+bf16 roundings and the flips compound with depth: running the oracle's own GEMMs and
+attention in float32 moves it from itself, at the Qwen3-8B shape, by up to 3.7e-2
+max-abs on request 0 of the batch-1 round (99.99th percentile 2.9e-2, median 5e-3) and
+by 3.4e-2 on the sampled rows of the batch-16 round, while one full-width layer stays
+at 1.1e-2.  The end-to-end comparison of the 5-layer configurations is therefore a
+documented envelope, not the parity bar: max-abs <= 5e-2, 99.99th percentile <=
+3.5e-2, median <= 1e-2; single-layer and small configurations keep 2e-2 end to end.
 """
 import sys
 
@@ -399,10 +399,73 @@ def test_full_width_one_layer_qwen3_8b():
 
 
 def test_full_size_qwen3_8b_b1():
+    """Every branch of the batch-1 request, end to end, against the oracle's tree pass."""
     wl = synth.WORKLOADS["qwen3_8b_b1"]
+    _say("case qwen3_8b_b1 end to end, all branches")
+    w = synth.make_weights(wl.shape, seed=wl.seed_w)
     ri = synth.make_round(wl)
-    r = int(ri.accept_planted[0])
-    _full_size("qwen3_8b_b1", [(0, sorted({0, r, wl.shape.gamma}))])
+    dr = run_full(wl, w, ri)
+    check_verify(ri, dr)
+    ref = O.backbone_all_boundaries(wl.shape, w, ri.ctx_feats[0], ri.spine[0], "bf16")["reps"]
+    check_reps(wl.shape, [np.abs(dr.reps[0].cpu().numpy() - ref)], "qwen3_8b_b1 all branches")
+    _say("qwen3_8b_b1 head steps skipped:", check_head(wl.shape, w, dr, "bf16", 0))
+
+
+# Requests checked layer by layer (all (gamma+1)^2 rows of each, spine rows included).
+LAYERWISE = {"qwen3_8b_b1": (0,), "qwen3_8b_b16": (0, 6, 11, 15), "qwen3_14b_b8": (0, 7)}
+
+
+@pytest.mark.parametrize("name", sorted(LAYERWISE))
+def test_layerwise_teacher_forced(name):
+    """Each drafter layer of the full-size configurations on its own, teacher-forced: the oracle's
+    layer_forward runs on the GPU's own residual stream entering that layer (every row of the
+    request: spine and every branch's masks; the oracle's own context K/V and tree mask), and its
+    output is compared with the GPU's residual after the layer.  The bar is the stated 2e-2
+    max-abs on the hidden representation, i.e. the residual normalised to unit root mean square
+    (the scale the next layer's norm and the final representations see).  The final layer's mask
+    rows, normalised with the final gain, are the reps the backbone returns (float32 rounding of
+    the norm apart)."""
+    from paper_2609_27396_amd import dpara as D
+    wl = synth.WORKLOADS[name]
+    s = wl.shape
+    _say("case layerwise", name, wl.description)
+    w = synth.make_weights(s, seed=wl.seed_w)
+    ri = synth.make_round(wl)
+    dr = _harness()(s, w, ri)
+    R, g, H, L = s.rows, s.gamma, s.hidden, s.n_layers
+    resid = torch.empty((L, dr.B, R, H), dtype=torch.float32, device="cuda")
+    D.backbone_trace(dr.d, dr.ctx, dr.spine, dr.reps, resid, dr.ws)
+    reps_trace = dr.reps.clone()
+    dr.backbone()
+    torch.cuda.synchronize()
+    assert dr.status() == 0
+    assert torch.equal(reps_trace, dr.reps)   # tracing leaves the result unchanged
+    rnd = O.Rounding("bf16")
+    vis = O.tree_visibility(g)
+    worst = 0.0
+    for b in LAYERWISE[name]:
+        n_b = int(ri.ctx_lens[b])
+        pos = O.row_positions(g, n_b)
+        x_in = np.empty((R, H), np.float64)
+        for j in range(g + 1):
+            x_in[j] = w["embed"][int(ri.spine[b, j])]
+        x_in[g + 1:] = w["mask_emb"][None, :]
+        for l in range(L):
+            ck, cv = O.context_kv(s, w, l, ri.ctx_feats[b], 0, rnd)
+            x_ref = O.layer_forward(s, w, l, x_in, pos, ck, cv, vis, rnd)
+            x_gpu = resid[l, b].cpu().numpy().astype(np.float64)
+            h_ref, h_gpu = O.rmsnorm(x_ref, 1.0, s.rms_eps), O.rmsnorm(x_gpu, 1.0, s.rms_eps)
+            e = np.abs(h_gpu - h_ref)
+            rms = float(np.sqrt(np.mean(x_ref ** 2)))
+            _say(f"{name} request {b} (ctx {n_b}) layer {l}: max|h-oracle| {e.max():.3e} (spine rows "
+                 f"{e[:g + 1].max():.3e}), q99.99 {np.quantile(e, 0.9999):.3e}, residual rms {rms:.3f}, "
+                 f"max|x-oracle|/rms {np.abs(x_gpu - x_ref).max() / rms:.3e}")
+            worst = max(worst, float(e.max()))
+            assert e.max() <= TOL["bf16"], (name, b, l)
+            x_in = x_gpu
+        reps = O.rmsnorm(x_in[g + 1:], w["final_norm"], s.rms_eps).reshape(g + 1, g, H)
+        np.testing.assert_allclose(dr.reps[b].cpu().numpy(), reps, rtol=1e-5, atol=1e-5)
+    _say(name, "layerwise worst max-abs", worst)
 
 
 def test_full_size_qwen3_8b_b16():
@@ -484,7 +547,10 @@ def test_target_forward_parity():
 
 
 def test_backbone_and_target_on_concurrent_streams():
-    """The drafter backbone and the target forward on two streams at once give the same bits as run alone."""
+    """The drafter backbone and the target forward on two streams at once give the same bits as
+    run alone, and those are the oracle's: reps within the bf16 bar of the oracle's tree pass,
+    target logits within the bar of the oracle's target forward (argmax equal where the margin
+    exceeds 1e-2)."""
     from paper_2609_27396_amd import dpara as D
     DeviceRound = _harness()
     shape, _ = SMALL_CASES["h256_hd128_g5"]
@@ -511,6 +577,19 @@ def test_backbone_and_target_on_concurrent_streams():
         torch.cuda.synchronize()
         assert torch.equal(reps1, dr.reps)
         assert torch.equal(l1, l2)
+    errs = []
+    for b in range(3):
+        ref = O.backbone_all_boundaries(shape, wd, ri.ctx_feats[b], ri.spine[b], "bf16")["reps"]
+        errs.append(np.abs(dr.reps[b].cpu().numpy() - ref))
+        tl = O.target_forward(s, w, [k[l][b] for l in range(s.n_layers)], [v[l][b] for l in range(s.n_layers)],
+                              block[b], "bf16")
+        got = l2[b].float().cpu().numpy()
+        assert np.all(np.abs(got - tl) <= 2.0 ** -8 * np.abs(tl) + TOL["bf16"]), b
+        for j in range(s.gamma + 1):
+            y, m = O.argmax_margin(tl[j])
+            if m > MARGIN + 2.0 ** -7 * np.abs(tl[j]).max():  # the logits here are bf16
+                assert int(np.argmax(got[j])) == y, (b, j)
+    check_reps(shape, errs, "concurrent streams")
 
 
 def test_verification_beside_backbone_on_one_workspace():
@@ -641,7 +720,122 @@ def test_round_graph_replays(case):
         assert torch.equal(dr.ctx.k, ref_k) and torch.equal(dr.ctx.v, ref_v)
         assert dr.status() == 0
     _say(case, "sampled" if sampled else "greedy", "graph replays identical to the eager round: 4")
+    # the last replay against the oracle: the context is the rewound prefix plus the appended rows
+    mode, errs = wl.shape.dtype, []
+    for b in range(B):
+        n0 = int(ri.ctx_lens[b]) - int(n_new_h[b])
+        feats = np.concatenate([ri.ctx_feats[b][:n0], ri.new_feats[b][:int(n_new_h[b])]])
+        ref = O.backbone_all_boundaries(wl.shape, w, feats, ri.spine[b], mode)["reps"]
+        errs.append(np.abs(dr.reps[b].cpu().numpy() - ref))
+    check_reps(wl.shape, errs, case + " graph replay")
+    if sampled:
+        from test_gpu_sampling import ACC_MARGIN, BONUS_MARGIN, _check_head_sampled
+        seed, s_in = seeds[3 % 2], dr.scores_in.cpu().numpy()
+        for b in range(B):
+            r, bonus, info = O.verify_sampled(ri.target_logits[b], s_in[b], ri.spine[b], 1.0, seed, b)
+            if np.abs(info["accept_margins"]).min() > ACC_MARGIN:
+                assert int(dr.accept[b]) == r, (b, int(dr.accept[b]), r)
+                if info["bonus_margin"] > BONUS_MARGIN:
+                    assert int(dr.bonus[b]) == bonus, b
+        compared = _check_head_sampled(wl.shape, w, dr, dr.scores_out, 1.0, seed, mode)
+        assert compared >= B * wl.shape.gamma - 2
+    else:
+        check_verify(ri, dr)
+        for b in range(B):
+            check_head(wl.shape, w, dr, mode, b)
 
+
+
+def test_full_round_graph_two_streams():
+    """Single-GPU colocation as one HIP graph (Section 4.3.2 and Appendix D: both forward passes
+    on two streams of one GPU and the head captured together).  Captured: a fork onto two streams
+    (the target's verification forward of the block on one; the drafter's context rewind, append
+    and all-boundary backbone on the other), the join, then the greedy verdict kernel and select +
+    head, whose inputs are device buffers.  Every replay, with eager work clobbering the outputs in
+    between, equals the eager round bit for bit; the last replay matches the oracle (target logits,
+    verdict from them, reps over the rewound prefix plus the appended rows, head teacher-forced).
+    The host reads the verdict and drafts after the replay (the acceptance bookkeeping stays
+    outside the graph)."""
+    from paper_2609_27396_amd import dpara as D
+    from paper_2609_27396_amd.harness import upload_cache
+    sd, st_ = LOOP_DRAFTER, LOOP_TARGET
+    ctx_lens, B, g = [40, 0, 170], 3, LOOP_DRAFTER.gamma
+    wd = synth.make_weights(sd, seed=51, gain_jitter=0.1, ar_e_std=1.0)
+    wt = synth.make_target_weights(st_, seed=52, gain_jitter=0.1)
+    wl = synth.Workload("fr", sd, batch=B, ctx_min=0, ctx_max=0, p_reject=0.3, seed_in=53)
+    ri = synth.make_round(wl, ctx_lens=ctx_lens)
+    dr = _harness()(sd, wd, ri, ctx_cap=256)
+    tk, tv = synth.make_target_cache(st_, ctx_lens, seed=54)
+    t = D.DeviceTarget(st_, wt)
+    tctx = D.DeviceContext(st_, B, 256)
+    upload_cache(tctx, tk, tv, ctx_lens, torch.bfloat16)
+    tws = D.Workspace(t.cfg, B, 256, target=True)
+    n_new_h = ri.accept_planted.astype(np.int32) + 1
+    n_new = torch.from_numpy(n_new_h).cuda()
+    base_len = torch.from_numpy((ri.ctx_lens - n_new_h).astype(np.int32)).cuda()
+    s_v, s_d = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def round_():
+        cur = torch.cuda.current_stream()
+        s_v.wait_stream(cur)
+        s_d.wait_stream(cur)
+        with torch.cuda.stream(s_d):
+            dr.ctx.ctx_len[:B].copy_(base_len)
+            dr.append(n_new, stream=s_d)
+            dr.backbone(stream=s_d)
+        with torch.cuda.stream(s_v):
+            D.target_forward(t, tctx, dr.spine, dr.logits, tws, stream=s_v)
+        cur.wait_stream(s_d)
+        cur.wait_stream(s_v)
+        dr.verify()
+        dr.head()
+
+    outs = ("logits", "reps", "accept", "bonus", "targmax", "gathered", "drafts", "next_spine", "margins")
+    round_()
+    torch.cuda.synchronize()
+    assert dr.status() == 0
+    ref = {k: getattr(dr, k).clone() for k in outs}
+    ref_k, ref_v = dr.ctx.k.clone(), dr.ctx.v.clone()
+    graph = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cs):
+        with torch.cuda.graph(graph, stream=cs):
+            round_()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for k in outs:
+            x = getattr(dr, k)
+            x.fill_(-7 if x.dtype == torch.int32 else float("nan"))
+        dr.ctx.ctx_len.fill_(0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k in outs:
+            assert torch.equal(getattr(dr, k), ref[k]), (rep, k)
+        assert torch.equal(dr.ctx.k, ref_k) and torch.equal(dr.ctx.v, ref_v)
+        assert dr.status() == 0
+    lg = dr.logits.float().cpu().numpy()
+    acc, bon, tg = dr.accept.cpu().numpy(), dr.bonus.cpu().numpy(), dr.targmax.cpu().numpy()
+    errs, compared = [], 0
+    for b in range(B):
+        tl = O.target_forward(st_, wt, [tk[l][b] for l in range(st_.n_layers)],
+                              [tv[l][b] for l in range(st_.n_layers)], ri.spine[b], "bf16")
+        assert np.all(np.abs(lg[b] - tl) <= 2.0 ** -8 * np.abs(tl) + TOL["bf16"]), b
+        r, bonus, gg = O.verify_greedy(lg[b], ri.spine[b])     # the verdict of the GPU's logits: exact
+        assert (int(acc[b]), int(bon[b])) == (r, bonus) and np.array_equal(tg[b], gg), b
+        r_o, bonus_o, _ = O.verify_greedy(tl, ri.spine[b])    # and the oracle's, where its margins allow
+        if min(O.argmax_margin(tl[j])[1] for j in range(r_o + 1)) > MARGIN + 2.0 ** -7 * np.abs(tl).max():
+            assert (r, bonus) == (r_o, bonus_o), b
+            compared += 1
+        n0 = int(ri.ctx_lens[b]) - int(n_new_h[b])
+        feats = np.concatenate([ri.ctx_feats[b][:n0], ri.new_feats[b][:int(n_new_h[b])]])
+        rep_ref = O.backbone_all_boundaries(sd, wd, feats, ri.spine[b], "bf16")["reps"]
+        errs.append(np.abs(dr.reps[b].cpu().numpy() - rep_ref))
+        check_head(sd, wd, dr, "bf16", b)
+    check_reps(sd, errs, "full-round graph replay")
+    _say("full-round graph: 4 replays identical to the eager round; verdicts compared with the oracle's:",
+         compared, "accepted", acc.tolist())
 
 
 # ----------------------------------------------------------------------------- feature fusion
@@ -724,8 +918,10 @@ def test_iterated_rounds_with_fused_target_features():
     a planted number of leading drafts replaced by the target's greedy chain, so the accepted
     length varies from 0 to gamma) and the append count is the oracle's r + 1; the GPU's
     hidden states, logits, verdict, reps, drafts and fused rows are checked against the
-    oracle's, wherever the oracle's argmax margins make them unique.  The oracle's context
-    grows by its own fused rows, the GPU's by the GPU's.  The target's own cache stays fixed."""
+    oracle's, wherever the oracle's argmax margins make them unique.  Both contexts grow by the
+    oracle's fused rows (the GPU's own fused rows are checked against them separately), so every
+    round's reps are held to the single-round bar on identical inputs.  The target's own cache
+    stays fixed."""
     from paper_2609_27396_amd import dpara as D
     from paper_2609_27396_amd.harness import upload_cache
     sd, st_ = LOOP_DRAFTER, LOOP_TARGET
@@ -768,6 +964,7 @@ def test_iterated_rounds_with_fused_target_features():
         logits_h = dr.logits.float().cpu().numpy()
         hid_h, fused_h = hid.float().cpu().numpy(), fused.float().cpu().numpy()
         nxt, n_new = np.zeros_like(spine), np.zeros(B, np.int32)
+        f_app = np.zeros((B, g + 1, H), np.float32)
         for b in range(B):
             tl, th = O.target_forward(st_, wt, [tk[l][b] for l in range(st_.n_layers)],
                                       [tv[l][b] for l in range(st_.n_layers)], spine[b], "bf16", FEAT_LAYERS)
@@ -784,13 +981,10 @@ def test_iterated_rounds_with_fused_target_features():
             if min(O.argmax_margin(tl[j])[1] for j in range(r_ref + 1)) > MARGIN:
                 assert (int(acc[b]), int(bonus[b])) == (r_ref, bonus_ref), (rnd, b)
                 compared["verdicts"] += 1
-            # from the second round on, the two contexts also differ by the appended rows
-            # (each side's own fused rows, up to the fused bar apart): the reps bar then adds
-            # the worst fused deviation seen so far to the single-round bar
             ref = O.backbone_all_boundaries(sd, wd, feats[b], spine[b], "bf16")["reps"]
             e = np.abs(dr.reps[b].cpu().numpy() - ref)
             worst["reps"] = max(worst["reps"], float(e.max()))
-            assert e.max() <= TOL["bf16"] + worst["fused"], (rnd, b)
+            assert e.max() <= TOL["bf16"], (rnd, b)
             check_head(sd, wd, dr, "bf16", b)
             hd = O.select_and_head(sd, wd, ref, r_ref, bonus_ref, "bf16")
             if int(acc[b]) == r_ref:
@@ -809,10 +1003,11 @@ def test_iterated_rounds_with_fused_target_features():
             worst["fused"] = max(worst["fused"], float(e.max()))
             assert np.all(e <= 2.0 ** -7 * np.abs(f_ref) + TOL["bf16"]), (rnd, b)
             feats[b] = np.concatenate([feats[b], f_ref.astype(np.float32)])
+            f_app[b, :k] = f_ref
             nxt[b], n_new[b] = hd["next_spine"], k
         before = dr.ctx.ctx_len[:B].clone()
         nn = torch.from_numpy(n_new).cuda()
-        dr.append(nn, fused)
+        dr.append(nn, torch.from_numpy(f_app).cuda().to(torch.bfloat16))   # the oracle's rows, bf16-valued
         torch.cuda.synchronize()
         assert torch.equal(dr.ctx.ctx_len[:B], before + nn)
         assert dr.status() == 0
