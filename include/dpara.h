@@ -186,6 +186,21 @@ int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* ta
                         int32_t* bonus, int32_t* target_argmax, void* ws, size_t ws_bytes,
                         void* stream);
 
+/* dpara_verify_greedy without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same
+ * arguments, outputs and results as dpara_verify_greedy; the partial argmax keys live in a
+ * static device array of the library (1 MiB per GPU, kept until the process ends) instead of
+ * `ws`.  Limit: 256 + batch * (gamma+1) * ceil(vocab / 4096) * 8 bytes must fit in 1 MiB (the
+ * Qwen3 vocabulary at gamma 16: batch <= 202); larger calls return DPARA_E_WORKSPACE before
+ * launching anything.
+ * status: (device, int32, may be NULL) DPARA_STATUS_* bits are OR-ed into it (the caller clears
+ *         it); with NULL, out-of-range draft ids are not reported (they still never match).
+ * Every call on one GPU shares that GPU's array: calls that overlap in time on one GPU (other
+ * streams, other threads) race and must be ordered by the caller. */
+int dpara_verify_greedy_noalloc(const dpara_config_t* cfg, int32_t batch, const void* target_logits,
+                                int32_t logits_dtype, const int32_t* spine, int32_t* accept_len,
+                                int32_t* bonus, int32_t* target_argmax, int32_t* status, void* stream);
+
 /* Select + AR head (Algorithm 1 after the barrier; head equation of Section 3.2).
  * reps: [batch, gamma+1, gamma, hidden] float32 (device) from the backbone.
  * accept_len, bonus: [batch] int32 (device) from verification.

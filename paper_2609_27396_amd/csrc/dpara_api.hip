@@ -431,6 +431,36 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
 
 }  // namespace
 
+// ---------------------------------------------------------------- allocation-free verification
+// dpara_verify_greedy_noalloc takes its scratch from this array instead of a workspace: a
+// 256-byte header (the status word when the caller passes none), then the per-chunk argmax
+// partials of the verification.  Each GPU the library runs on holds its own copy until the
+// process ends.  Host code uses only the address hipGetSymbolAddress returns for the current
+// device, never the array's name.
+constexpr size_t kNoAllocScratchBytes = (size_t)1 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_dev[64];  // device address of `scratch` per device index (NULL until looked up)
+
+// Device address of `scratch` on the current device, looked up once per device.
+int scratch_address(void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(DPARA_E_UNSUPPORTED, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(DPARA_E_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return DPARA_OK;
+}
+}  // namespace
+
 extern "C" {
 
 int dpara_profile_enable(int32_t on) {
@@ -687,6 +717,33 @@ int dpara_verify_greedy(const dpara_config_t* cfg, int32_t batch, const void* ta
                         target_argmax, at<uint64_t>(ws, p.vpart), p.v_chunks, p.v_chunk, at<int>(ws, 0),
                         (hipStream_t)stream),
           "verify");
+  return DPARA_OK;
+}
+
+int dpara_verify_greedy_noalloc(const dpara_config_t* cfg, int32_t batch, const void* target_logits,
+                                int32_t logits_dtype, const int32_t* spine, int32_t* accept_len, int32_t* bonus,
+                                int32_t* target_argmax, int32_t* status, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch < 1) return fail(DPARA_E_INVALID, "batch must be >= 1");
+  if (logits_dtype != DPARA_F32 && logits_dtype != DPARA_BF16)
+    return fail(DPARA_E_UNSUPPORTED, "logits_dtype must be F32 or BF16");
+  if (!target_logits || !spine || !accept_len || !bonus)
+    return fail(DPARA_E_INVALID, "target_logits, spine, accept_len and bonus must be non-NULL");
+  if (status && ((uintptr_t)status & 3u)) return fail(DPARA_E_INVALID, "status is not 4-byte aligned");
+  const Plan p = make_plan(cfg, batch, 64);
+  const size_t need = 256 + up256((size_t)batch * (cfg->gamma + 1) * p.v_chunks * 8);
+  if (need > kNoAllocScratchBytes)
+    return fail(DPARA_E_WORKSPACE,
+                "batch %d x %d rows x %d vocabulary chunks needs %zu bytes of scratch; the allocation-free "
+                "verification holds %zu", batch, cfg->gamma + 1, p.v_chunks, need, kNoAllocScratchBytes);
+  if ((rc = check_device())) return rc;
+  void* sp = nullptr;
+  if ((rc = scratch_address(&sp))) return rc;
+  HIP_TRY(launch_verify(logits_dtype, batch, cfg->gamma, cfg->vocab, target_logits, spine, accept_len, bonus,
+                        target_argmax, (uint64_t*)((char*)sp + 256), p.v_chunks, p.v_chunk,
+                        status ? status : (int*)sp, (hipStream_t)stream),
+          "verify (no allocation)");
   return DPARA_OK;
 }
 

@@ -27,7 +27,8 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_last_error", "dpara_version", "dpara_profile_enable", "dpara_profile_read",
            "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_target_forward_hidden",
            "dpara_fuse_workspace_bytes", "dpara_fuse_features", "dpara_select_and_head_sampled",
-           "dpara_verify_sampled", "dpara_head_prepare", "dpara_backbone_trace")
+           "dpara_verify_sampled", "dpara_head_prepare", "dpara_backbone_trace",
+           "dpara_verify_greedy_noalloc")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -92,6 +93,7 @@ def lib():
         L.dpara_backbone_trace.argtypes = [P(DparaConfig), P(DparaWeights), P(DparaCtx), I32, VP, VP, VP, VP, SZ,
                                            VP]
         L.dpara_verify_greedy.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, VP, VP, VP, SZ, VP]
+        L.dpara_verify_greedy_noalloc.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, VP, VP, VP, VP]
         L.dpara_select_and_head.argtypes = [P(DparaConfig), P(DparaWeights), I32, VP, VP, VP, VP, VP, VP, VP, VP,
                                             SZ, VP]
         L.dpara_branch_candidates_bytes.argtypes = [P(DparaConfig), I32]
@@ -123,7 +125,7 @@ def lib():
                      "dpara_clear_status", "dpara_profile_enable",
                      "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features",
                      "dpara_target_forward_hidden", "dpara_select_and_head_sampled", "dpara_verify_sampled",
-                     "dpara_head_prepare", "dpara_backbone_trace"):
+                     "dpara_head_prepare", "dpara_backbone_trace", "dpara_verify_greedy_noalloc"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -383,6 +385,21 @@ def verify_greedy(d: DeviceDrafter, logits, spine, accept_len, bonus, target_arg
     ldt = DPARA_BF16 if logits.dtype == torch.bfloat16 else DPARA_F32
     dpara_verify_greedy(d.cfg, int(spine.shape[0]), _ptr(logits), ldt, _ptr(spine), _ptr(accept_len), _ptr(bonus),
                         _ptr(target_argmax), ws.ptr, ws.nbytes, _stream(stream))
+
+
+def dpara_verify_greedy_noalloc(cfg, batch, target_logits, logits_dtype, spine, accept_len, bonus, target_argmax,
+                                status, stream):
+    _check(lib().dpara_verify_greedy_noalloc(_ref(cfg), batch, target_logits, logits_dtype, spine, accept_len, bonus,
+                                             target_argmax, status, stream))
+
+
+def verify_greedy_noalloc(d, logits, spine, accept_len, bonus, target_argmax=None, status=None, stream=None):
+    """verify_greedy without a workspace (the library's static scratch); status: an int32 device
+    tensor the DPARA_STATUS_* bits are OR-ed into, or None."""
+    import torch
+    ldt = DPARA_BF16 if logits.dtype == torch.bfloat16 else DPARA_F32
+    dpara_verify_greedy_noalloc(d.cfg, int(spine.shape[0]), _ptr(logits), ldt, _ptr(spine), _ptr(accept_len),
+                                _ptr(bonus), _ptr(target_argmax), _ptr(status), _stream(stream))
 
 
 def select_and_head(d: DeviceDrafter, reps, accept_len, bonus, gathered, drafts, next_spine, margins,

@@ -198,3 +198,32 @@ def test_head_prepare_validation_without_gpu():
     assert _rc("dpara_head_prepare", R(bad), R(w), FAKE, FAKE, nb, None) in (D.DPARA_E_INVALID,
                                                                            D.DPARA_E_UNSUPPORTED)
     assert "ar_rank" in D.dpara_last_error()
+
+
+def test_trace_and_noalloc_validation_without_gpu():
+    """dpara_backbone_trace needs its residual buffer; dpara_verify_greedy_noalloc rejects calls
+    whose partials exceed its static scratch (1 MiB: at the Qwen3 vocabulary and gamma 16,
+    batch 202 fits and 203 does not) and bad arguments, all before any launch."""
+    s = synth.shrink(synth.QWEN3_8B, n_layers=2)
+    cfg = D.make_config(s)
+    w, _keep = _fake_weights(s)
+    ctx = D.DparaCtx(k=FAKE, v=FAKE, ctx_len=FAKE, batch_cap=2, ctx_cap=2112)
+    need = D.dpara_workspace_bytes(cfg, 2, 2112)
+    R = ctypes.byref
+    assert _rc("dpara_backbone_trace", R(cfg), R(w), R(ctx), 2, FAKE, FAKE, None, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    assert "resid" in D.dpara_last_error()
+    assert _rc("dpara_backbone_trace", R(cfg), R(w), R(ctx), 2, FAKE, FAKE, FAKE + 4, FAKE, need, None) \
+        == D.DPARA_E_INVALID
+    assert _rc("dpara_backbone_trace", R(cfg), R(w), R(ctx), 2, FAKE, FAKE, FAKE, FAKE, need - 1, None) \
+        == D.DPARA_E_WORKSPACE
+    nv = "dpara_verify_greedy_noalloc"
+    assert _rc(nv, R(cfg), 203, FAKE, 1, FAKE, FAKE, FAKE, None, None, None) == D.DPARA_E_WORKSPACE
+    assert "1048576" in D.dpara_last_error()
+    assert _rc(nv, R(cfg), 0, FAKE, 1, FAKE, FAKE, FAKE, None, None, None) == D.DPARA_E_INVALID
+    assert _rc(nv, R(cfg), 1, FAKE, 5, FAKE, FAKE, FAKE, None, None, None) == D.DPARA_E_UNSUPPORTED
+    assert _rc(nv, R(cfg), 1, FAKE, 1, FAKE, FAKE, None, None, None, None) == D.DPARA_E_INVALID
+    assert _rc(nv, R(cfg), 1, FAKE, 1, FAKE, FAKE, FAKE, None, FAKE + 2, None) == D.DPARA_E_INVALID
+    with pytest.raises(D.DparaError) as e:
+        D.dpara_verify_greedy_noalloc(cfg, 203, FAKE, 1, FAKE, FAKE, FAKE, None, None, None)
+    assert e.value.code == D.DPARA_E_WORKSPACE
