@@ -118,6 +118,10 @@ typedef struct dpara_weights {
   const float* ar_w_norm2_max;         /* optional (device, one float): max_v |ar_W[v]|^2 as
                                           dpara_head_prepare writes it; NULL: every head call
                                           computes it (one pass over ar_W) */
+  const float* embed_norm2_max;        /* optional (device, one float): max_v |embed[v]|^2 as
+                                          dpara_candidates_prepare writes it; NULL: every
+                                          dpara_branch_candidates call computes it (one pass
+                                          over embed) */
 } dpara_weights_t;
 
 /* Feature cache C kept as per-layer context K/V (Section 3.3: C over the accepted
@@ -287,10 +291,14 @@ int dpara_head_prepare(const dpara_config_t* cfg, const dpara_weights_t* w, floa
 /* Head variant with every branch's base logits computed off the serial path (Algorithm 1
  * computes the base logits during Precompute).
  * dpara_branch_candidates, issued after the backbone (for instance on its stream, where it
- * overlaps verification), scores every row reps[b][r][i-1] against embed (the tied LM head,
- * float32 rows applied as bf16 hi + lo) and keeps in `cand`, per row, the 16 largest
- * logits and a bound on all the others (the largest remaining logit or the third largest of
- * any 128-column tile, whichever is larger), plus max_v |ar_W[v]|^2.
+ * overlaps verification), ranks every row reps[b][r][i-1] against embed (the tied LM head) by
+ * the row's bf16 part hi = bf16(x) alone, keeps per row the 16 largest of those scores, then
+ * rescores these 16 with the full float32 row (applied as bf16 hi + lo, bit for bit the value
+ * the LM head of dpara_select_and_head computes) and bounds every other logit of the row by the
+ * largest hi score left out (the largest remaining one or the third largest of any
+ * 128-column tile) plus |embed|max (|lo| + 6 hidden 2^-24 (|hi| + |lo|)): the lo part's
+ * share by Cauchy-Schwarz and the float32 rounding of both sums.  It also keeps
+ * max_v |ar_W[v]|^2.
  * cand: device buffer of dpara_branch_candidates_bytes(cfg, batch) bytes, 256-byte aligned;
  *       its layout is private to the library.
  * dpara_select_and_head_cand takes the accepted branch's candidates and produces the same
@@ -298,8 +306,12 @@ int dpara_head_prepare(const dpara_config_t* cfg, const dpara_weights_t* w, floa
  * exact candidate steps; the LM head over the gathered rows and the full head run only if
  * some step is not proven (the int32 at byte offset 4 of `ws` is then nonzero).
  * bf16 drafters with ar_rank in {64, 128, 256}, vocab >= 64 and gamma <= 63 only (else
- * DPARA_E_UNSUPPORTED).  ws: a workspace of dpara_workspace_bytes(cfg, batch, ctx_cap) bytes
- * with ctx_cap >= 64. */
+ * DPARA_E_UNSUPPORTED).  ws: a workspace of
+ * dpara_workspace_bytes(cfg, batch, ctx_cap) bytes with ctx_cap >= 64.
+ * dpara_candidates_prepare writes max_v |embed[v]|^2 into embed_norm2_max (device, one
+ * float): set w->embed_norm2_max to it and later dpara_branch_candidates calls skip their
+ * own pass over embed, with the same results.  ws: dpara_workspace_bytes(cfg, 1, 64) bytes
+ * or more (scratch). */
 size_t dpara_branch_candidates_bytes(const dpara_config_t* cfg, int32_t batch);
 int dpara_branch_candidates(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
                             const float* reps, void* cand, void* ws, size_t ws_bytes, void* stream);
@@ -308,6 +320,8 @@ int dpara_select_and_head_cand(const dpara_config_t* cfg, const dpara_weights_t*
                                const int32_t* bonus, float* gathered, int32_t* drafts,
                                int32_t* next_spine, float* margins, void* ws, size_t ws_bytes,
                                void* stream);
+int dpara_candidates_prepare(const dpara_config_t* cfg, const dpara_weights_t* w, float* embed_norm2_max,
+                             void* ws, size_t ws_bytes, void* stream);
 
 /* Target verification forward, used for the single-GPU overlap of verification and drafting
  * (Algorithm 1, Verify; Section 4.3.2 and Appendix D: both passes on two streams of one GPU).

@@ -117,7 +117,7 @@ struct Plan {
   bool afrag;              // normed activations in MFMA fragment order (QKV and gate/up GEMMs)
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
-      hflag, F, KV32, rope_app, csplit, cpart, spart, plogits, erows;
+      hflag, F, KV32, rope_app, csplit, cpart, cscr, spart, plogits, erows;
   int ar_grid;  // persistent AR head grid (0: step kernels only)
   size_t total;
 };
@@ -203,6 +203,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   const size_t crows = (size_t)B * (c->gamma + 1) * c->gamma;
   p.csplit = take(c->dtype == DPARA_BF16 ? 2 * crows * H * 2 : 0);
   p.cpart = take(c->dtype == DPARA_BF16 ? head_cand_part_bytes(B, c->gamma, c->vocab) : 0);
+  p.cscr = take(c->dtype == DPARA_BF16 ? head_cand_scratch_bytes(B, c->gamma) : 0);
   p.plogits = take((size_t)B * c->gamma * c->vocab * 4);  // sampled head: perturbed logits
   p.erows = take((size_t)B * c->gamma * c->ar_rank * p.esz);  // sampled head: E rows of the previous tokens
   p.total = off;
@@ -1001,15 +1002,33 @@ int dpara_branch_candidates(const dpara_config_t* cfg, const dpara_weights_t* w,
   CHECK_PTR(cand, "cand");
   if (!aligned16(reps)) return fail(DPARA_E_INVALID, "reps is not 16-byte aligned");
   if (((uintptr_t)cand & 255u) != 0) return fail(DPARA_E_INVALID, "cand must be 256-byte aligned");
-  if (cfg->hidden % 4) return fail(DPARA_E_UNSUPPORTED, "hidden must be a multiple of 4");
   const Plan p = make_plan(cfg, batch, 64);
   if (!ws) return fail(DPARA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace must be 256-byte aligned");
   if (ws_bytes < p.total) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, p.total);
   if ((rc = check_device())) return rc;
   HIP_TRY(launch_branch_candidates(batch, cfg->gamma, cfg->hidden, cfg->vocab, cfg->ar_rank, reps, w->embed, w->ar_W,
-                                   cand, at<bf16_t>(ws, p.csplit), at<uint64_t>(ws, p.cpart), (hipStream_t)stream),
+                                   w->embed_norm2_max, cand, at<bf16_t>(ws, p.csplit), at<uint64_t>(ws, p.cpart),
+                                   at<void>(ws, p.cscr), (hipStream_t)stream),
           "branch candidates");
+  return DPARA_OK;
+}
+
+int dpara_candidates_prepare(const dpara_config_t* cfg, const dpara_weights_t* w, float* embed_norm2_max, void* ws,
+                             size_t ws_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (cfg->dtype != DPARA_BF16) return fail(DPARA_E_UNSUPPORTED, "branch candidates need a bf16 drafter");
+  if (!w || !w->embed) return fail(DPARA_E_INVALID, "weights or embed is NULL");
+  CHECK_PTR(embed_norm2_max, "embed_norm2_max");
+  if (!ws || ((uintptr_t)ws & 255u) != 0) return fail(DPARA_E_INVALID, "workspace is NULL or not 256-byte aligned");
+  const Plan p = make_plan(cfg, 1, 64);
+  const size_t need = p.cscr + head_cand_scratch_bytes(1, cfg->gamma);
+  if (ws_bytes < need) return fail(DPARA_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if ((rc = check_device())) return rc;
+  HIP_TRY(launch_embed_prepare(w->embed, cfg->vocab, cfg->hidden, at<float>(ws, p.cscr), embed_norm2_max,
+                               (hipStream_t)stream),
+          "candidates prepare");
   return DPARA_OK;
 }
 

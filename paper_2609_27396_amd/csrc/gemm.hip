@@ -191,37 +191,36 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
   }
 
   if constexpr (EPI == EPI_TOP2) {
-    static_assert(BN == 128, "the top-2 tiles are 128 columns");
-    // Per lane: its columns of each row (FN of them); then the 16 lanes that share the row
-    // (DPP); then the WNW wave columns through LDS, which the K loop no longer uses.
-    Top3 t[FM][4];
+    // One (key1, key2, third value) triple per row and 128-column tile (WPT wave columns each):
+    // per lane over its columns of each row (FN of them); then the 16 lanes that share the
+    // row (DPP); then the tile's wave columns through LDS, which the K loop no longer uses.
+    static_assert(BN % 128 == 0 && 128 % WN == 0, "top-2 tiles are 128 columns of whole wave columns");
+    constexpr int WPT = 128 / WN, QT = BN / 128;
+    __syncthreads();
+    Top3* xs = (Top3*)smem;  // [WNW][BM]
+    // one 16-row block at a time (keeps few triples live beside the accumulators)
 #pragma unroll
     for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        t[mi][r] = Top3{};
+        Top3 t{};
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni) {
           const int col = nt * BN + wn * WN + ni * 16 + lr;
-          if (col < a.N) t[mi][r].add(argmax_key(acc[mi][ni][r], (uint32_t)col));
+          if (col < a.N) t.add(argmax_key(acc[mi][ni][r], (uint32_t)col));
         }
-        t[mi][r] = t[mi][r].row16();
+        t = t.row16();
+        if (lr == 0) xs[wn * BM + wm * WM + mi * 16 + (lane >> 4) * 4 + r] = t;
       }
     __syncthreads();
-    Top3* xs = (Top3*)smem;  // [WNW][BM]
-    if (lr == 0) {
-#pragma unroll
-      for (int mi = 0; mi < FM; ++mi)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) xs[wn * BM + wm * WM + mi * 16 + (lane >> 4) * 4 + r] = t[mi][r];
-    }
-    __syncthreads();
-    for (int lrow = threadIdx.x; lrow < BM; lrow += blockDim.x) {
-      const int row = m0 + lrow;
-      if (row >= a.M) continue;
-      Top3 m = xs[lrow];
-      for (int c = 1; c < WNW; ++c) m = Top3::merge(m, xs[c * BM + lrow]);
-      uint64_t* o = (uint64_t*)a.C + ((int64_t)row * a.ldc + nt) * 3;
+    const int n_tiles = (a.N + 127) / 128;
+    for (int e = threadIdx.x; e < QT * BM; e += blockDim.x) {
+      const int lrow = e % BM, q = e / BM;
+      const int row = m0 + lrow, tile = nt * QT + q;
+      if (row >= a.M || tile >= n_tiles) continue;
+      Top3 m = xs[q * WPT * BM + lrow];
+      for (int c = 1; c < WPT; ++c) m = Top3::merge(m, xs[(q * WPT + c) * BM + lrow]);
+      uint64_t* o = (uint64_t*)a.C + ((int64_t)row * a.ldc + tile) * 3;
       o[0] = m.k1;
       o[1] = m.k2;
       o[2] = (uint64_t)__float_as_uint(m.v3);
@@ -559,18 +558,21 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     }
   }
   if (amode == A_BF16_DUAL) {
-    // Top-2 over every branch row (hundreds to thousands of rows, compute-bound): 96-row
-    // tiles with a 2-deep ring (80 KB of LDS, two workgroups per CU) measured 12-30% faster
-    // on MI355X than one workgroup per CU with a 3-deep ring.
-    if (epi == EPI_TOP2) {
-      if (a.ldc < (a.N + 127) / 128) return hipErrorInvalidValue;
-      return run_pipe<96, 128, 2, 2, 2, 128, EPI_TOP2, 1>(a, st);
-    }
+    if (epi == EPI_TOP2) return hipErrorInvalidValue;
     if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 128, EPI_STORE_F32, 1>(a, st);
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }
-  if (epi == EPI_TOP2) return hipErrorInvalidValue;
+  if (epi == EPI_TOP2) {
+    // Top-2 over every branch row from one bf16 plane.  Measured on MI355X at the Qwen3
+    // vocabulary (272 rows a request): up to 1536 rows 192 x 128 tiles (4 waves of 96 x 64, a
+    // 2-deep ring of 80 KB), 22% faster than the large-M tile at 272 rows and 10% at 1088;
+    // beyond, the large-M tile (256 x 256, 8 waves of 128 x 64, two top-2 tiles per
+    // workgroup), 12% faster at 4352 rows.
+    if (amode != A_BF16 || a.ldc < (a.N + 127) / 128) return hipErrorInvalidValue;
+    if (a.M <= 1536) return run_pipe<192, 128, 2, 2, 2, 128, EPI_TOP2, 0>(a, st);
+    return run_pipe<256, 256, 2, 4, 2, 128, EPI_TOP2, 0>(a, st);
+  }
   if (amode == A_BF16_FRAG) {
     if (epi == EPI_SWIGLU) return run_adir<EPI_SWIGLU>(a, st);
     if (epi == EPI_STORE_F32) return run_adir<EPI_STORE_F32>(a, st);

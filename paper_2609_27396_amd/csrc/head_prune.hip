@@ -44,8 +44,10 @@ namespace {
 constexpr int kTopK = 16;         // candidates kept per row
 constexpr int kKeys = kTopK + 1;  // + the bound key
 constexpr int kCollect = 512;     // collection buffer of the second pass
+constexpr int kHiList = 64;       // hi-plane candidates rescored per branch row (off the serial path)
 constexpr int kMaxGamma = 63;
 constexpr int kMaxSplits = 16;
+constexpr int kEmbedNormParts = 512;  // workgroups of the embedding row-norm pass
 
 // EPL contiguous elements from p as float, in 16-byte (or 8-byte) pieces.
 template <typename T, int EPL>
@@ -184,28 +186,148 @@ __global__ __launch_bounds__(256) void logit_topk(const float* logits, int V, in
   }
 }
 
-// fp32 rows -> bf16 hi + lo planes (hi = bf16(x), lo = bf16(x - hi)), 4 elements a thread.
-__global__ __launch_bounds__(256) void split_hi_lo(const float* X, int64_t n4, bf16_t* hi, bf16_t* lo) {
-  const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (k >= n4) return;
-  const float4 v = ((const float4*)X)[k];
-  const float x[4] = {v.x, v.y, v.z, v.w};
-  bf16_t h[4], l[4];
+// fp32 rows -> bf16 hi + lo planes (hi = bf16(x), lo = bf16(x - hi)), one workgroup per row,
+// and the planes' Euclidean norms (nrm[2 row] = |hi|, nrm[2 row + 1] = |lo|, each rounded up
+// by a factor 1 + 2^-10 that covers the float32 sum of squares of up to 2^13 terms).
+__global__ __launch_bounds__(256) void split_rows_norms(const float* X, int H, bf16_t* hi, bf16_t* lo, float* nrm) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  const float4* xr = (const float4*)(X + row * H);
+  float shi = 0.f, slo = 0.f;
+  for (int k = threadIdx.x; k < H / 4; k += 256) {
+    const float4 v = xr[k];
+    const float x[4] = {v.x, v.y, v.z, v.w};
+    bf16_t h[4], l[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    h[j] = f2bf(x[j]);
-    l[j] = f2bf(x[j] - bf2f(h[j]));
+    for (int j = 0; j < 4; ++j) {
+      h[j] = f2bf(x[j]);
+      const float hf = bf2f(h[j]);
+      l[j] = f2bf(x[j] - hf);
+      const float lf = bf2f(l[j]);
+      shi = fmaf(hf, hf, shi);
+      slo = fmaf(lf, lf, slo);
+    }
+    *(uint2*)(hi + row * H + 4 * k) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+    *(uint2*)(lo + row * H + 4 * k) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
   }
-  *(uint2*)(hi + 4 * k) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
-  *(uint2*)(lo + 4 * k) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+  shi = block_sum256(shi, red);
+  slo = block_sum256(slo, red);
+  if (threadIdx.x == 0) {
+    constexpr float up = 1.0f + 0x1p-10f;
+    nrm[2 * row] = sqrtf(shi) * up;
+    nrm[2 * row + 1] = sqrtf(slo) * up;
+  }
+}
+
+// Per-workgroup maxima of |E_v|^2 over the rows of a [V, H] bf16 matrix (H % 8 == 0), one
+// wave per row at a time.
+__global__ __launch_bounds__(256) void row_norm2_max(const bf16_t* E, int V, int H, float* part) {
+  __shared__ float red[4];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float m = 0.f;
+  for (int v = blockIdx.x * 4 + wave; v < V; v += gridDim.x * 4) {
+    const bf16_t* er = E + (int64_t)v * H;
+    float s = 0.f;
+    for (int k = lane * 8; k < H; k += 512) {
+      const bf16x8_t x = *(const bf16x8_t*)(er + k);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s = fmaf((float)x[j], (float)x[j], s);
+    }
+    m = fmaxf(m, wave_sum(s));
+  }
+  if (lane == 0) red[wave] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// Exact logits of the candidates, from the single-plane (hi) top lists.  One wave per branch
+// row: the row's kHiList hi-plane candidates are rescored with the full row and the kTopK
+// largest exact logits, in descending order, plus a bound key go to the row's slots in
+// `keys`.  Candidate rows of the embedding are the 16 columns of MFMA B operands (one
+// 16-column block per 16 candidates) and the row's hi and lo planes fill every A row, so
+// that each candidate's logit accumulates through exactly the sequence of MFMAs that the
+// two-plane LM head GEMM applies to its element (per 32-deep k chunk in order: hi, then lo,
+// from a zero accumulator): the rescored values are the LM head's, bit for bit.
+// Bound: a v outside the hi list has l_hi_v <= L_hi (the list's own bound, slot kHiList),
+// and
+//   l_v <= l_hi_v + |lo . E_v| + |rounding of both sums|
+//       <= L_hi + |E|max (|lo| + cacc (|hi| + |lo|)),
+// with |lo . E_v| <= |lo| |E_v| (Cauchy-Schwarz) and each float32 sum of n products off by
+// at most 2 n 2^-24 of the sum of their magnitudes (a bound that also holds for truncating
+// adders), which Cauchy-Schwarz bounds by (|hi| + |lo|) |E_v|: cacc = 2 (2H + H) 2^-24.  A v
+// in the list but not among the kTopK exact largest is at most the (kTopK+1)-th exact value.
+// The bound key holds the larger of the two.
+__global__ __launch_bounds__(256) void rescore_candidates(int rows, int H, int V, const bf16_t* hi, const bf16_t* lo,
+                                                          const bf16_t* E, const float* nrm, const float* emax2,
+                                                          float cacc, const uint64_t* hlist, uint64_t* keys) {
+  static_assert(kHiList == 64 && kTopK < kHiList, "one hi-list candidate per lane");
+  constexpr int NB = kHiList / 16;  // 16-column blocks
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= rows) return;  // (no block-wide synchronisation below)
+  const uint64_t* hr = hlist + row * (kHiList + 1);
+  const int j = lane & 15, g4 = lane >> 4;
+  const bf16_t* ep[NB];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const uint64_t kc = hr[c * 16 + j];
+    const uint32_t v = kc ? min(key_index(kc), (uint32_t)(V - 1)) : 0u;
+    ep[c] = E + (int64_t)v * H + g4 * 8;
+  }
+  const bf16_t* hp = hi + row * H + g4 * 8;
+  const bf16_t* lp = lo + row * H + g4 * 8;
+  f32x4_t acc[NB];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int kc = 0; kc < H / 32; ++kc) {
+    const bf16x8_t ah = *(const bf16x8_t*)(hp + kc * 32);
+    const bf16x8_t al = *(const bf16x8_t*)(lp + kc * 32);
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      const bf16x8_t b = *(const bf16x8_t*)(ep[c] + kc * 32);
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc[c], 0, 0, 0);
+      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc[c], 0, 0, 0);
+    }
+  }
+  // every A row is this row, so each lane holds its column's value in every element: lane q
+  // takes candidate q (block g4, column j)
+  float val = acc[0][0];
+#pragma unroll
+  for (int c = 1; c < NB; ++c) val = g4 == c ? acc[c][0] : val;
+  const uint64_t kq = hr[lane];
+  const uint64_t nk = kq ? argmax_key(val, key_index(kq)) : 0;
+  int rank = 0;
+  for (int t = 0; t < kHiList; ++t) {
+    const uint64_t o = ((uint64_t)__shfl((uint32_t)(nk >> 32), t, kWave) << 32) | __shfl((uint32_t)nk, t, kWave);
+    rank += (o > nk) | ((o == nk) & (t < lane));
+  }
+  uint64_t* kr = keys + row * kKeys;
+  if (rank < kTopK) kr[rank] = nk;
+  // the (kTopK+1)-th exact value (-inf if the list holds no more keys)
+  float vk = rank == kTopK && nk ? key_value(nk) : -INFINITY;
+  vk = wave_max(vk);
+  if (lane == 0) {
+    const uint64_t kb = hr[kHiList];
+    float bound = vk;
+    if (kb) {
+      const float e = sqrtf(*emax2) * (1.0f + 0x1p-10f);
+      const float nh = nrm[2 * row], nl = nrm[2 * row + 1];
+      const float delta = e * (nl + cacc * (nh + nl)) * (1.0f + 0x1p-10f);
+      bound = fmaxf(bound, key_value(kb) + delta);
+    }
+    kr[kTopK] = argmax_key(bound, 0xFFFFFFFEu);
+  }
 }
 
 // Per row: the tiles' (key1, key2, third value) triples of the top-2 GEMM epilogue ->
-// the kTopK largest keys of the row and, in slot kTopK, a key whose value bounds every
-// other logit of the row: the largest of the remaining keys and of the tiles' third values
-// (a logit that is not among its tile's two largest is at most that tile's third value).
-// Fewer than kTopK keys (a vocabulary of few tiles) leave zero keys, which never win.
+// the N largest keys of the row and, in slot N, a key whose value bounds every other logit
+// of the row: the largest of the remaining keys and of the tiles' third values (a logit
+// that is not among its tile's two largest is at most that tile's third value).  Fewer than
+// N keys (a vocabulary of few tiles) leave zero keys, which never win.
+template <int N>
 __global__ __launch_bounds__(256) void tile_top2_merge(const uint64_t* part, int NT, uint64_t* out, int* flag) {
+  static_assert(N < 256 && N < kCollect, "the threshold is a rank among 256 thread maxima");
   __shared__ __attribute__((aligned(16))) uint64_t tm[256];
   __shared__ uint64_t buf[kCollect];
   __shared__ float red[4];
@@ -233,9 +355,9 @@ __global__ __launch_bounds__(256) void tile_top2_merge(const uint64_t* part, int
     const uint4 u = *(const uint4*)&tm[j];
     r += (((uint64_t)u.y << 32 | u.x) > best) + (((uint64_t)u.w << 32 | u.z) > best);
   }
-  if (r == kTopK && best != 0) thr = best;
+  if (r == N && best != 0) thr = best;
   __syncthreads();
-  const uint64_t T = thr;  // 0: fewer than kKeys tiles hold a key; then every key is taken
+  const uint64_t T = thr;  // 0: fewer than N + 1 threads hold a key; then every key is taken
   for (int t = tid; t < NT; t += 256)
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -247,24 +369,24 @@ __global__ __launch_bounds__(256) void tile_top2_merge(const uint64_t* part, int
     }
   __syncthreads();
   const int n = cnt;
-  uint64_t* o = out + (int64_t)row * kKeys;
+  uint64_t* o = out + (int64_t)row * (N + 1);
   if (n > kCollect) {
     if (tid == 0) atomicOr(flag, 1);
     return;
   }
-  for (int e = tid; e < kKeys; e += 256) o[e] = 0;
+  for (int e = tid; e <= N; e += 256) o[e] = 0;
   __syncthreads();
   for (int e = tid; e < n; e += 256) {
     const uint64_t k = buf[e];
     int rr = 0;
     for (int j = 0; j < n; ++j) rr += buf[j] > k;
-    if (rr < kKeys) o[rr] = k;
+    if (rr <= N) o[rr] = k;
   }
   __syncthreads();
   if (tid == 0) {
     float bound = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    if (n > kTopK) bound = fmaxf(bound, key_value(o[kTopK]));
-    o[kTopK] = argmax_key(bound, 0xFFFFFFFEu);
+    if (n > N) bound = fmaxf(bound, key_value(o[N]));
+    o[N] = argmax_key(bound, 0xFFFFFFFEu);
   }
 }
 
@@ -565,23 +687,36 @@ size_t head_cand_bytes(int B, int gamma) { return 4096 + (size_t)B * (gamma + 1)
 size_t head_cand_part_bytes(int B, int gamma, int V) { return (size_t)B * (gamma + 1) * gamma * ((V + 127) / 128) * 24; }
 
 hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
-                                    const void* W, void* cand, bf16_t* split, uint64_t* part, hipStream_t st) {
-  if (!head_prune_supported(1, gamma, V, rank) || B < 1 || H % 4) return hipErrorNotSupported;
+                                    const void* W, const float* emax2_pre, void* cand, bf16_t* split, uint64_t* part,
+                                    void* scratch, hipStream_t st) {
+  if (!head_prune_supported(1, gamma, V, rank) || B < 1 || H % 64) return hipErrorNotSupported;
   int* overflow = (int*)cand;
   float* wpart = (float*)((unsigned char*)cand + 256);
   uint64_t* keys = (uint64_t*)((unsigned char*)cand + 4096);
   const int rows = B * (gamma + 1) * gamma;
   const int NT = (V + 127) / 128;
+  bf16_t* hi = split;
+  bf16_t* lo = split + (int64_t)rows * H;
+  // scratch: the hi lists (kHiList + 1 keys a row), then |hi|, |lo| a row, then the
+  // embedding norm partials and their maximum
+  uint64_t* hlist = (uint64_t*)scratch;
+  float* nrm = (float*)(hlist + (int64_t)rows * (kHiList + 1));
+  float* eparts = nrm + 2 * (int64_t)rows;
   Phase ph("lm_head", st);
-  const int64_t n4 = (int64_t)rows * H / 4;
-  hipLaunchKernelGGL(split_hi_lo, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, st, reps, n4, split,
-                     split + (int64_t)rows * H);
+  hipLaunchKernelGGL(split_rows_norms, dim3(rows), dim3(256), 0, st, reps, H, hi, lo, nrm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if ((e = launch_wnorm(1, rank, W, V, wpart, overflow, st)) != hipSuccess) return e;  // also clears `overflow`
+  const float* emax2 = emax2_pre;
+  if (!emax2) {  // one pass over the embedding
+    hipLaunchKernelGGL(row_norm2_max, dim3(kEmbedNormParts), dim3(256), 0, st, (const bf16_t*)embed, V, H, eparts);
+    hipLaunchKernelGGL(max_of, dim3(1), dim3(256), 0, st, eparts, kEmbedNormParts, eparts + kEmbedNormParts);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    emax2 = eparts + kEmbedNormParts;
+  }
+  // top lists from the hi plane alone: half the work of the two-plane product
   GemmArgs g{};
-  g.A = split;
-  g.lo_off = (int64_t)rows * H;
+  g.A = hi;
   g.lda = H;
   g.B0 = g.B1 = g.B2 = embed;
   g.n1 = g.n2 = V;
@@ -590,8 +725,23 @@ hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, co
   g.K = H;
   g.C = part;
   g.ldc = NT;
-  if ((e = launch_gemm(A_BF16_DUAL, EPI_TOP2, g, st)) != hipSuccess) return e;
-  hipLaunchKernelGGL(tile_top2_merge, dim3(rows), dim3(256), 0, st, part, NT, keys, overflow);
+  if ((e = launch_gemm(A_BF16, EPI_TOP2, g, st)) != hipSuccess) return e;
+  hipLaunchKernelGGL(tile_top2_merge<kHiList>, dim3(rows), dim3(256), 0, st, part, NT, hlist, overflow);
+  const float cacc = (float)(6.0 * H / 16777216.0);
+  hipLaunchKernelGGL(rescore_candidates, dim3((rows + 3) / 4), dim3(256), 0, st, rows, H, V, hi, lo,
+                     (const bf16_t*)embed, nrm, emax2, cacc, hlist, keys);
+  return hipGetLastError();
+}
+
+size_t head_cand_scratch_bytes(int B, int gamma) {
+  const size_t rows = (size_t)B * (gamma + 1) * gamma;
+  return rows * (kHiList + 1) * 8 + (rows * 2 + kEmbedNormParts + 1) * 4;
+}
+
+hipError_t launch_embed_prepare(const void* embed, int V, int H, float* parts, float* out, hipStream_t st) {
+  if (H % 8) return hipErrorNotSupported;
+  hipLaunchKernelGGL(row_norm2_max, dim3(kEmbedNormParts), dim3(256), 0, st, (const bf16_t*)embed, V, H, parts);
+  hipLaunchKernelGGL(max_of, dim3(1), dim3(256), 0, st, parts, kEmbedNormParts, out);
   return hipGetLastError();
 }
 

@@ -53,7 +53,7 @@ struct GemmArgs {
   int splits = 1;  // split-K: S >= 1 fp32 planes of C (plane stride M*ldc); EPI_STORE_F32 only
   // EPI_SWIGLU: B0 = gate [N, K], B1 = up [N, K], C = bf16/f32 [M, N] of silu(g) * u,
   // where N is the FFN width.
-  // EPI_TOP2 (A_BF16_DUAL only): instead of C, per row and 128-column tile t the two largest
+  // EPI_TOP2 (A_BF16 only): instead of C, per row and 128-column tile t the two largest
   // (value, column) argmax keys of the row's tile and the third largest value, as three
   // uint64 words at C + (row * ldc + t) * 3 (the value's float bits in the low word);
   // columns past N do not count.  ldc >= ceil(N / 128).
@@ -224,11 +224,19 @@ hipError_t launch_draft_scores(int dtype, int B, int gamma, int V, int rank, con
 // Candidates of every branch row, off the serial path (bf16): reps [B, gamma+1, gamma, H]
 // fp32 -> `cand` (head_cand_bytes: a 4 KB header with an overflow flag at 0 and the
 // |W_v|^2 maxima at byte 256, then kTopK+1 keys per row); `split` holds 2 * rows * H bf16,
-// `part` head_cand_part_bytes.  The serial step then takes the accepted branch's rows.
+// `part` head_cand_part_bytes, `scratch` head_cand_scratch_bytes (8-byte aligned).  The top
+// lists come from the hi plane of each row; their candidates are then rescored exactly and
+// the bound widened by the lo plane's and the rounding's share.  emax2_pre: max_v |embed_v|^2 (one float, device) as
+// launch_embed_prepare writes it, or NULL (one pass over the embedding per call).  The serial
+// step then takes the accepted branch's rows.
 size_t head_cand_bytes(int B, int gamma);
 size_t head_cand_part_bytes(int B, int gamma, int V);
+size_t head_cand_scratch_bytes(int B, int gamma);
 hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
-                                    const void* W, void* cand, bf16_t* split, uint64_t* part, hipStream_t st);
+                                    const void* W, const float* emax2_pre, void* cand, bf16_t* split, uint64_t* part,
+                                    void* scratch, hipStream_t st);
+// max_v |embed_v|^2 of a [V, H] bf16 matrix into out (one float); parts: 512 floats of scratch.
+hipError_t launch_embed_prepare(const void* embed, int V, int H, float* parts, float* out, hipStream_t st);
 hipError_t launch_head_from_candidates(int B, int gamma, int V, int rank, const void* cand, const void* E,
                                        const void* W, const int* accept_len, const int* bonus, int* drafts,
                                        int* next_spine, float* margins, int* flag, int* status, hipStream_t st);

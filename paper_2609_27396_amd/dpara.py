@@ -28,7 +28,7 @@ EXPORTS = ("dpara_workspace_bytes", "dpara_ctx_append", "dpara_backbone_all_boun
            "dpara_target_workspace_bytes", "dpara_target_forward", "dpara_target_forward_hidden",
            "dpara_fuse_workspace_bytes", "dpara_fuse_features", "dpara_select_and_head_sampled",
            "dpara_verify_sampled", "dpara_head_prepare", "dpara_backbone_trace",
-           "dpara_verify_greedy_noalloc")
+           "dpara_verify_greedy_noalloc", "dpara_candidates_prepare")
 
 PHASES = ("append_gemm", "append_store", "assemble", "rmsnorm", "qkv_gemm", "qk_norm_rope", "attn_ctx",
           "attn_merge", "o_gemm", "gateup_gemm", "down_gemm", "final_norm", "verify", "gather", "lm_head",
@@ -57,7 +57,8 @@ class DparaLayerWeights(ctypes.Structure):
 class DparaWeights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("mask_emb", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
                 ("ar_E", ctypes.c_void_p), ("ar_W", ctypes.c_void_p),
-                ("layers", ctypes.POINTER(DparaLayerWeights)), ("ar_w_norm2_max", ctypes.c_void_p)]
+                ("layers", ctypes.POINTER(DparaLayerWeights)), ("ar_w_norm2_max", ctypes.c_void_p),
+                ("embed_norm2_max", ctypes.c_void_p)]
 
 
 class DparaTargetWeights(ctypes.Structure):
@@ -116,6 +117,7 @@ def lib():
                                                     VP, F32, U64, VP, VP, VP, SZ, VP]
         L.dpara_verify_sampled.argtypes = [P(DparaConfig), I32, VP, I32, VP, VP, F32, U64, VP, VP, VP, VP, SZ, VP]
         L.dpara_head_prepare.argtypes = [P(DparaConfig), P(DparaWeights), VP, VP, SZ, VP]
+        L.dpara_candidates_prepare.argtypes = [P(DparaConfig), P(DparaWeights), VP, VP, SZ, VP]
         L.dpara_last_error.restype = ctypes.c_char_p
         L.dpara_version.restype = I32
         L.dpara_profile_enable.argtypes = [I32]
@@ -125,7 +127,8 @@ def lib():
                      "dpara_clear_status", "dpara_profile_enable",
                      "dpara_profile_read", "dpara_target_forward", "dpara_fuse_features",
                      "dpara_target_forward_hidden", "dpara_select_and_head_sampled", "dpara_verify_sampled",
-                     "dpara_head_prepare", "dpara_backbone_trace", "dpara_verify_greedy_noalloc"):
+                     "dpara_head_prepare", "dpara_backbone_trace", "dpara_verify_greedy_noalloc",
+                     "dpara_candidates_prepare"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -276,6 +279,18 @@ class DeviceDrafter:
 
     def unprepare_head(self):
         self.w.ar_w_norm2_max = None
+
+    def prepare_candidates(self, ws, stream=None):
+        """Compute max_v |embed[v]|^2 once (dpara_candidates_prepare) and point the weights at
+        it, so dpara_branch_candidates calls skip their own pass over the embedding."""
+        import torch
+        self.enorm2 = torch.empty(1, dtype=torch.float32, device=self.device)
+        _check(lib().dpara_candidates_prepare(_ref(self.cfg), _ref(self.w), _ptr(self.enorm2), ws.ptr, ws.nbytes,
+                                              _stream(stream)))
+        self.w.embed_norm2_max = _ptr(self.enorm2)
+
+    def unprepare_candidates(self):
+        self.w.embed_norm2_max = None
 
 
 class DeviceTarget:

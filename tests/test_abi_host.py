@@ -2,6 +2,7 @@
 
 These run without a GPU: every call here fails validation before any HIP call."""
 import ctypes
+import dataclasses
 import os
 import re
 
@@ -198,6 +199,23 @@ def test_head_prepare_validation_without_gpu():
     assert _rc("dpara_head_prepare", R(bad), R(w), FAKE, FAKE, nb, None) in (D.DPARA_E_INVALID,
                                                                            D.DPARA_E_UNSUPPORTED)
     assert "ar_rank" in D.dpara_last_error()
+
+
+def test_candidates_prepare_validation_without_gpu():
+    """dpara_candidates_prepare rejects a missing output, a missing, misaligned or small
+    workspace and a float32 drafter on the host, before any launch."""
+    shape = synth.QWEN3_8B
+    cfg = D.make_config(shape)
+    w, _layers = _fake_weights(shape)
+    R = ctypes.byref
+    nb = D.dpara_workspace_bytes(cfg, 1, 64)
+    assert _rc("dpara_candidates_prepare", R(cfg), R(w), None, FAKE, nb, None) == D.DPARA_E_INVALID
+    assert "embed_norm2_max" in D.dpara_last_error()
+    assert _rc("dpara_candidates_prepare", R(cfg), R(w), FAKE, None, nb, None) == D.DPARA_E_INVALID
+    assert _rc("dpara_candidates_prepare", R(cfg), R(w), FAKE, FAKE + 16, nb, None) == D.DPARA_E_INVALID
+    assert _rc("dpara_candidates_prepare", R(cfg), R(w), FAKE, FAKE, 1024, None) == D.DPARA_E_WORKSPACE
+    f32 = D.make_config(dataclasses.replace(shape, dtype="f32"))
+    assert _rc("dpara_candidates_prepare", R(f32), R(w), FAKE, FAKE, nb, None) == D.DPARA_E_UNSUPPORTED
 
 
 def test_trace_and_noalloc_validation_without_gpu():
