@@ -63,15 +63,14 @@ __device__ __forceinline__ int key_perm(int kb, int i) { return (kb >> 1) * 32 +
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
-__device__ __forceinline__ uint4 as_u4(bf16x8_t v) { return __builtin_bit_cast(uint4, v); }
 
 // The K and V^T tiles of a 64-key block are filled by direct global->LDS DMA
 // (global_load_lds_dwordx4: lane i's 16 bytes land at M0 + 16*i), through a ring of
 // STAGES stages: STAGES-1 blocks are in flight while one is consumed.  Every load is a
 // full 16-byte chunk: the context cache and the in-block buffers hold a multiple of 64
 // keys, so a block never reads past its buffer; keys past the valid count are excluded
-// from the scores by the mask, and their V^T entries are zeroed in the operand (a tail
-// block only) so that stale memory cannot turn 0 * V into NaN.
+// from the scores by the mask, and their V^T entries are zeroed in LDS (a tail block
+// only) so that stale memory cannot turn 0 * V into NaN.
 //
 // Workgroup = NW waves x U 16-row query tiles per wave.  Fragment reads: the K operand
 // row of MFMA block kb for lane lq is key_perm(kb, lq), whose swizzle depends on lq only
@@ -116,28 +115,32 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
   const bf16_t* Vg = (const bf16_t*)a.Vc + kvbase * HD * a.cap;
   const bf16_t* Kin = (const bf16_t*)a.Kb + kvbase * a.Rp * HD;
   const bf16_t* Vin = (const bf16_t*)a.Vb + kvbase * HD * a.Rp;
+  // Per-lane byte offsets of this wave's DMA chunks within a block (instruction j fills tile
+  // chunks (wave + NW*j)*64 + lane of K and of V^T); the block's base address is uniform.
+  int koff[NINS], voff_ctx[NINS], voff_in[NINS];
+#pragma unroll
+  for (int j = 0; j < NINS; ++j) {
+    const int idx = (wave + NW * j) * 64 + lane;
+    const int r = idx / (HD / 8), c = idx % (HD / 8);
+    koff[j] = (r * HD + k_swz<HD>(r, c) * 8) * 2;
+    const int d = idx / (kKeyBlock / 8), cv = idx % (kKeyBlock / 8);
+    voff_ctx[j] = (d * a.cap + v_swz(d, cv) * 8) * 2;
+    voff_in[j] = (d * a.Rp + v_swz(d, cv) * 8) * 2;
+  }
   auto issue = [&](int vb, int stage) {
     const bool inblk = vb >= nb_ctx;
     const int kb0 = (inblk ? vb - nb_ctx : vb) * kKeyBlock;
-    const bf16_t* Ks = (inblk ? Kin : Kg) + (int64_t)kb0 * HD;
-    const bf16_t* Vs = (inblk ? Vin : Vg) + kb0;
-    const int vstride = inblk ? a.Rp : a.cap;
+    const char* Ks = (const char*)((inblk ? Kin : Kg) + (int64_t)kb0 * HD);
+    const char* Vs = (const char*)((inblk ? Vin : Vg) + kb0);
     unsigned char* sb = smem + stage * STAGE_BYTES;
-    // instruction j of this wave fills tile chunks (wave + NW*j)*64 + lane of K and of V^T
 #pragma unroll
-    for (int j = 0; j < NINS; ++j) {
-      const int idx = (wave + NW * j) * 64 + lane;
-      const int r = idx / (HD / 8), c = idx % (HD / 8);
-      __builtin_amdgcn_global_load_lds((const void*)(Ks + r * HD + k_swz<HD>(r, c) * 8),
-                                       (lds_void_t*)(sb + (wave + NW * j) * 1024), 16, 0, 0);
-    }
+    for (int j = 0; j < NINS; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(Ks + koff[j]), (lds_void_t*)(sb + (wave + NW * j) * 1024), 16,
+                                       0, 0);
 #pragma unroll
-    for (int j = 0; j < NINS; ++j) {
-      const int idx = (wave + NW * j) * 64 + lane;
-      const int d = idx / (kKeyBlock / 8), c = idx % (kKeyBlock / 8);
-      __builtin_amdgcn_global_load_lds((const void*)(Vs + d * vstride + v_swz(d, c) * 8),
+    for (int j = 0; j < NINS; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(Vs + (inblk ? voff_in[j] : voff_ctx[j])),
                                        (lds_void_t*)(sb + K_BYTES + (wave + NW * j) * 1024), 16, 0, 0);
-    }
   };
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
@@ -190,13 +193,38 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     if (i + STAGES - 1 < n_blk) issue(vb_begin + i + STAGES - 1, (i + STAGES - 1) % STAGES);
-    if (!wave_live) continue;
-
     const unsigned char* sb = smem + (i % STAGES) * STAGE_BYTES;
     const int vb = vb_begin + i;
     const bool inblk = vb >= nb_ctx;
     const int kb0 = (inblk ? vb - nb_ctx : vb) * kKeyBlock;
     const int kend = inblk ? a.R : L;
+    if (kb0 + kKeyBlock > kend) {
+      // A tail block (at most two per workgroup, a uniform branch): zero the V^T entries of
+      // keys >= kend in LDS, so that stale memory past the valid keys cannot turn 0 * V into
+      // NaN, and every block then takes the same PV code (one PV path keeps the accumulators
+      // in one set of registers: 116 VGPRs, two workgroups per CU).  Thread t owns the CPT
+      // consecutive 16-byte chunks from t * CPT of the tile (8 chunks a V^T row).
+      static_assert((HD * 8) % (NW * 64) == 0, "the V^T tile's chunks split evenly over the threads");
+      constexpr int CPT = HD * 8 / (NW * 64);  // chunks per thread
+      unsigned char* vt = smem + (i % STAGES) * STAGE_BYTES + K_BYTES;
+#pragma unroll
+      for (int q = 0; q < CPT; ++q) {
+        const int e = threadIdx.x * CPT + q;  // chunk e of the tile: row e / 8, chunk e % 8
+        const int d = e >> 3, c = e & 7;
+        const int nv = kend - (kb0 + c * 8);  // valid keys in this chunk (may be <= 0 or >= 8)
+        if (nv < 8) {
+          uint4* cp = (uint4*)(vt + d * kKeyBlock * 2 + v_swz(d, c) * 16);
+          uint4 x = *cp;
+          x.x &= (0 < nv ? 0xFFFFu : 0u) | (1 < nv ? 0xFFFF0000u : 0u);
+          x.y &= (2 < nv ? 0xFFFFu : 0u) | (3 < nv ? 0xFFFF0000u : 0u);
+          x.z &= (4 < nv ? 0xFFFFu : 0u) | (5 < nv ? 0xFFFF0000u : 0u);
+          x.w &= (6 < nv ? 0xFFFFu : 0u) | (7 < nv ? 0xFFFF0000u : 0u);
+          *cp = x;
+        }
+      }
+      __syncthreads();
+    }
+    if (!wave_live) continue;
 
     // S^T blocks: s[u][kb][r] = score(key kb0 + key_perm(kb, 4*g4 + r), query qi[u])
     f32x4_t s[U][4];
@@ -276,32 +304,19 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
       m_run[u] = m_new;
     }
     // O^T += V^T P^T over 64 keys = 2 k-steps of 32.
-    auto pv = [&](auto zero_tail) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const unsigned char* vp = sb + K_BYTES + v_lane + ((t * 4 + g4) ^ vx) * 16;
+    for (int t = 0; t < 2; ++t) {
+      const unsigned char* vp = sb + K_BYTES + v_lane + ((t * 4 + g4) ^ vx) * 16;
 #pragma unroll
-        for (int hb = 0; hb < NHB; ++hb) {
-          bf16x8_t vf = *(const bf16x8_t*)(vp + hb * 16 * kKeyBlock * 2);
-          if constexpr (decltype(zero_tail)::value) {  // zero V^T entries of keys >= kend
-            const int nv = kend - (kb0 + t * 32 + g4 * 8);
-            uint4 x = as_u4(vf);
-            x.x &= (0 < nv ? 0xFFFFu : 0u) | (1 < nv ? 0xFFFF0000u : 0u);
-            x.y &= (2 < nv ? 0xFFFFu : 0u) | (3 < nv ? 0xFFFF0000u : 0u);
-            x.z &= (4 < nv ? 0xFFFFu : 0u) | (5 < nv ? 0xFFFF0000u : 0u);
-            x.w &= (6 < nv ? 0xFFFFu : 0u) | (7 < nv ? 0xFFFF0000u : 0u);
-            vf = as_bf16x8(x);
-          }
+      for (int hb = 0; hb < NHB; ++hb) {
+        const bf16x8_t vf = *(const bf16x8_t*)(vp + hb * 16 * kKeyBlock * 2);
 #pragma unroll
-          for (int u = 0; u < U; ++u) {
-            o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][t], o[u][hb], 0, 0, 0);
-            o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[u][t], o[u][hb], 0, 0, 0);
-          }
+        for (int u = 0; u < U; ++u) {
+          o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][t], o[u][hb], 0, 0, 0);
+          o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[u][t], o[u][hb], 0, 0, 0);
         }
       }
-    };
-    if (kb0 + kKeyBlock > kend) pv(std::true_type{});
-    else pv(std::false_type{});
+    }
   }
 
 #pragma unroll
