@@ -16,7 +16,11 @@ namespace dpara {
 namespace {
 
 
-__device__ __forceinline__ float silu_f(float g) { return g / (1.0f + expf(-g)); }
+// silu(g) = g / (1 + e^-g) from the hardware exp2 and reciprocal (about 1 ulp each, far below
+// the bf16 rounding of the result; e^-g -> inf for very negative g gives g * 0 = -0).
+__device__ __forceinline__ float silu_f(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g * -1.4426950408889634f));
+}
 
 // Logical tile for physical workgroup p: tiles are split into 8 contiguous ranges, one per
 // XCD (workgroups are dispatched round-robin over the 8 XCDs), M fastest inside a range.
@@ -145,48 +149,52 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int KT = Ks / KB;
+  const int lr = lane & 15, lc = lane >> 4;
+  // Fragments of k-step ks (32 deep) of the stage in ring slot `slot`.
+  auto load_frags = [&](int slot, int ks, bf16x8_t(&af)[NPL][FM], bf16x8_t(&bf)[FN]) {
+    const unsigned char* sa = smem + slot * STAGE_BYTES;
+    const unsigned char* sb = sa + A_ROWS * BKB;
+    const int c = ks * 4 + lc;
+#pragma unroll
+    for (int ni = 0; ni < FN; ++ni) {
+      const int r = b_frag_row<BN, WN, FN, EPI>(wn, ni) + lr;
+      bf[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
+    }
+#pragma unroll
+    for (int pl = 0; pl < NPL; ++pl)
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi) {
+        const int r = pl * BM + wm * WM + mi * 16 + lr;
+        af[pl][mi] = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
+      }
+  };
+  auto mfmas = [&](const bf16x8_t(&af)[NPL][FM], const bf16x8_t(&bf)[FN]) {
+#pragma unroll
+    for (int pl = 0; pl < NPL; ++pl)
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[pl][mi], bf[ni], acc[mi][ni], 0, 0, 0);
+  };
+  bf16x8_t af[2][NPL][FM], bfr[2][FN];  // two register sets, declared once for the whole loop
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < KT) issue(st, st);
-  const int lr = lane & 15, lc = lane >> 4;
   for (int kt = 0; kt < KT; ++kt) {
     if (kt + STAGES - 2 < KT) wait_vmcnt<(STAGES - 2) * (A_INS + B_INS)>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    const unsigned char* sa = smem + (kt % STAGES) * STAGE_BYTES;
-    const unsigned char* sb = sa + A_ROWS * BKB;
     // Fragments of k-step ks+1 are read from LDS before k-step ks's MFMAs are issued (two
     // register sets), so the LDS latency hides behind the math.
-    auto load_frags = [&](int ks, bf16x8_t(&af)[NPL][FM], bf16x8_t(&bf)[FN]) {
-      const int c = ks * 4 + lc;
-#pragma unroll
-      for (int ni = 0; ni < FN; ++ni) {
-        const int r = b_frag_row<BN, WN, FN, EPI>(wn, ni) + lr;
-        bf[ni] = *(const bf16x8_t*)(sb + r * BKB + swz<CH>(r, c) * 16);
-      }
-#pragma unroll
-      for (int pl = 0; pl < NPL; ++pl)
-#pragma unroll
-        for (int mi = 0; mi < FM; ++mi) {
-          const int r = pl * BM + wm * WM + mi * 16 + lr;
-          af[pl][mi] = *(const bf16x8_t*)(sa + r * BKB + swz<CH>(r, c) * 16);
-        }
-    };
-    bf16x8_t af[2][NPL][FM], bfr[2][FN];
-    load_frags(0, af[0], bfr[0]);
+    load_frags(kt % STAGES, 0, af[0], bfr[0]);
 #pragma unroll
     for (int ks = 0; ks < KB / 32; ++ks) {
       const int cur = ks & 1;
-      if (ks + 1 < KB / 32) load_frags(ks + 1, af[cur ^ 1], bfr[cur ^ 1]);
+      if (ks + 1 < KB / 32) load_frags(kt % STAGES, ks + 1, af[cur ^ 1], bfr[cur ^ 1]);
       __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of this step's MFMAs
-#pragma unroll
-      for (int pl = 0; pl < NPL; ++pl)
-#pragma unroll
-        for (int mi = 0; mi < FM; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < FN; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[cur][pl][mi], bfr[cur][ni], acc[mi][ni], 0, 0, 0);
+      mfmas(af[cur], bfr[cur]);
     }
   }
 
