@@ -142,6 +142,7 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
       __builtin_amdgcn_global_load_lds((const void*)(Vs + (inblk ? voff_in[j] : voff_ctx[j])),
                                        (lds_void_t*)(sb + K_BYTES + (wave + NW * j) * 1024), 16, 0, 0);
   };
+  debug_poison_lds<STAGES * STAGE_BYTES>(smem);
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < n_blk) issue(vb_begin + st, st);

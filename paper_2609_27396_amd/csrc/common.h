@@ -66,6 +66,23 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
 // Generic LDS pointer type of the direct global->LDS DMA builtin.
 typedef __attribute__((address_space(3))) void lds_void_t;
 
+// Debug builds (DPARA_DEBUG_LDS_POISON=1) fill a kernel's LDS ring with NaN bit patterns
+// before its first DMA, so that a fragment read of any LDS byte the DMA did not write turns
+// the outputs into NaN, which the parity tests catch.  The fill completes (waitcnt + barrier)
+// before the first DMA is issued.  A no-op otherwise.
+#ifndef DPARA_DEBUG_LDS_POISON
+#define DPARA_DEBUG_LDS_POISON 0
+#endif
+template <int BYTES>
+__device__ __forceinline__ void debug_poison_lds(unsigned char* smem) {
+  if constexpr (DPARA_DEBUG_LDS_POISON != 0) {
+    static_assert(BYTES % 16 == 0, "the ring is a whole number of 16-byte chunks");
+    for (int i = threadIdx.x; i < BYTES / 16; i += blockDim.x)
+      ((uint4*)smem)[i] = make_uint4(0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu);
+    __syncthreads();
+  }
+}
+
 // Wait until at most N vector-memory loads (DMA included) of this wave are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {

@@ -150,6 +150,7 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
 
   const int KT = Ks / KB;
   const int lr = lane & 15, lc = lane >> 4;
+  debug_poison_lds<STAGES * STAGE_BYTES>(smem);
   // Fragments of k-step ks (32 deep) of the stage in ring slot `slot`.
   auto load_frags = [&](int slot, int ks, bf16x8_t(&af)[NPL][FM], bf16x8_t(&bf)[FN]) {
     const unsigned char* sa = smem + slot * STAGE_BYTES;
@@ -342,6 +343,7 @@ __global__ __launch_bounds__(256) void gemm_adir_kernel(GemmArgs a, int NT) {
   // past the end the refill repeats the last step into a slot nobody reads again.
   constexpr int PER = KS * FM + B_INS;  // vector memory instructions per issue
   const int KT = Ks / KB;
+  debug_poison_lds<SB * STAGE_BYTES>(smem);
 #pragma unroll
   for (int s = 0; s < SB - 1; ++s) issue(s, s, s);
   for (int kt0 = 0; kt0 < KT; kt0 += SB) {

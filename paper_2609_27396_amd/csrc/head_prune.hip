@@ -279,7 +279,6 @@ __global__ __launch_bounds__(256) void rescore_candidates(int rows, int H, int V
   f32x4_t acc[NB];
 #pragma unroll
   for (int c = 0; c < NB; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
   for (int kc = 0; kc < H / 32; ++kc) {
     const bf16x8_t ah = *(const bf16x8_t*)(hp + kc * 32);
     const bf16x8_t al = *(const bf16x8_t*)(lp + kc * 32);

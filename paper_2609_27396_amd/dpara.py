@@ -15,7 +15,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libdpara.so")
+# DPARA_LIB_PATH selects another build of the same library (the tests load the host-sanitized
+# libdpara_asan.so through it); the default is the in-tree libdpara.so.
+LIB_PATH = os.environ.get("DPARA_LIB_PATH") or os.path.join(_HERE, "libdpara.so")
 
 DPARA_OK, DPARA_E_INVALID, DPARA_E_UNSUPPORTED, DPARA_E_WORKSPACE, DPARA_E_CAPACITY, DPARA_E_HIP = 0, -1, -2, -3, -4, -5
 DPARA_F32, DPARA_BF16 = 0, 1
