@@ -66,6 +66,15 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
 // Generic LDS pointer type of the direct global->LDS DMA builtin.
 typedef __attribute__((address_space(3))) void lds_void_t;
 
+// Row layout of one request (Section 3.2): rows 0..gamma are the spine t_0..t_gamma;
+// row gamma+1 + r*gamma + (i-1) is mask i of branch r.  Position offset from the
+// context length: spine j -> j; branch r mask i -> r + i.
+__device__ __forceinline__ int row_pos_offset(int row, int gamma) {
+  if (row <= gamma) return row;
+  const int k = row - gamma - 1;
+  return k / gamma + k % gamma + 1;
+}
+
 // Debug builds (DPARA_DEBUG_LDS_POISON=1) fill a kernel's LDS ring with NaN bit patterns
 // before its first DMA, so that a fragment read of any LDS byte the DMA did not write turns
 // the outputs into NaN, which the parity tests catch.  The fill completes (waitcnt + barrier)

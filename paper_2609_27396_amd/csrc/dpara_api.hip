@@ -115,6 +115,7 @@ struct Plan {
   int B, R, Rp, M, S, chunk, CH, esz;
   int s_qkv, s_o, s_down;  // split-K planes of the QKV, O and down projections
   bool afrag;              // normed activations in MFMA fragment order (QKV and gate/up GEMMs)
+  bool qkv_fused;          // the QKV GEMM applies q/k-norm and RoPE in its epilogue
   int v_chunk, v_chunks, h_chunk, h_chunks;
   size_t X, A, QKV, Q, Kb, Vb, Opart, ML, O, Hmid, P, rope, vpart, G, Gsplit, logits, hpart, arpart, hcand, hwpart,
       hflag, F, KV32, rope_app, csplit, cpart, cscr, spart, plogits, erows;
@@ -158,6 +159,7 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   // Up to 320 rows the GEMMs fed by an RMSNorm read their activations in fragment order.
   p.afrag = c->dtype == DPARA_BF16 && p.M <= 320 && H % 256 == 0;
   p.s_qkv = gemm_splits(p.afrag ? A_BF16_FRAG : amode, EPI_STORE_F32, p.M, (nq + 2 * nkv) * hd, H);
+  p.qkv_fused = c->dtype == DPARA_BF16 && hd == 128 && p.M > 1024 && p.s_qkv == 1;
   p.s_o = gemm_splits(amode, EPI_STORE_F32, p.M, H, nq * hd);
   p.s_down = gemm_splits(amode, EPI_STORE_F32, p.M, H, c->ffn);
   const size_t M = p.M;
@@ -329,16 +331,34 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
     q.C = at<void>(ws, p.QKV);
     q.ldc = q.N;
     q.splits = p.s_qkv;
-    {
-    Phase ph("qkv_gemm", st);
-    HIP_TRY(launch_gemm(p.afrag ? A_BF16_FRAG : amode, EPI_STORE_F32, q, st), "qkv gemm");
-    }
-    {
-    Phase ph("qk_norm_rope", st);
-    HIP_TRY(launch_qk_norm_rope(dt, batch, R, p.Rp, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
-                                p.s_qkv, Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
-                                at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
-            "qk_norm_rope");
+    if (p.qkv_fused) {
+      // above 1024 rows (no split-K) the GEMM's epilogue applies q/k-norm and RoPE itself and
+      // writes Q, K, V^T in bf16: the float32 Q|K|V never leaves the chip
+      q.qkv.R = R;
+      q.qkv.Rp = p.Rp;
+      q.qkv.gamma = g;
+      q.qkv.n_q = nq;
+      q.qkv.n_kv = nkv;
+      q.qkv.qk_norm = cfg->qk_norm;
+      q.qkv.eps = cfg->rms_eps;
+      q.qkv.qn = Lw.q_norm;
+      q.qkv.kn = Lw.k_norm;
+      q.qkv.table = at<float2>(ws, p.rope);
+      q.qkv.Q = at<void>(ws, p.Q);
+      q.qkv.Kb = at<void>(ws, p.Kb);
+      q.qkv.Vb = at<void>(ws, p.Vb);
+      Phase ph("qkv_gemm", st);
+      HIP_TRY(launch_gemm(amode, EPI_QKV, q, st), "qkv gemm (fused q/k-norm and RoPE)");
+    } else {
+      {
+      Phase ph("qkv_gemm", st);
+      HIP_TRY(launch_gemm(p.afrag ? A_BF16_FRAG : amode, EPI_STORE_F32, q, st), "qkv gemm");
+      }
+      Phase ph("qk_norm_rope", st);
+      HIP_TRY(launch_qk_norm_rope(dt, batch, R, p.Rp, g, nq, nkv, hd, cfg->qk_norm, cfg->rms_eps, at<float>(ws, p.QKV),
+                                  p.s_qkv, Lw.q_norm, Lw.k_norm, at<float2>(ws, p.rope), at<void>(ws, p.Q),
+                                  at<void>(ws, p.Kb), at<void>(ws, p.Vb), st),
+              "qk_norm_rope");
     }
     AttnArgs aa{};
     aa.B = batch;

@@ -31,15 +31,6 @@ __device__ __forceinline__ float4 sum_planes4(float4 acc, const float* p, int64_
   return acc;
 }
 
-// Row layout of one request (Section 3.2): rows 0..gamma are the spine t_0..t_gamma;
-// row gamma+1 + r*gamma + (i-1) is mask i of branch r.  Position offset from the
-// context length: spine j -> j; branch r mask i -> r + i.
-__device__ __forceinline__ int row_pos_offset(int row, int gamma) {
-  if (row <= gamma) return row;
-  const int k = row - gamma - 1;
-  return k / gamma + k % gamma + 1;
-}
-
 template <typename T>
 __global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, int V, const int* spine,
                                                      const T* embed, const T* mask_emb, float* X,

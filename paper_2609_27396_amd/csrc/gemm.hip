@@ -199,6 +199,83 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     }
   }
 
+  if constexpr (EPI == EPI_QKV) {
+    // One 128-wide head per wave column: the row's sum of squares over the head is this
+    // lane's eight columns plus the 16 lanes sharing the row (DPP), and RoPE's rotate-half
+    // partner of column d (d +- 64) is fragment ni +- 4 of the same lane.  Same arithmetic as
+    // the q/k-norm kernel: y = x * (1 / sqrt(ss / 128 + eps)) * g, then
+    // y_d = y_d cos - y_{d+64} sin, y_{d+64} = y_{d+64} cos + y_d sin.  The bf16 results go
+    // through this wave's part of the (now free) LDS ring, [WM rows][128 + 8 columns], so that
+    // Q and K leave as 16-byte row pieces and V^T as 64 consecutive rows per store (the launch
+    // sizes the dynamic LDS for this staging: up to 139 KB against the 128 KB ring).
+    static_assert(WN == 128 && FN == 8 && WM <= 64 && DUAL == 0, "one 128-wide head per wave column");
+    constexpr int LDT = 136;  // staging row stride in bf16 (272 bytes: rows fall on different banks)
+    const QkvEpi& e = a.qkv;
+    const int slot = nt * (BN / 128) + wn;
+    const int grp = e.n_q / e.n_kv;
+    const bool live = slot < e.n_q + 2 * e.n_kv;
+    const bool isv = slot >= e.n_q + e.n_kv, isq = slot < e.n_q;
+    bf16_t* stg = (bf16_t*)smem + wave * WM * LDT;
+    __syncthreads();  // every wave is done with the ring
+    if (!live) return;  // past the last head (no barrier follows)
+    const float* gain = isq ? e.qn : e.kn;
+    const int row0 = m0 + wm * WM;  // this wave's first row
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lrow = mi * 16 + lc * 4 + r, row = row0 + lrow;
+        float v[FN];
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) v[ni] = acc[mi][ni][r];
+        if (!isv) {
+          if (e.qk_norm) {
+            float ss = 0.f;
+#pragma unroll
+            for (int ni = 0; ni < FN; ++ni) ss += v[ni] * v[ni];
+            ss = row16_sum(ss);
+            const float rn = 1.0f / sqrtf(ss / 128.0f + e.eps);
+#pragma unroll
+            for (int ni = 0; ni < FN; ++ni) v[ni] = v[ni] * rn * gain[ni * 16 + lr];
+          }
+          const int rc = min(row, a.M - 1), b = rc / e.R;
+          const float2* cs = e.table + ((int64_t)b * (2 * e.gamma + 1) + row_pos_offset(rc - b * e.R, e.gamma)) * 64 + lr;
+#pragma unroll
+          for (int ni = 0; ni < FN / 2; ++ni) {
+            const float2 c = cs[ni * 16];
+            const float lo = v[ni], hi = v[ni + 4];
+            v[ni] = lo * c.x + -1.f * hi * c.y;
+            v[ni + 4] = hi * c.x + 1.f * lo * c.y;
+          }
+        }
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) stg[lrow * LDT + ni * 16 + lr] = f2bf(v[ni]);
+      }
+    }
+    if (!isv) {
+      // row pieces: lane (rq, piece) stores 16 bytes = columns 8 piece .. +7 of rows rq, rq+4, ...
+      const int piece = lane & 15;
+#pragma unroll 4
+      for (int lrow = lane >> 4; lrow < WM; lrow += 4) {
+        const int row = row0 + lrow;
+        if (row >= a.M) break;
+        const int b = row / e.R, rr = row - b * e.R;
+        bf16_t* dst = isq ? (bf16_t*)e.Q + (((int64_t)(b * e.n_kv + slot / grp) * grp + slot % grp) * e.R + rr) * 128
+                          : (bf16_t*)e.Kb + ((int64_t)(b * e.n_kv + (slot - e.n_q)) * e.Rp + rr) * 128;
+        *(uint4*)(dst + piece * 8) = *(const uint4*)(stg + lrow * LDT + piece * 8);
+      }
+    } else {
+      // V^T [128][Rp]: lane = row, one store per head dimension (WM consecutive rows of a
+      // request, split where a request ends)
+      const int row = row0 + lane;
+      if (lane < WM && row < a.M) {
+        const int b = row / e.R, rr = row - b * e.R;
+        bf16_t* dst = (bf16_t*)e.Vb + (int64_t)(b * e.n_kv + (slot - e.n_q - e.n_kv)) * 128 * e.Rp + rr;
+        for (int d = 0; d < 128; ++d) dst[(int64_t)d * e.Rp] = stg[lane * LDT + d];
+      }
+    }
+    return;
+  }
   if constexpr (EPI == EPI_TOP2) {
     // One (key1, key2, third value) triple per row and 128-column tile (WPT wave columns each):
     // per lane over its columns of each row (FN of them); then the 16 lanes that share the
@@ -490,7 +567,9 @@ template <int BM, int BN, int WMW, int WNW, int STAGES, int BKB, int EPI, int DU
 hipError_t run_pipe(const GemmArgs& a, hipStream_t st) {
   const int MT = (a.M + BM - 1) / BM;
   const int NT = EPI == EPI_SWIGLU ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
-  constexpr int lds = STAGES * ((DUAL ? 2 : 1) * BM + BN) * BKB;
+  constexpr int ring = STAGES * ((DUAL ? 2 : 1) * BM + BN) * BKB;
+  constexpr int stage_out = EPI == EPI_QKV ? (BM / WMW) * WMW * WNW * 136 * 2 : 0;  // the QKV epilogue's staging
+  constexpr int lds = ring > stage_out ? ring : stage_out;
   static_assert(lds <= 163840, "LDS ring exceeds 160 KB");
   auto kern = gemm_pipe_kernel<BM, BN, WMW, WNW, STAGES, BKB, EPI, DUAL>;
   static const hipError_t attr =
@@ -572,6 +651,15 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 128, EPI_STORE_F32, 1>(a, st);
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
+  }
+  if (epi == EPI_QKV) {
+    if (amode != A_BF16 || a.M <= 1024 || a.splits != 1 || a.N != (a.qkv.n_q + 2 * a.qkv.n_kv) * 128 ||
+        a.qkv.n_kv < 1 || a.qkv.n_q % a.qkv.n_kv || a.qkv.R < 1 || a.qkv.Rp < a.qkv.R)
+      return hipErrorInvalidValue;
+    // the same tile choice as the plain projection (192 rows when they fill the rounds better)
+    if (round_fill(a.M, a.N, 192) > round_fill(a.M, a.N, 256) + 0.1)
+      return run_pipe<192, 256, 4, 2, 2, 128, EPI_QKV, 0>(a, st);
+    return run_pipe<256, 256, 4, 2, 2, 128, EPI_QKV, 0>(a, st);
   }
   if (epi == EPI_TOP2) {
     // Top-2 over every branch row from one bf16 plane.  Measured on MI355X at the Qwen3

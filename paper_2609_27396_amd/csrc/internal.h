@@ -22,7 +22,22 @@ struct Phase {
 // C[M, N] (op)= A[M, K] . B[N, K]^T with B given in up to three row segments
 // (rows [0, n1) from B0, [n1, n2) from B1, [n2, N) from B2), or, with seg_rows > 0 (not for
 // EPI_SWIGLU), in equal segments: row n from seg[n / seg_rows], row n % seg_rows.
-enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3, EPI_TOP2 = 4 };
+enum GemmEpi { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_STORE_BF16 = 3, EPI_TOP2 = 4, EPI_QKV = 5 };
+
+// Parameters of the EPI_QKV epilogue: the Q|K|V projection of R rows per request written as
+// the attention kernel's bf16 operands (Q [B, n_kv, grp * R, 128], in-block K [B, n_kv, Rp, 128],
+// V^T [B, n_kv, 128, Rp]) after the per-head q/k RMSNorm (qk_norm != 0, gains qn / kn) and RoPE
+// (table: (cos, sin) per request, position offset and frequency, as the q/k-norm kernel reads it).
+struct QkvEpi {
+  int R = 0, Rp = 0, gamma = 0, n_q = 0, n_kv = 0, qk_norm = 0;
+  float eps = 0.f;
+  const float* qn = nullptr;
+  const float* kn = nullptr;
+  const float2* table = nullptr;
+  void* Q = nullptr;
+  void* Kb = nullptr;
+  void* Vb = nullptr;
+};
 // A_BF16: A is bf16, row-major with leading dimension lda.  A_F32: float32 FMA kernel
 // (the float32 model path; B is then float32 too).
 // A_BF16_DUAL: A given as two bf16 planes hi (at A) and lo (at A + lo_off elements) with
@@ -60,6 +75,7 @@ struct GemmArgs {
   const int* only_if = nullptr;  // non-NULL: every workgroup returns at once unless *only_if != 0
   int seg_rows = 0;               // > 0: B rows from seg[] (N <= kMaxGemmSegs * seg_rows)
   const void* seg[16] = {};
+  QkvEpi qkv{};  // EPI_QKV only (bf16, head_dim 128, more than 1024 rows, no split-K)
 };
 
 constexpr int kMaxGemmSegs = 16;
