@@ -605,6 +605,27 @@ hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
   if (a.M > 1024) {
     if (EPI != EPI_SWIGLU && round_fill(a.M, a.N, 192) > round_fill(a.M, a.N, 256) + 0.1)
       return run_pipe<192, 256, 2, 4, 2, 128, EPI>(a, st);
+    if constexpr (EPI == EPI_SWIGLU) {
+      // When the 256 x 256 tiles leave a last round of workgroups at most half full, the FFN
+      // columns of that round go to a second launch of 128 x 128 tiles (64 gate + 64 up
+      // columns, two workgroups per CU), four times as many workgroups each a quarter of the
+      // work: the first launch runs whole rounds only.  Measured on MI355X: 4.3% off the
+      // Qwen3-14B batch-8 gate/up (5.3 rounds), 2.6% off Qwen3-8B batch 16 (7.1 rounds).
+      const int MT = (a.M + 255) / 256, NT = (a.N + 127) / 128, T = MT * NT;
+      const int NT1 = (T / 256) * 256 / MT;  // FFN column tiles of the whole rounds
+      if (T % 256 != 0 && T % 256 <= 128 && NT1 > 0 && NT1 < NT) {
+        GemmArgs head = a, tail = a;
+        head.N = NT1 * 128;
+        const int f0 = NT1 * 128;
+        tail.B0 = (const bf16_t*)a.B0 + (int64_t)f0 * a.K;
+        tail.B1 = (const bf16_t*)a.B1 + (int64_t)f0 * a.K;
+        tail.C = (bf16_t*)a.C + f0;
+        tail.N = a.N - f0;
+        const hipError_t e = run_pipe<256, 256, 2, 4, 2, 128, EPI>(head, st);
+        if (e != hipSuccess) return e;
+        return run_pipe<128, 128, 2, 2, 2, 128, EPI>(tail, st);
+      }
+    }
     return run_pipe<256, 256, 2, 4, 2, 128, EPI>(a, st);
   }
   if (a.M > 320 || (a.M <= 64 && EPI != EPI_SWIGLU)) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
