@@ -144,6 +144,16 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
     const int max_s = min(max_blocks / 2, kMaxAttnSplits);
     if (S > max_s) S = max_s;
     if (S < 1) S = 1;
+    if (base > DPARA_ATTN_TARGET_WG && max_s >= 2) {
+      // Large batches: two workgroups fit on a CU (512 at once).  When the workgroups make at
+      // most two rounds and the last one is at most 70% full, a split of two fills the rounds
+      // (measured on MI355X at Qwen3-14B batch 8, context 8192: 1.5 -> 3 rounds, attention
+      // 665 -> 609 us per layer with the fold); with more rounds, or contexts of mixed lengths,
+      // the fold costs more than it saves (Qwen3-8B batch 16: 447 -> 479 us).
+      constexpr int kSlots = 512;
+      const int rounds = (base + kSlots - 1) / kSlots;
+      if (rounds <= 2 && base % kSlots != 0 && base % kSlots <= kSlots * 7 / 10) S = 2;
+    }
     p.S = S;
     p.chunk = 0;
   } else {
