@@ -356,9 +356,9 @@ int dpara_target_forward_hidden(const dpara_config_t* cfg, const dpara_target_we
                                 void* logits, int32_t logits_dtype, const int32_t* feat_layers,
                                 int32_t n_feat, void* hidden, void* ws, size_t ws_bytes, void* stream);
 
-/* Feature fusion, the step before the cache update (Section 3.2, "Trainable and frozen
- * parameters": the projection that fuses the concatenated multi-layer target features, and
- * the input normalization).  For every row x of `hidden` (the target's hidden states at
+/* Feature fusion, the step before the cache update (Section 3.2, trainable and frozen
+ * parameters: a learned linear map of the target's hidden states from several layers, joined
+ * end to end, followed by a normalisation).  For every row x of `hidden` (the target's hidden states at
  * n_feat layers, concatenated): f = RMSNorm(x fc^T) * norm (eps cfg->rms_eps), the fused
  * feature dpara_ctx_append takes.  The projection accumulates in float32; f is rounded to
  * the cfg dtype.

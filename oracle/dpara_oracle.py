@@ -185,9 +185,9 @@ def row_positions(gamma: int, n_b: int) -> np.ndarray:
 # drafter layers
 # ----------------------------------------------------------------------------
 def fuse_features(shape, wf, hidden, mode: str = "bf16"):
-    """Fused target features, the rows the feature cache C takes (Section 3.2, "Trainable
-    and frozen parameters": the projection fusing the concatenated multi-layer target
-    features, and the input normalization).  Reading R16: f = RMSNorm(fc x) * g for x the
+    """Fused target features, the rows the feature cache C takes (Section 3.2, trainable and
+    frozen parameters: a learned linear map of the target's hidden states from several layers,
+    joined end to end, then a normalisation).  Reading R16: f = RMSNorm(fc x) * g for x the
     concatenation of the target's hidden states at n_feat layers, fc [H, n_feat*H] without
     bias; the projection is kept in float32 and the result rounded to the cache dtype.
     hidden: [n, n_feat*H] -> [n, H]."""

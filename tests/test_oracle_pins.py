@@ -161,8 +161,8 @@ def test_tree_mask_counts(gamma):
 
 
 def test_layout_matches_paper_message_size():
-    # Appendix D: hidden states of all d+1 branches across d positions are 573 KB for a
-    # Qwen3-14B drafter (hidden 5120) at d = 7 in 16-bit.
+    # Appendix D: the message carrying every branch's hidden states ((d+1) branches, d rows
+    # each) is 573 KB for a Qwen3-14B drafter (hidden 5120) at d = 7 in 16-bit.
     d, H = 7, 5120
     assert (d + 1) * d * H * 2 == 573_440
 
