@@ -134,9 +134,11 @@ Plan make_plan(const dpara_config_t* c, int B, int ctx_cap, int R = 0) {
   const int grp = nq / nkv;
   if (c->dtype == DPARA_BF16) {
     // Split each request's key blocks (context + in-block) over S workgroups so that the
-    // MFMA pass launches at most about DPARA_ATTN_TARGET_WG workgroups (one resident
-    // workgroup per CU), with at least 2 key blocks each; partial (O, m, l) traffic grows
-    // with S, so no more splits than that.
+    // MFMA pass launches at most about DPARA_ATTN_TARGET_WG workgroups (one per CU), with at
+    // least 2 key blocks each; partial (O, m, l) traffic grows with S, so no more splits than
+    // that.  Two workgroups fit on a CU, but more splits were measured slower at Qwen3-8B
+    // batch 1 (targets 384 / 512 / 768: 44.9 / 43.2 / 50.7 us per layer with the fold, 41.8 at
+    // 256).
     const int tiles = (grp * p.R + attn_rows_per_workgroup() - 1) / attn_rows_per_workgroup();
     const int base = B * nkv * tiles;
     const int max_blocks = (ctx_cap + 63) / 64 + p.Rp / 64;
