@@ -224,8 +224,14 @@ int dpara_verify_greedy_noalloc(const dpara_config_t* cfg, int32_t batch, const 
  * The full head: bf16 drafters with ar_rank in {64, 128, 256}, vocab <= 2^18 and
  * batch <= 16 run the gamma head steps in one launch that needs all of its workgroups
  * resident at once (one per CU); if the GPU is shared so that they cannot all run, the
- * launch gives up after about 0.3 s per step and sets DPARA_STATUS_HEAD_TIMEOUT.  Other
- * configurations launch one kernel per step. */
+ * launch gives up after about 0.3 s per step and sets DPARA_STATUS_HEAD_TIMEOUT.  The
+ * drafts, next_spine and margins of that call are then not valid (a workgroup whose wait
+ * timed out stops there, and the steps from that one on are not all computed): the caller
+ * checks the status word and repeats the call.  The single launch returns at once, without waiting, whenever
+ * every pruned step was proven, so the bit can only be set by a call that needed the full
+ * head.  (The timeout is not turned into a second, per-step pass on the device: that
+ * needs one launch per step on every call, about 17 launches at gamma 16, even when
+ * nothing timed out.)  Other configurations launch one kernel per step. */
 int dpara_select_and_head(const dpara_config_t* cfg, const dpara_weights_t* w, int32_t batch,
                           const float* reps, const int32_t* accept_len, const int32_t* bonus,
                           float* gathered, int32_t* drafts, int32_t* next_spine, float* margins,
