@@ -78,6 +78,7 @@ __device__ __forceinline__ int b_frag_row(int wn, int ni) {
 // right after the barrier, so STAGES-1 stages are in flight while one is consumed.
 template <int CH>
 __device__ __forceinline__ int swz(int r, int c) {
+  if (CH == 16) return c ^ (r & 15);
   if (CH == 8) return c ^ (r & 7);
   return c ^ ((r >> 1) & 3);
 }
@@ -694,7 +695,10 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
   }
   if (amode == A_BF16_DUAL) {
     if (epi == EPI_TOP2) return hipErrorInvalidValue;
-    if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 128, EPI_STORE_F32, 1>(a, st);
+    // 16 rows (the LM head over one request's gamma rows): 128-deep K stages in a 4-deep ring
+    // (160 KB, one workgroup per CU), 4.5% faster on MI355X than 64-deep stages at two
+    // workgroups per CU; the per-32-deep-chunk order of the MFMAs (hi, then lo) is unchanged.
+    if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 256, EPI_STORE_F32, 1>(a, st);
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }
