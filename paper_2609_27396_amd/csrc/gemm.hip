@@ -699,6 +699,9 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     // (160 KB, one workgroup per CU), 4.5% faster on MI355X than 64-deep stages at two
     // workgroups per CU; the per-32-deep-chunk order of the MFMAs (hi, then lo) is unchanged.
     if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 256, EPI_STORE_F32, 1>(a, st);
+    // 32 rows (two requests): the same 128-deep stages in a 3-deep ring, 15% faster than the
+    // 64-row tile with half its rows idle (batch-2 head 325-345 -> 282 us on MI355X).
+    if (a.M <= 32) return run_pipe<32, 128, 1, 4, 3, 256, EPI_STORE_F32, 1>(a, st);
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }

@@ -5,12 +5,13 @@ The bound-pruned steps prove every step at the full-size shapes, so the parity t
 rounds never reach the full head there.  The first cases make the pruned bound fail on purpose
 (a large head matrix W and token embedding E: max_v |W_v| |E[y]| swamps every logit gap), so
 that every call hands over to the full head: the single-launch head (one workgroup per CU, its
-step exchange and bounded wait) at batch 1 and 16, and the per-step kernels at batch 20.  Greedy
+step exchange and bounded wait) at batch 1, 2 and 16, and the per-step kernels at batch 20.  Greedy
 drafts are checked teacher-forced (the oracle's step i is fed the GPU's y_{i-1}) wherever the
 oracle's top1 - top2 margin exceeds 1e-2; sampled draws likewise, with the tempered scores
 within 1e-3 + 1e-3 |s|.  The last cases run the off-serial-path head (candidates of every
 branch row ranked by the rows' bf16 hi part, then rescored) at the default weight scales, where
-the steps are proven, against the plain head bit for bit and against the oracle.  The head
+the steps are proven, against the plain head bit for bit and against the oracle, at batch 1, 2,
+4 and 16 (each batch up to 4 takes its own LM-head tile).  The head
 reads only the gathered rows, the tied embedding and E, W, so the representations here are
 synthetic N(0, 1) rows rather than a backbone's output."""
 import dataclasses
@@ -60,7 +61,7 @@ def _inputs(B, seed):
     return reps, acc, bon
 
 
-@pytest.mark.parametrize("B", [1, 16, 20])
+@pytest.mark.parametrize("B", [1, 2, 16, 20])
 def test_full_head_at_qwen3_vocabulary(B):
     from paper_2609_27396_amd import dpara as D
     w, dd, w64 = _setup("full")
@@ -136,7 +137,7 @@ def test_full_head_at_qwen3_vocabulary(B):
         assert np.array_equal(m2.cpu().numpy(), greedy[2]) and np.array_equal(g2.cpu().numpy(), gh)
 
 
-@pytest.mark.parametrize("B", [1, 16])
+@pytest.mark.parametrize("B", [1, 2, 4, 16])
 def test_candidates_head_at_qwen3_vocabulary(B):
     """The off-serial-path head at the Qwen3 vocabulary with the default weight scales: every
     branch row ranked by its bf16 hi part, the 16 candidates rescored with hi + lo, the bound
