@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
 COPY_PROBE_BYTES = 256 << 20
-GATEUP_KERNEL_SMALL_M = "gemm_adir_kernel<2, 4>"  # the gate/up SwiGLU GEMM at <= 320 rows
+GATEUP_KERNEL_SMALL_M = "gemm_adir_kernel<2, 4, 0>"  # the gate/up SwiGLU GEMM at <= 320 rows
 
 
 def log(*a):
