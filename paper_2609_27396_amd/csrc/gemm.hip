@@ -619,6 +619,11 @@ template <int EPI>
 hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
   if (a.M > 1024) {
     if constexpr (EPI == EPI_STORE_F32) {
+      // Fewer than 192 tiles of 256 x 256 (under three quarters of one round, e.g. the
+      // 2048-row feature fusion, 4096 columns: 128 tiles): 128 x 128 tiles at two workgroups
+      // per CU fill the chip instead.
+      if (a.splits == 1 && (int64_t)((a.M + 255) / 256) * ((a.N + 255) / 256) < 192)
+        return run_pipe<128, 128, 2, 2, 2, 128, EPI>(a, st);
       // One weight matrix, no split-K: when the last round of BM x 256 tiles is at most 60%
       // full, the columns of that round go to a second launch of 128 x 128 tiles (two
       // workgroups per CU) and the first runs whole rounds only.  Measured on MI355X at

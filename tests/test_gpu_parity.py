@@ -847,8 +847,9 @@ FUSE_CASES = {
     "h256_f32": (synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
                                     vocab=1000, gamma=4, ar_rank=64, qk_norm=True, dtype="f32"),
                  [5, 90]),
-    # Qwen3-8B width: a round at b=1 and a prefill that spans two 4096-row passes
-    "qwen3_8b": (synth.QWEN3_8B, [17, 4100]),
+    # Qwen3-8B width: a round at b=1, a 2048-row prefill (one pass of under a round of large
+    # tiles) and a prefill that spans two 4096-row passes
+    "qwen3_8b": (synth.QWEN3_8B, [17, 2048, 4100]),
 }
 
 
@@ -871,7 +872,8 @@ def test_fuse_features_parity(case):
         ws = torch.empty(D.dpara_fuse_workspace_bytes(fus.cfg, n, n_feat), dtype=torch.uint8, device="cuda")
         D.fuse_features(fus, hd, out, ws)
         torch.cuda.synchronize()
-        rows = np.arange(n) if n <= 1000 else np.unique(np.r_[0:40, 4080:4100, n - 5:n])
+        rows = np.arange(n) if n <= 1000 else np.unique(np.r_[0:40, 1000:1010, 4080:4100, n - 5:n])
+        rows = rows[rows < n]
         ref = O.fuse_features(shape, wf, hid[rows], shape.dtype)
         got = out.float().cpu().numpy()[rows]
         err = np.abs(got - ref)
