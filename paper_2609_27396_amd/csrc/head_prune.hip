@@ -279,14 +279,32 @@ __global__ __launch_bounds__(256) void rescore_candidates(int rows, int H, int V
   f32x4_t acc[NB];
 #pragma unroll
   for (int c = 0; c < NB; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int kc = 0; kc < H / 32; ++kc) {
-    const bf16x8_t ah = *(const bf16x8_t*)(hp + kc * 32);
-    const bf16x8_t al = *(const bf16x8_t*)(lp + kc * 32);
+  // The embedding rows are scattered over the table, so each k chunk's loads are a full
+  // memory latency: chunks are loaded PD ahead in a register ring (past the end the last
+  // chunk is loaded again and never used).  The MFMAs still run in k order, hi then lo.
+  constexpr int PD = 4;
+  const int KC = H / 32;
+  bf16x8_t rh[PD], rl[PD], re[PD][NB];
+  auto load = [&](int kc, bf16x8_t& h, bf16x8_t& l, bf16x8_t(&e)[NB]) {
+    kc = min(kc, KC - 1);
+    h = *(const bf16x8_t*)(hp + kc * 32);
+    l = *(const bf16x8_t*)(lp + kc * 32);
 #pragma unroll
-    for (int c = 0; c < NB; ++c) {
-      const bf16x8_t b = *(const bf16x8_t*)(ep[c] + kc * 32);
-      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc[c], 0, 0, 0);
-      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc[c], 0, 0, 0);
+    for (int c = 0; c < NB; ++c) e[c] = *(const bf16x8_t*)(ep[c] + kc * 32);
+  };
+#pragma unroll
+  for (int d = 0; d < PD; ++d) load(d, rh[d], rl[d], re[d]);
+  for (int kc0 = 0; kc0 < KC; kc0 += PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      if (kc0 + d < KC) {
+#pragma unroll
+        for (int c = 0; c < NB; ++c) {
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rh[d], re[d][c], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rl[d], re[d][c], acc[c], 0, 0, 0);
+        }
+      }
+      load(kc0 + d + PD, rh[d], rl[d], re[d]);
     }
   }
   // every A row is this row, so each lane holds its column's value in every element: lane q
