@@ -226,6 +226,16 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
       __syncthreads();
     }
     if (!wave_live) continue;
+    if (inblk) {
+      // Under the tree mask a row sees at most two short runs of in-block keys (the spine
+      // prefix and its own branch): a block that none of the wave's rows sees adds nothing
+      // (every p is 0, no maximum moves), so the wave skips its products.
+      bool need = false;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        need |= (kb0 < e1[u]) | ((span[u] > 0) & (kb0 < lo2[u] + span[u]) & (kb0 + kKeyBlock > lo2[u]));
+      if (!__any(need)) continue;
+    }
 
     // S^T blocks: s[u][kb][r] = score(key kb0 + key_perm(kb, 4*g4 + r), query qi[u])
     f32x4_t s[U][4];
