@@ -23,12 +23,26 @@ __device__ __forceinline__ float silu_f(float g) {
 }
 
 // Logical tile for physical workgroup p: tiles are split into 8 contiguous ranges, one per
-// XCD (workgroups are dispatched round-robin over the 8 XCDs), M fastest inside a range.
+// XCD (workgroups are dispatched round-robin over the 8 XCDs), M fastest inside a range (or
+// inside a group of 8 M tiles, below).
 __device__ __forceinline__ void tile_of(int p, int MT, int NT, int& mt, int& nt) {
   const int total = MT * NT;
   const int per = total >> 3;
   int L = p;
   if (p < (per << 3)) L = (p & 7) * per + (p >> 3);
+  // At 16 or more M tiles, groups of 8 M tiles, M fastest inside a group: the 32 workgroups
+  // an XCD runs at once then cover about 8 M x 4 N tiles (each A tile read by 4, each weight
+  // tile by 8) instead of all M tiles of 1-2 columns, so more of the activation stays in L2
+  // (Qwen3-8B batch 16, 19-25 M tiles: 11.98 -> 11.60 ms per step; at 10 M tiles, 14B batch
+  // 8, the grouping was 0.8% slower, so fewer stay in plain M-fastest order).
+  constexpr int GM = 8;
+  if (MT >= 2 * GM) {
+    const int grp = L / (GM * NT), first = grp * GM;
+    const int gm = min(MT - first, GM), r = L - grp * GM * NT;
+    mt = first + r % gm;
+    nt = r / gm;
+    return;
+  }
   mt = L % MT;
   nt = L / MT;
 }
