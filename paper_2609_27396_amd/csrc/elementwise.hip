@@ -65,6 +65,13 @@ __global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, in
   }
 }
 
+// Four consecutive outputs in one store (8 bytes of bf16, 16 of float32; the address is a
+// multiple of 4 elements).
+__device__ __forceinline__ void st4(bf16_t* p, float a, float b, float c, float d) {
+  *(uint2*)p = make_uint2((uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16), (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16));
+}
+__device__ __forceinline__ void st4(float* p, float a, float b, float c, float d) { *(float4*)p = make_float4(a, b, c, d); }
+
 // One block (8 waves) per output row, VN float4 per thread.  x = X row + the S pending
 // split-K partial planes of that row (added in plane order); optionally x is written back
 // into X; y = x / rms(x) * g.
@@ -92,25 +99,16 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, in
   }
   ss = block_sum<kNormThreads / 64>(ss, red);
   const float r = 1.0f / sqrtf(ss / (float)H + eps);
-  // fragment order: 4 consecutive k of one row stay consecutive (k % 8 is 0 or 4)
+  // fragment blocks: 4 consecutive k of one row stay consecutive (k % 4 == 0), and the 8
+  // threads of one 32-k block row write its 64 bytes together
   TO* y = FRAG ? Y : Y + (int64_t)m * H;
 #pragma unroll
   for (int t = 0; t < VN; ++t) {
     const int i = (threadIdx.x + kNormThreads * t) * 4;
     if (i < H) {
       const float4 gg = *(const float4*)(g + i);
-      if (FRAG) {
-        TO* yf = Y + frag_index(m, i, H);
-        st_f(yf + 0, v[t].x * r * gg.x);
-        st_f(yf + 1, v[t].y * r * gg.y);
-        st_f(yf + 2, v[t].z * r * gg.z);
-        st_f(yf + 3, v[t].w * r * gg.w);
-        continue;
-      }
-      st_f(y + i + 0, v[t].x * r * gg.x);
-      st_f(y + i + 1, v[t].y * r * gg.y);
-      st_f(y + i + 2, v[t].z * r * gg.z);
-      st_f(y + i + 3, v[t].w * r * gg.w);
+      st4(FRAG ? Y + frag_index(m, i, H) : y + i, v[t].x * r * gg.x, v[t].y * r * gg.y, v[t].z * r * gg.z,
+          v[t].w * r * gg.w);
     }
   }
 }

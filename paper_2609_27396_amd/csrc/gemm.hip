@@ -402,7 +402,7 @@ __global__ __launch_bounds__(256) void gemm_adir_kernel(GemmArgs a, int NT) {
 #pragma unroll
   for (int mi = 0; mi < FM; ++mi) {
     const int rb = min(wave * FM + mi, last_rb);
-    ap[mi] = (const bf16_t*)a.A + ((int64_t)rb * KC + kbeg / 32) * 512 + lane * 8;
+    ap[mi] = (const bf16_t*)a.A + ((int64_t)rb * KC + kbeg / 32) * 512 + (lane & 15) * 32 + (lane >> 4) * 8;
   }
   const bf16_t* bsrc[B_INS];
   const int lrow = lane / CH, lslot = lane % CH;

@@ -46,12 +46,13 @@ struct QkvEpi {
 // K a multiple of 256 * splits; EPI_SWIGLU or EPI_STORE_F32 only.
 enum GemmAMode { A_BF16 = 0, A_BF16_FRAG = 1, A_F32 = 2, A_BF16_DUAL = 3 };
 
-// Element (row, k) of a bf16 operand stored in MFMA fragment order: blocks of 16 rows x 32 k
-// (ceil(rows/16) x K/32 of them, row blocks outermost), each 64 lanes x 8 values, where lane
-// l holds row 16*rb + l%16 and k = 32*kc + 8*(l/16) .. +7.  One wave loads one block (1 KB)
-// with one 16-byte load per lane, already in the operand layout of v_mfma_f32_16x16x32_bf16.
+// Element (row, k) of a bf16 operand stored in MFMA fragment blocks: blocks of 16 rows x 32 k
+// (ceil(rows/16) x K/32 of them, row blocks outermost), row-major inside a block (64 bytes a
+// row).  One wave loads one block (1 KB) with one 16-byte load per lane, lane l taking row
+// l%16, k 8*(l/16) .. +7: the operand layout of v_mfma_f32_16x16x32_bf16.  A row's 32 values
+// of a block are contiguous, so the writer (one row per workgroup) stores whole 64-byte pieces.
 __host__ __device__ inline int64_t frag_index(int row, int k, int K) {
-  return ((int64_t)(row >> 4) * (K >> 5) + (k >> 5)) * 512 + ((((k & 31) >> 3) << 4) + (row & 15)) * 8 + (k & 7);
+  return ((int64_t)(row >> 4) * (K >> 5) + (k >> 5)) * 512 + (row & 15) * 32 + (k & 31);
 }
 
 struct GemmArgs {
