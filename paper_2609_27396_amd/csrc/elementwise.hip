@@ -204,10 +204,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope(int R, int Rp, int gamma, in
     const int kvh = slot - n_q;
     dst = Kb + ((int64_t)(b * n_kv + kvh) * Rp + row) * HD + j0;
   }
-  st_f(dst, y0);
-  st_f(dst + 1, y1);
-  st_f(dst + 2, y2);
-  st_f(dst + 3, y3);
+  st4(dst, y0, y1, y2, y3);
 }
 
 template <typename T>

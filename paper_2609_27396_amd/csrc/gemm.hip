@@ -81,6 +81,27 @@ __device__ __forceinline__ int b_frag_row(int wn, int ni) {
   return wn * WN + ni * 16;
 }
 
+// SwiGLU outputs of a tile, staged in LDS (rows [0, BM) x OC columns, row stride LDO), leave
+// as 16-byte row pieces instead of one 2-byte store per accumulator element.
+template <int BM, int OC, int LDO>
+__device__ __forceinline__ void swiglu_copy_out(const bf16_t* so, bf16_t* C, int64_t ldc, int m0, int f0, int M,
+                                                int N) {
+  static_assert(OC % 8 == 0 && LDO % 8 == 0, "16-byte pieces");
+  constexpr int CPR = OC / 8;
+  for (int e = threadIdx.x; e < BM * CPR; e += blockDim.x) {
+    const int lrow = e / CPR, ch = e % CPR;
+    const int row = m0 + lrow, f = f0 + ch * 8;
+    if (row >= M || f >= N) continue;
+    const bf16_t* src = so + lrow * LDO + ch * 8;
+    bf16_t* dst = C + (int64_t)row * ldc + f;
+    if (f + 8 <= N && (ldc & 7) == 0) {
+      *(uint4*)dst = *(const uint4*)src;
+    } else {
+      for (int j = 0; j < 8 && f + j < N; ++j) dst[j] = src[j];
+    }
+  }
+}
+
 // ------------------------------------------------------------------ pipelined bf16 path
 // Tiles stream through a ring of STAGES LDS buffers filled by direct global->LDS DMA
 // (global_load_lds_dwordx4: lane i's 16 bytes land at M0 + 16*i, so one instruction moves
@@ -333,20 +354,31 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
     }
     return;
   }
+  if constexpr (EPI == EPI_SWIGLU) {
+    constexpr int OC = BN / 2, LDO = OC + 8;
+    static_assert(BM * LDO * 2 <= STAGES * STAGE_BYTES, "the output tile fits the ring");
+    bf16_t* so = (bf16_t*)smem;
+    __syncthreads();  // every wave is done with the ring
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lrow = wm * WM + mi * 16 + (lane >> 4) * 4 + r;
+#pragma unroll
+        for (int ni = 0; ni < FN / 2; ++ni)
+          so[lrow * LDO + wn * (WN / 2) + ni * 16 + lr] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+      }
+    __syncthreads();
+    swiglu_copy_out<BM, OC, LDO>(so, (bf16_t*)a.C, a.ldc, m0, nt * OC, a.M, a.N);
+    return;
+  }
 #pragma unroll
   for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = m0 + wm * WM + mi * 16 + (lane >> 4) * 4 + r;
       if (row >= a.M) continue;
-      if constexpr (EPI == EPI_SWIGLU) {
-        bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
-#pragma unroll
-        for (int ni = 0; ni < FN / 2; ++ni) {
-          const int f = nt * (BN / 2) + wn * (WN / 2) + ni * 16 + lr;
-          if (f < a.N) C[f] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
-        }
-      } else if constexpr (EPI == EPI_STORE_BF16) {
+      if constexpr (EPI == EPI_STORE_BF16) {
         bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni) {
@@ -475,20 +507,31 @@ __global__ __launch_bounds__(256) void gemm_adir_kernel(GemmArgs a, int NT) {
   }
   wait_vmcnt<0>();
 
+  if constexpr (EPI == EPI_SWIGLU) {
+    constexpr int OC = BN / 2, LDO = OC + 8;
+    static_assert(BM * LDO * 2 <= SB * STAGE_BYTES, "the output tile fits the ring");
+    bf16_t* so = (bf16_t*)smem;
+    __syncthreads();  // every wave is done with the ring
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lrow = wave * WM + mi * 16 + lc * 4 + r;
+#pragma unroll
+        for (int ni = 0; ni < FN / 2; ++ni)
+          so[lrow * LDO + ni * 16 + lr] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+      }
+    __syncthreads();
+    swiglu_copy_out<BM, OC, LDO>(so, (bf16_t*)a.C, a.ldc, 0, nt * OC, a.M, a.N);
+    return;
+  }
 #pragma unroll
   for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = wave * WM + mi * 16 + lc * 4 + r;
       if (row >= a.M) continue;
-      if constexpr (EPI == EPI_SWIGLU) {
-        bf16_t* C = (bf16_t*)a.C + (int64_t)row * a.ldc;
-#pragma unroll
-        for (int ni = 0; ni < FN / 2; ++ni) {
-          const int f = nt * (BN / 2) + ni * 16 + lr;
-          if (f < a.N) C[f] = f2bf(silu_f(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
-        }
-      } else {
+      {
         float* C = (float*)a.C + ((int64_t)split * a.M + row) * a.ldc;
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni) {
