@@ -786,7 +786,7 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     if (a.M <= 64) return run_pipe<64, 128, 2, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
     // 129-256 rows (batch 9-16): one 256-row tile (both planes, 2-deep ring of 160 KB), so each
     // weight tile is read once: the batch-16 head 860 -> 797 us.
-    if (a.M <= 256) return run_pipe<256, 128, 4, 2, 2, 128, EPI_STORE_F32, 1>(a, st);
+    if (a.M > 128 && a.M <= 256) return run_pipe<256, 128, 4, 2, 2, 128, EPI_STORE_F32, 1>(a, st);
     return run_pipe<128, 128, 4, 2, 3, 128, EPI_STORE_F32, 1>(a, st);
   }
   if (epi == EPI_QKV) {
