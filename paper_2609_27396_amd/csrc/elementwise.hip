@@ -77,11 +77,11 @@ __device__ __forceinline__ void st4(float* p, float a, float b, float c, float d
 // into X; y = x / rms(x) * g.
 constexpr int kNormThreads = 512;
 // FRAG: Y is bf16 in MFMA fragment order (frag_index) instead of row-major.
-template <typename TO, int VN, int FRAG = 0>
-__global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, int grp, int64_t in_stride,
+template <typename TO, int VN, int FRAG = 0, int NTH = kNormThreads>
+__global__ __launch_bounds__(NTH) void rmsnorm_rows(int H, float* X, int grp, int64_t in_stride,
                                                              int in_off, const float* P, int S, int64_t pstride,
                                                              int write_back, const float* g, float eps, TO* Y) {
-  __shared__ float red[kNormThreads / 64];
+  __shared__ float red[NTH / 64];
   const int m = blockIdx.x;
   const int64_t roff = (int64_t)(m / grp) * in_stride + (int64_t)(in_off + m % grp) * H;
   float* x = X + roff;
@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, in
   float ss = 0.f;
 #pragma unroll
   for (int t = 0; t < VN; ++t) {
-    const int i = (threadIdx.x + kNormThreads * t) * 4;
+    const int i = (threadIdx.x + NTH * t) * 4;
     if (i < H) {
       const float4 a = sum_planes4(*(const float4*)(x + i), P + roff + i, pstride, S);
       if (write_back && S > 0) *(float4*)(x + i) = a;
@@ -97,14 +97,14 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_rows(int H, float* X, in
       ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
     }
   }
-  ss = block_sum<kNormThreads / 64>(ss, red);
+  ss = block_sum<NTH / 64>(ss, red);
   const float r = 1.0f / sqrtf(ss / (float)H + eps);
   // fragment blocks: 4 consecutive k of one row stay consecutive (k % 4 == 0), and the 8
   // threads of one 32-k block row write its 64 bytes together
   TO* y = FRAG ? Y : Y + (int64_t)m * H;
 #pragma unroll
   for (int t = 0; t < VN; ++t) {
-    const int i = (threadIdx.x + kNormThreads * t) * 4;
+    const int i = (threadIdx.x + NTH * t) * 4;
     if (i < H) {
       const float4 gg = *(const float4*)(g + i);
       st4(FRAG ? Y + frag_index(m, i, H) : y + i, v[t].x * r * gg.x, v[t].y * r * gg.y, v[t].z * r * gg.z,
@@ -347,6 +347,13 @@ hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V
 template <typename TO, int VN>
 void rmsnorm_launch(int rows, int H, float* X, int grp, int64_t in_stride, int in_off, const float* P, int S,
                     int64_t pstride, int write_back, const float* g, float eps, void* Y, hipStream_t st) {
+  // Up to 64 rows (a target verifying 17 rows a request) each row's workgroup is one of only a
+  // few on the chip: 1024 threads per row put twice the loads in flight on its CU.
+  if (rows <= 64 && (H / 4 + 1023) / 1024 <= (VN + 1) / 2) {
+    hipLaunchKernelGGL((rmsnorm_rows<TO, (VN + 1) / 2, 0, 1024>), dim3(rows), dim3(1024), 0, st, H, X, grp, in_stride,
+                       in_off, P, S, pstride, write_back, g, eps, (TO*)Y);
+    return;
+  }
   hipLaunchKernelGGL((rmsnorm_rows<TO, VN>), dim3(rows), dim3(kNormThreads), 0, st, H, X, grp, in_stride, in_off, P,
                      S, pstride, write_back, g, eps, (TO*)Y);
 }
