@@ -113,7 +113,7 @@ __device__ __forceinline__ void swiglu_copy_out(const bf16_t* so, bf16_t* C, int
 // right after the barrier, so STAGES-1 stages are in flight while one is consumed.
 template <int CH>
 __device__ __forceinline__ int swz(int r, int c) {
-  if (CH == 16) return c ^ (r & 15);
+  if (CH == 16 || CH == 32) return c ^ (r & 15);  // 16 rows of a fragment read: 16 distinct slots
   if (CH == 8) return c ^ (r & 7);
   return c ^ ((r >> 1) & 3);
 }
@@ -779,10 +779,12 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
   }
   if (amode == A_BF16_DUAL) {
     if (epi == EPI_TOP2) return hipErrorInvalidValue;
-    // 16 rows (the LM head over one request's gamma rows): 128-deep K stages in a 4-deep ring
-    // (160 KB, one workgroup per CU), 4.5% faster on MI355X than 64-deep stages at two
-    // workgroups per CU; the per-32-deep-chunk order of the MFMAs (hi, then lo) is unchanged.
-    if (a.M <= 16) return run_pipe<16, 128, 1, 4, 4, 256, EPI_STORE_F32, 1>(a, st);
+    // 16 rows (the LM head over one request's gamma rows): 256-deep K stages (512-byte runs of
+    // each embedding row) in a 2-deep ring of 160 KB, one workgroup per CU.  Measured on MI355X
+    // for the whole batch-1 head: 64-deep stages at two workgroups per CU 280 us, 128-deep in a
+    // 4-deep ring 266-270, 256-deep 256-258.  The per-32-deep-chunk order of the MFMAs (hi,
+    // then lo) is unchanged.
+    if (a.M <= 16) return run_pipe<16, 128, 1, 4, 2, 512, EPI_STORE_F32, 1>(a, st);
     // 32 rows (two requests): the same 128-deep stages in a 3-deep ring, 15% faster than the
     // 64-row tile with half its rows idle (batch-2 head 325-345 -> 282 us on MI355X).
     if (a.M <= 32) return run_pipe<32, 128, 1, 4, 3, 256, EPI_STORE_F32, 1>(a, st);
