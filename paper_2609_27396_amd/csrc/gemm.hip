@@ -735,10 +735,12 @@ hipError_t run_bf16(const GemmArgs& a, hipStream_t st) {
   if (a.M <= 32 && EPI != EPI_SWIGLU) return run_pipe<32, 128, 2, 2, 3, 128, EPI>(a, st);
   if (a.M > 320 || (a.M <= 64 && EPI != EPI_SWIGLU)) return run_pipe<64, 128, 2, 2, 3, 128, EPI>(a, st);
   // SwiGLU up to 64 rows (a target verifying 17 rows a request): weight streaming with a
-  // 6-deep ring of 96-row weight tiles and 64 activation rows, four waves of 16 rows, the
-  // empty row blocks skipped.  36-layer target at batch 1: gate|up 54 -> 46 us per layer.
+  // 3-deep ring of 96-row weight tiles 128 deep in K (256-byte runs of each weight row) and 64
+  // activation rows, four waves of 16 rows, the empty row blocks skipped.  36-layer target at
+  // batch 1: gate|up 54 -> 46 us per layer with 64-deep stages in a 6-deep ring, then 1.2% off
+  // the whole target with the 128-deep stages.
   if constexpr (EPI == EPI_SWIGLU)
-    if (a.M <= 64) return run_pipe<64, 96, 4, 1, 6, 128, EPI>(a, st);
+    if (a.M <= 64) return run_pipe<64, 96, 4, 1, 3, 256, EPI>(a, st);
   // SwiGLU: 48 gate + 48 up rows per tile, so that the Qwen3-8B FFN (12288) gives 256 tiles
   if constexpr (EPI == EPI_SWIGLU) return run_pipe<320, 96, 4, 1, 2, 128, EPI>(a, st);
   return run_pipe<320, 128, 4, 2, 2, 128, EPI>(a, st);
