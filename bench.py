@@ -318,9 +318,12 @@ def recorded_traffic(kernel: str):
 
 def prepare_head(dr):
     """Weight preparation at load time (outside every timed region): the AR head's max row
-    norm, a constant of the weights that the bound-pruned head steps use."""
+    norm and the embedding's max row norm, constants of the weights that the bound-pruned head
+    steps and the hi-plane candidate ranking use."""
     if dr.shape.ar_rank in (64, 128, 256):
         dr.d.prepare_head(dr.ws)
+        if dr.shape.dtype == "bf16":
+            dr.d.prepare_candidates(dr.ws)
 
 
 def fuse_timing(shape, rows=(17, 2048), n_feat=3, iters=20):
@@ -389,8 +392,6 @@ def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
         out["plain_us"][k] = timed(lambda: D.select_and_head(dr.d, reps, acc, bon, None, drafts, nspine, None, ws))
         out["plain_fallback"][k] = ws.head_fallback()
         cand = D.branch_candidates_buffer(dr.d, B)
-        if B == batches[0]:  # max |embed_v|^2 once, as a deployment prepares it with the weights
-            dr.d.prepare_candidates(ws)
         out["candidates_us"][k] = timed(lambda: D.branch_candidates(dr.d, reps, cand, ws))
         out["cand_serial_us"][k] = timed(
             lambda: D.select_and_head_cand(dr.d, reps, cand, acc, bon, None, drafts, nspine, None, ws))
@@ -404,7 +405,6 @@ def head_sweep(dr, shape, batches=(1, 2, 4, 8, 16), iters=20):
         out["sampled_verify_us"][k] = timed(lambda: D.verify_sampled(dr.d, tl, scores, nspine, 1.0, 78, acc, bon, ws))
         assert ws.status() == 0, f"device status {ws.status()}"
         del ws, reps, cand, scores, tl
-    dr.d.unprepare_candidates()
     return out
 
 

@@ -812,6 +812,9 @@ hipError_t launch_gemm(int amode, int epi, const GemmArgs& a, hipStream_t st) {
     // beyond, the large-M tile (256 x 256, 8 waves of 128 x 64, two top-2 tiles per
     // workgroup), 12% faster at 4352 rows.
     if (amode != A_BF16 || a.ldc < (a.N + 127) / 128) return hipErrorInvalidValue;
+    // exactly 193-256 rows (the greedy head's ranking at batch 13-16): one 256 x 256 tile row
+    // (the batch-16 head 587 -> 526 us against two 192-row tiles)
+    if (a.M > 192 && a.M <= 256) return run_pipe<256, 256, 2, 4, 2, 128, EPI_TOP2, 0>(a, st);
     if (a.M <= 1536) return run_pipe<192, 128, 2, 2, 2, 128, EPI_TOP2, 0>(a, st);
     return run_pipe<256, 256, 2, 4, 2, 128, EPI_TOP2, 0>(a, st);
   }

@@ -703,14 +703,18 @@ int head_prune_wparts() { return 512; }
 size_t head_cand_bytes(int B, int gamma) { return 4096 + (size_t)B * (gamma + 1) * gamma * kKeys * 8; }
 size_t head_cand_part_bytes(int B, int gamma, int V) { return (size_t)B * (gamma + 1) * gamma * ((V + 127) / 128) * 24; }
 
-hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
-                                    const void* W, const float* emax2_pre, void* cand, bf16_t* split, uint64_t* part,
-                                    void* scratch, hipStream_t st) {
-  if (!head_prune_supported(1, gamma, V, rank) || B < 1 || H % 64) return hipErrorNotSupported;
+size_t head_row_cand_bytes(int rows) { return 4096 + (size_t)rows * kKeys * 8; }
+
+// Candidates (kTopK exact logits and a bound key) of `rows` float32 rows against the bf16
+// embedding: split into hi/lo planes, hi-plane top-2 GEMM, merge into kHiList keys a row,
+// exact rescoring.  With wnorm_pre the |W_v|^2 pass is skipped (the caller passes the
+// prepared maximum to the steps) and only the overflow flag is cleared.
+hipError_t launch_row_candidates(int rows, int H, int V, int rank, const float* reps, const void* embed,
+                                 const void* W, const float* emax2_pre, const float* wnorm_pre, void* cand,
+                                 bf16_t* split, uint64_t* part, void* scratch, hipStream_t st) {
   int* overflow = (int*)cand;
   float* wpart = (float*)((unsigned char*)cand + 256);
   uint64_t* keys = (uint64_t*)((unsigned char*)cand + 4096);
-  const int rows = B * (gamma + 1) * gamma;
   const int NT = (V + 127) / 128;
   bf16_t* hi = split;
   bf16_t* lo = split + (int64_t)rows * H;
@@ -723,7 +727,9 @@ hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, co
   hipLaunchKernelGGL(split_rows_norms, dim3(rows), dim3(256), 0, st, reps, H, hi, lo, nrm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if ((e = launch_wnorm(1, rank, W, V, wpart, overflow, st)) != hipSuccess) return e;  // also clears `overflow`
+  if ((e = wnorm_pre ? launch_clear_status(overflow, st) : launch_wnorm(1, rank, W, V, wpart, overflow, st)) !=
+      hipSuccess)
+    return e;  // (the |W_v|^2 pass also clears `overflow`)
   const float* emax2 = emax2_pre;
   if (!emax2) {  // one pass over the embedding
     hipLaunchKernelGGL(row_norm2_max, dim3(kEmbedNormParts), dim3(256), 0, st, (const bf16_t*)embed, V, H, eparts);
@@ -750,6 +756,31 @@ hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, co
   hipLaunchKernelGGL(rescore_candidates, dim3(rows), dim3(64), 0, st, rows, H, V, hi, lo,
                      (const bf16_t*)embed, nrm, emax2, cacc, hlist, keys);
   return hipGetLastError();
+}
+
+hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
+                                    const void* W, const float* emax2_pre, void* cand, bf16_t* split, uint64_t* part,
+                                    void* scratch, hipStream_t st) {
+  if (!head_prune_supported(1, gamma, V, rank) || B < 1 || H % 64) return hipErrorNotSupported;
+  return launch_row_candidates(B * (gamma + 1) * gamma, H, V, rank, reps, embed, W, emax2_pre, nullptr, cand, split,
+                               part, scratch, st);
+}
+
+hipError_t launch_head_ranked(int B, int gamma, int H, int V, int rank, const float* G, const void* embed,
+                              const void* E, const void* W, const float* emax2_pre, const float* wnorm_pre,
+                              const int* bonus, int* drafts, int* next_spine, float* margins, int* flag, int* status,
+                              void* cand, bf16_t* split, uint64_t* part, void* scratch, hipStream_t st) {
+  if (!head_prune_supported(1, gamma, V, rank) || B < 1 || H % 64) return hipErrorNotSupported;
+  hipError_t e = launch_row_candidates(B * gamma, H, V, rank, G, embed, W, emax2_pre, wnorm_pre, cand, split, part,
+                                       scratch, st);
+  if (e != hipSuccess) return e;
+  const int* overflow = (const int*)cand;
+  const float* wpart = wnorm_pre ? wnorm_pre : (const float*)((const unsigned char*)cand + 256);
+  const uint64_t* keys = (const uint64_t*)((const unsigned char*)cand + 4096);
+  Phase ph("ar_step", st);
+  if ((e = launch_clear_status(flag, st)) != hipSuccess) return e;
+  return dispatch_pruned(1, rank, B, gamma, V, 1, keys, wpart, wnorm_pre ? 1 : head_prune_wparts(), E, W, bonus,
+                         drafts, next_spine, margins, flag, status, nullptr, overflow, 1.0f, st);
 }
 
 size_t head_cand_scratch_bytes(int B, int gamma) {

@@ -252,6 +252,17 @@ size_t head_cand_scratch_bytes(int B, int gamma);
 hipError_t launch_branch_candidates(int B, int gamma, int H, int V, int rank, const float* reps, const void* embed,
                                     const void* W, const float* emax2_pre, void* cand, bf16_t* split, uint64_t* part,
                                     void* scratch, hipStream_t st);
+// The greedy head's steps for B requests from candidates of their gathered rows G [B, gamma,
+// H] fp32 (the same ranking and exact rescoring as above over B * gamma rows, `cand` of
+// head_row_cand_bytes(B * gamma) bytes, split / part / scratch sized for at least those rows):
+// drafts, next_spine and margins as the pruned head writes them, `flag` nonzero if some step
+// is not proven (the caller then runs the full head).  wnorm_pre: the prepared max |W_v|^2, or
+// NULL (one pass over W).
+size_t head_row_cand_bytes(int rows);
+hipError_t launch_head_ranked(int B, int gamma, int H, int V, int rank, const float* G, const void* embed,
+                              const void* E, const void* W, const float* emax2_pre, const float* wnorm_pre,
+                              const int* bonus, int* drafts, int* next_spine, float* margins, int* flag, int* status,
+                              void* cand, bf16_t* split, uint64_t* part, void* scratch, hipStream_t st);
 // max_v |embed_v|^2 of a [V, H] bf16 matrix into out (one float); parts: 512 floats of scratch.
 hipError_t launch_embed_prepare(const void* embed, int V, int H, float* parts, float* out, hipStream_t st);
 hipError_t launch_head_from_candidates(int B, int gamma, int V, int rank, const void* cand, const void* E,

@@ -11,7 +11,9 @@ oracle's top1 - top2 margin exceeds 1e-2; sampled draws likewise, with the tempe
 within 1e-3 + 1e-3 |s|.  The last cases run the off-serial-path head (candidates of every
 branch row ranked by the rows' bf16 hi part, then rescored) at the default weight scales, where
 the steps are proven, against the plain head bit for bit and against the oracle, at batch 1, 2,
-4 and 16 (each batch up to 4 takes its own LM-head tile).  The head
+4, 9 and 16 (each batch up to 4 takes its own LM-head tile); with the embedding's max row norm
+prepared, the plain head over more than 128 gathered rows takes the same ranking over the
+accepted rows, and gives the same bits (also through its fallback to the full head).  The head
 reads only the gathered rows, the tied embedding and E, W, so the representations here are
 synthetic N(0, 1) rows rather than a backbone's output."""
 import dataclasses
@@ -135,9 +137,22 @@ def test_full_head_at_qwen3_vocabulary(B):
         assert ws.status() == 0 and ws.head_fallback() != 0
         assert np.array_equal(d2.cpu().numpy(), greedy[0]) and np.array_equal(n2.cpu().numpy(), greedy[1])
         assert np.array_equal(m2.cpu().numpy(), greedy[2]) and np.array_equal(g2.cpu().numpy(), gh)
+    if B * g > 128:
+        # with the embedding's max row norm prepared, the plain greedy head over more than 128
+        # gathered rows ranks by the hi parts first; here no step is proven, so it hands over to
+        # the same LM head and full head: the same bits
+        dd.prepare_candidates(ws)
+        d3, n3 = torch.empty_like(drafts), torch.empty_like(nsp)
+        m3, g3 = torch.empty_like(margins), torch.empty_like(gathered)
+        D.select_and_head(dd, reps, acc, bon, g3, d3, n3, m3, ws)
+        torch.cuda.synchronize()
+        dd.unprepare_candidates()
+        assert ws.status() == 0 and ws.head_fallback() != 0
+        assert np.array_equal(d3.cpu().numpy(), greedy[0]) and np.array_equal(n3.cpu().numpy(), greedy[1])
+        assert np.array_equal(m3.cpu().numpy(), greedy[2]) and np.array_equal(g3.cpu().numpy(), gh)
 
 
-@pytest.mark.parametrize("B", [1, 2, 4, 16])
+@pytest.mark.parametrize("B", [1, 2, 4, 9, 16])
 def test_candidates_head_at_qwen3_vocabulary(B):
     """The off-serial-path head at the Qwen3 vocabulary with the default weight scales: every
     branch row ranked by its bf16 hi part, the 16 candidates rescored with hi + lo, the bound
@@ -180,7 +195,17 @@ def test_candidates_head_at_qwen3_vocabulary(B):
         torch.cuda.synchronize()
         assert ws.status() == 0
         runs.append((ws.head_fallback(), d1.cpu(), n1.cpu(), m1.cpu(), g1.cpu()))
+    # the plain head again, now with the norm prepared: above 128 gathered rows it ranks by the
+    # hi parts and rescores (the same machinery over the accepted rows only)
+    d4, n4, m4, g4 = outs()
+    D.select_and_head(dd, reps, acc, bon, g4, d4, n4, m4, ws)
+    torch.cuda.synchronize()
+    fb_ranked = ws.head_fallback()
     dd.unprepare_candidates()
+    assert torch.equal(g4.cpu(), g0.cpu())
+    if fb_ranked == 0 and fb_plain == 0:
+        for a, b in zip((d4.cpu(), n4.cpu(), m4.cpu()), (d0.cpu(), n0.cpu(), m0.cpu())):
+            assert torch.equal(a, b)
     fb = runs[0][0]
     _say(f"batch {B}: fallback flags plain {fb_plain}, candidates {fb}")
     for a, b in zip(runs[0], runs[1]):
