@@ -221,6 +221,11 @@ int dpara_verify_greedy_noalloc(const dpara_config_t* cfg, int32_t batch, const 
  * step's top two when both candidates exceed it.  If any step of any request is not
  * proven, the int32 at byte offset 4 of `ws` is left nonzero (diagnostic; 0 otherwise) and
  * the full head below recomputes every request; the results are the same either way.
+ * A bf16 drafter with more than 128 gathered rows (batch * gamma) and w->embed_norm2_max set
+ * (dpara_candidates_prepare) takes the candidates another way: the gathered rows are ranked
+ * by their bf16 hi parts and 64 candidates a row are rescored exactly, as in
+ * dpara_branch_candidates (same drafts, next spine and margins bit for bit whenever every
+ * step is proven); the two-plane LM head then runs only as part of the fallback.
  * The full head: bf16 drafters with ar_rank in {64, 128, 256}, vocab <= 2^18 and
  * batch <= 16 run the gamma head steps in one launch that needs all of its workgroups
  * resident at once (one per CU); if the GPU is shared so that they cannot all run, the
