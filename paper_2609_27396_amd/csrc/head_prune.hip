@@ -709,7 +709,7 @@ size_t head_row_cand_bytes(int rows) { return 4096 + (size_t)rows * kKeys * 8; }
 // embedding: split into hi/lo planes, hi-plane top-2 GEMM, merge into kHiList keys a row,
 // exact rescoring.  With wnorm_pre the |W_v|^2 pass is skipped (the caller passes the
 // prepared maximum to the steps) and only the overflow flag is cleared.
-hipError_t launch_row_candidates(int rows, int H, int V, int rank, const float* reps, const void* embed,
+static hipError_t launch_row_candidates(int rows, int H, int V, int rank, const float* reps, const void* embed,
                                  const void* W, const float* emax2_pre, const float* wnorm_pre, void* cand,
                                  bf16_t* split, uint64_t* part, void* scratch, hipStream_t st) {
   int* overflow = (int*)cand;
