@@ -11,7 +11,7 @@ oracle's top1 - top2 margin exceeds 1e-2; sampled draws likewise, with the tempe
 within 1e-3 + 1e-3 |s|.  The last cases run the off-serial-path head (candidates of every
 branch row ranked by the rows' bf16 hi part, then rescored) at the default weight scales, where
 the steps are proven, against the plain head bit for bit and against the oracle, at batch 1, 2,
-4, 9 and 16 (each batch up to 4 takes its own LM-head tile); with the embedding's max row norm
+4, 9, 13 and 16 (each batch up to 4 takes its own LM-head tile); with the embedding's max row norm
 prepared, the plain head over more than 128 gathered rows takes the same ranking over the
 accepted rows, and gives the same bits (also through its fallback to the full head).  The head
 reads only the gathered rows, the tied embedding and E, W, so the representations here are
@@ -152,7 +152,7 @@ def test_full_head_at_qwen3_vocabulary(B):
         assert np.array_equal(m3.cpu().numpy(), greedy[2]) and np.array_equal(g3.cpu().numpy(), gh)
 
 
-@pytest.mark.parametrize("B", [1, 2, 4, 9, 16])
+@pytest.mark.parametrize("B", [1, 2, 4, 9, 13, 16])
 def test_candidates_head_at_qwen3_vocabulary(B):
     """The off-serial-path head at the Qwen3 vocabulary with the default weight scales: every
     branch row ranked by its bf16 hi part, the 16 candidates rescored with hi + lo, the bound
