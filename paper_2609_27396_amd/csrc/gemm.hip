@@ -111,6 +111,16 @@ __device__ __forceinline__ void swiglu_copy_out(const bf16_t* so, bf16_t* C, int
 // counts outstanding DMA instructions), then one s_barrier makes every wave's part of that
 // stage visible; the refill of the ring slot freed by the previous iteration is issued
 // right after the barrier, so STAGES-1 stages are in flight while one is consumed.
+// Cache policy of the weight DMA: when the grid has one M tile every weight element is read by
+// exactly one workgroup, so the weights stream through L2 as non-temporal lines (nt) and leave
+// the activation tile, which every workgroup re-reads, resident (M <= 320: 3-7% per GEMM); with
+// several M tiles the weight tiles are shared and keep the default policy.
+constexpr int kAuxStream = 2;
+template <int AUX>
+__device__ __forceinline__ void dma16(const void* g, void* l) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void_t*)l, 16, 0, AUX);
+}
+
 template <int CH>
 __device__ __forceinline__ int swz(int r, int c) {
   if (CH == 16 || CH == 32) return c ^ (r & 15);  // 16 rows of a fragment read: 16 distinct slots
@@ -172,10 +182,13 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
 #pragma unroll
     for (int j = 0; j < A_INS; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + k0), (lds_void_t*)(sb + (wave + NW * j) * 1024), 16, 0, 0);
+    if (MT == 1) {
 #pragma unroll
-    for (int j = 0; j < B_INS; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(bsrc[j] + k0),
-                                       (lds_void_t*)(sb + A_ROWS * BKB + (wave + NW * j) * 1024), 16, 0, 0);
+      for (int j = 0; j < B_INS; ++j) dma16<kAuxStream>(bsrc[j] + k0, sb + A_ROWS * BKB + (wave + NW * j) * 1024);
+    } else {
+#pragma unroll
+      for (int j = 0; j < B_INS; ++j) dma16<0>(bsrc[j] + k0, sb + A_ROWS * BKB + (wave + NW * j) * 1024);
+    }
   };
 
   f32x4_t acc[FM][FN];
@@ -408,8 +421,8 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_pipe_kernel(GemmArgs a, i
 // once.  A therefore bypasses LDS: it arrives in MFMA fragment order (frag_index), and each
 // of the 4 waves (one per SIMD) loads the fragments of its own 80 rows straight into a
 // register ring SB stages deep (one 16-byte load per lane per 1 KB block).  Only the weight
-// tile (96 rows of B per 64-deep K step) goes through an LDS ring filled by direct DMA and
-// read by all four waves.  Row blocks past the last valid one are clamped to it (their
+// tile (96 rows of B per 64-deep K step) goes through an LDS ring filled by direct DMA (as
+// non-temporal lines: each is read once) and read by all four waves.  Row blocks past the last valid one are clamped to it (their
 // accumulator rows are never stored).  SwiGLU tiles hold 48 gate + 48 up columns; the fp32
 // store splits K over `splits` workgroups writing planes [S][M][ldc].
 template <int EPI, int SB, int SKIP>
@@ -456,9 +469,7 @@ __global__ __launch_bounds__(256) void gemm_adir_kernel(GemmArgs a, int NT) {
     __builtin_amdgcn_sched_barrier(0);
     unsigned char* sb = smem + slot * STAGE_BYTES;
 #pragma unroll
-    for (int j = 0; j < B_INS; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(bsrc[j] + k_ld * KB), (lds_void_t*)(sb + (wave + NW * j) * 1024),
-                                       16, 0, 0);
+    for (int j = 0; j < B_INS; ++j) dma16<kAuxStream>(bsrc[j] + k_ld * KB, sb + (wave + NW * j) * 1024);
     __builtin_amdgcn_sched_barrier(0);
   };
 
