@@ -62,6 +62,32 @@ __device__ __forceinline__ int key_perm(int kb, int i) { return (kb >> 1) * 32 +
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
+// Maximum and sum over the four 16-lane rows of a wave (lanes lq, lq + 16, lq + 32, lq + 48):
+// v_permlane16_swap / v_permlane32_swap exchange whole rows between two registers on the
+// VALU, so the reduction needs no LDS round trip.
+__device__ __forceinline__ float rows4_max(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// The running maximum of a row is the reference of its probabilities p = 2^(s - m).  It
+// moves only when a block's maximum passes it by more than kLazyMax (log2 units), so the
+// accumulators are rescaled rarely; p then stays below 2^kLazyMax, which the bf16 hi + lo
+// pair and the float32 sums carry with unchanged relative precision.
+constexpr float kLazyMax = 8.f;
+
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
 // The K and V^T tiles of a 64-key block are filled by direct global->LDS DMA
@@ -278,10 +304,9 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[u][kb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float m_new = fmaxf(m_run[u], mx * sc);          // running max, log2 units
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;  // row sees no key yet
+      mx = rows4_max(mx) * sc;                                          // block max, log2 units
+      const float m_new = mx > m_run[u] + kLazyMax ? mx : m_run[u];   // reference of p
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;            // row sees no key yet
       float psum = 0.f;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -297,6 +322,7 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
           h[0] = (__bf16)p0;
           h[1] = (__bf16)p1;
           hw[q] = __builtin_bit_cast(uint32_t, h);
+          asm("" : "+v"(hw[q]));  // keeps the compiler from converting p0 a second time below
           bf16x2_t l;
           l[0] = (__bf16)(p0 - __uint_as_float(hw[q] << 16));
           l[1] = (__bf16)(p1 - __uint_as_float(hw[q] & 0xFFFF0000u));
@@ -305,7 +331,7 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
         pf[u][t] = as_bf16x8(make_uint4(hw[0], hw[1], hw[2], hw[3]));
         pfl[u][t] = as_bf16x8(make_uint4(lw[0], lw[1], lw[2], lw[3]));
       }
-      // o is rescaled only when some row of the wave raised its max (alpha == 1 else)
+      // o is rescaled only when some row of the wave moved its reference (alpha == 1 else)
       const float alpha = __builtin_amdgcn_exp2f(m_run[u] - m_use);
       l_run[u] = l_run[u] * alpha + psum;
       if (__any(m_new > m_run[u])) {
@@ -314,26 +340,30 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
       }
       m_run[u] = m_new;
     }
-    // O^T += V^T P^T over 64 keys = 2 k-steps of 32.
+    // O^T += V^T P^T over 64 keys = 2 k-steps of 32; the V^T fragment of the next product is
+    // read while the current one's MFMAs run.
+    const unsigned char* vp0 = sb + K_BYTES + v_lane + (g4 ^ vx) * 16;
+    const unsigned char* vp1 = sb + K_BYTES + v_lane + ((4 + g4) ^ vx) * 16;
+    auto vfrag = [&](int q) {
+      return *(const bf16x8_t*)((q < NHB ? vp0 : vp1) + (q % NHB) * 16 * kKeyBlock * 2);
+    };
+    bf16x8_t vf[2];
+    vf[0] = vfrag(0);
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const unsigned char* vp = sb + K_BYTES + v_lane + ((t * 4 + g4) ^ vx) * 16;
+    for (int q = 0; q < 2 * NHB; ++q) {
+      if (q + 1 < 2 * NHB) vf[(q + 1) & 1] = vfrag(q + 1);
+      const int t = q / NHB, hb = q % NHB;
 #pragma unroll
-      for (int hb = 0; hb < NHB; ++hb) {
-        const bf16x8_t vf = *(const bf16x8_t*)(vp + hb * 16 * kKeyBlock * 2);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][t], o[u][hb], 0, 0, 0);
-          o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[u][t], o[u][hb], 0, 0, 0);
-        }
+      for (int u = 0; u < U; ++u) {
+        o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[q & 1], pf[u][t], o[u][hb], 0, 0, 0);
+        o[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[q & 1], pfl[u][t], o[u][hb], 0, 0, 0);
       }
     }
   }
 
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    float l_tot = l_run[u] + __shfl_xor(l_run[u], 16, kWave);
-    l_tot += __shfl_xor(l_tot, 32, kWave);
+    const float l_tot = rows4_sum(l_run[u]);
     if (qi[u] >= nrows) continue;
     const int gi = qi[u] / a.R, row = qi[u] % a.R;
     const int h = kvh * grp + gi;
