@@ -24,8 +24,8 @@
 //                   than kTopK keys of the union exceed.  Per step, 16 lanes per candidate
 //                   take the dot product W_v . e over rank slices; the candidates of a step
 //                   depend on the row only, so their W and E rows are fetched three steps
-//                   ahead into registers, and the winner's E row is in registers when the
-//                   step ends.
+//                   ahead into an LDS ring by DMA, and the winner's E row is in the ring
+//                   when the step ends.
 //
 // A row whose candidate collection overflows, or a step whose bound does not hold, sets
 // the fallback flag; the full head (launch_ar_head with only_if = flag) then recomputes
@@ -48,6 +48,18 @@ constexpr int kHiList = 64;       // hi-plane candidates rescored per branch row
 constexpr int kMaxGamma = 63;
 constexpr int kMaxSplits = 16;
 constexpr int kEmbedNormParts = 512;  // workgroups of the embedding row-norm pass
+constexpr int kPrunedRing = 4;        // steps of candidate rows in flight in the pruned head
+
+// LDS ring of the pruned head: per step, every thread's piece (RANK / 16 elements) of its
+// candidate's W row and E row, moved in 16-byte (else 4-byte) DMA granules.
+template <typename T, int RANK>
+struct PrunedRing {
+  static constexpr int kPiece = RANK / 16 * (int)sizeof(T);
+  static constexpr int kGranule = kPiece % 16 == 0 ? 16 : 4;
+  static constexpr int kSlot = 2 * 256 * kPiece;
+  static constexpr int kListBytes = 16 * kMaxSplits * (kTopK + 1) * 8;
+  static constexpr int kDynBytes = kPrunedRing * kSlot > kListBytes ? kPrunedRing * kSlot : kListBytes;
+};
 
 // EPL contiguous elements from p as float, in 16-byte (or 8-byte) pieces.
 template <typename T, int EPL>
@@ -461,11 +473,57 @@ struct RawPiece {
       }
     }
   }
+  // The piece a DMA ring slot holds for `lane`: chunk q of GR bytes at base + (q * 64 + lane) * GR.
+  // 16-byte chunks are read by inline ds_read_b128 with the LDS wait in the same block: for
+  // ordinary loads of a DMA-filled buffer the compiler waits for every outstanding DMA first,
+  // which would drain the ring each step.
+  template <int GR>
+  __device__ __forceinline__ void load_lds(const unsigned char* base, int lane) {
+    if constexpr (GR == 16) {
+      static_assert(WORDS == 4 || WORDS == 8 || WORDS == 16, "1, 2 or 4 chunks");
+      uint4 u[WORDS / 4];
+      const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)base + lane * 16;
+      if constexpr (WORDS == 4) {
+        asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(u[0]) : "v"(a) : "memory");
+      } else if constexpr (WORDS == 8) {
+        asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:1024\n\ts_waitcnt lgkmcnt(0)"
+                     : "=v"(u[0]), "=v"(u[1]) : "v"(a) : "memory");
+      } else {
+        asm volatile(
+            "ds_read_b128 %0, %4\n\tds_read_b128 %1, %4 offset:1024\n\tds_read_b128 %2, %4 offset:2048\n\t"
+            "ds_read_b128 %3, %4 offset:3072\n\ts_waitcnt lgkmcnt(0)"
+            : "=v"(u[0]), "=v"(u[1]), "=v"(u[2]), "=v"(u[3]) : "v"(a) : "memory");
+      }
+#pragma unroll
+      for (int q = 0; q < WORDS / 4; ++q) {
+        w[4 * q] = u[q].x;
+        w[4 * q + 1] = u[q].y;
+        w[4 * q + 2] = u[q].z;
+        w[4 * q + 3] = u[q].w;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < WORDS * 4 / GR; ++q) w[q] = *(const uint32_t*)(base + (q * 64 + lane) * 4);
+    }
+  }
   __device__ __forceinline__ float at(int j) const {
     if constexpr (sizeof(T) == 2) return __uint_as_float((j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16));
     else return __uint_as_float(w[j]);
   }
 };
+
+// One direct global->LDS DMA instruction of GR bytes a lane (lane l's bytes land at l * GR
+// past the wave-uniform LDS address).
+template <int GR>
+__device__ __forceinline__ void dma_granule(const void* g, void* l) {
+  if constexpr (GR == 16) __builtin_amdgcn_global_load_lds(g, (lds_void_t*)l, 16, 0, 0);
+  else __builtin_amdgcn_global_load_lds(g, (lds_void_t*)l, 4, 0, 0);
+}
+
+// Workgroup barrier for LDS traffic only: the wave's LDS accesses complete, then s_barrier.
+// (__syncthreads also waits for every outstanding global load, which would drain the
+// candidate-row ring each step.)
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 template <typename T, int RANK>
 __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const uint64_t* cand,
@@ -474,13 +532,20 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
                                                  int* flag, int* status, const int* accept_len,
                                                  const int* pre_flag, float inv_t) {
   constexpr int EPT = RANK / 16;
-  constexpr int D = 4;  // steps of candidate rows in flight, in registers
-  __shared__ uint64_t lists[16][kMaxSplits * kKeys];  // the split lists of 16 rows in flight
-  __shared__ uint64_t ck[kMaxGamma][kKeys];           // per row: top kTopK keys, then the bound key
-  __shared__ float es[RANK];                          // E(y_{i-1})
+  constexpr int D = kPrunedRing;
+  constexpr int PB = PrunedRing<T, RANK>::kPiece, GR = PrunedRing<T, RANK>::kGranule;
+  constexpr int NQ = PB / GR;                          // DMA instructions per piece
+  constexpr int SLOT = PrunedRing<T, RANK>::kSlot;     // W pieces, then E pieces, of every thread
+  __shared__ uint64_t ck[kMaxGamma][kKeys];            // per row: top kTopK keys, then the bound key
+  __shared__ float es[RANK];                           // E(y_{i-1})
   __shared__ float zs[kTopK];
+  __shared__ float ms[kMaxGamma];
+  __shared__ int ys[kMaxGamma];
   __shared__ float red[4];
   __shared__ int ybc, stop;
+  // dynamic LDS: the split lists of 16 head rows during the merge, then the candidate-row ring
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  auto lists = (uint64_t(*)[kMaxSplits * kKeys])dyn;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kc = tid >> 4, slice = tid & 15;  // 16-lane row kc: candidate kc, rank slice `slice`
 
@@ -509,10 +574,20 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
   // merge: 16 head rows at a time, lane `slice` of row kc walks split list `slice`
   for (int j0 = 0; j0 < gamma; j0 += 16) {
     const int nrow = min(16, gamma - j0);
-    for (int i = tid; i < nrow * S * kKeys; i += 256) {
-      const int rr = i / (S * kKeys), q = i % (S * kKeys);
-      lists[rr][q] = cand[((int64_t)(row0 + j0 + rr)) * S * kKeys + q];
-    }
+    // the 16 rows' lists are contiguous in cand: every load of a thread is issued before the
+    // first store to LDS (one memory round trip instead of one per element)
+    constexpr int kPer = (16 * kMaxSplits * kKeys + 255) / 256;
+    const int n = nrow * S * kKeys;
+    const uint64_t* src = cand + (int64_t)(row0 + j0) * S * kKeys;
+    uint64_t t[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) t[u] = tid + 256 * u < n ? src[tid + 256 * u] : 0;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if (tid + 256 * u < n) {
+        const int i = tid + 256 * u;
+        lists[i / (S * kKeys)][i % (S * kKeys)] = t[u];
+      }
     __syncthreads();
     if (kc < nrow) {
       int pos = 0;
@@ -534,67 +609,84 @@ __global__ __launch_bounds__(256) void ar_pruned(int gamma, int V, int S, const 
   // (exactly 1 for the greedy head)
   const float wmax_t = wmax * inv_t;
 
-  // Step s's (1-based) candidate rows; steps past gamma reload step gamma's (in bounds,
-  // never used).  Candidate indices are clamped into the vocabulary (keys of a complete
-  // list always are).
-  RawPiece<T, EPT> wb[D], eb[D];
-  auto fetch = [&](int s, RawPiece<T, EPT>& w, RawPiece<T, EPT>& e) {
+  // Step s's (1-based) candidate rows go to ring slot s % D by direct global->LDS DMA: each
+  // thread's W piece (and E piece) of its candidate row, chunk q of every lane of a wave in
+  // one instruction (lane l's GR bytes land at the wave's base + l * GR).  A thread reads back
+  // only the bytes its own lane fetched, so a wave needs only its own vmcnt wait, and D - 1
+  // steps stay in flight.  Steps past gamma reload step gamma's rows (in bounds, never used);
+  // candidate indices are clamped into the vocabulary (keys of a complete list always are).
+  // The loop issues no other vector-memory access: the drafts are kept in LDS and written
+  // after it, and every exit drains the ring first.
+  auto fetch = [&](int s) {
     const int v = (int)min(key_index(ck[min(s, gamma) - 1][kc]), (uint32_t)(V - 1));
-    w.load(W + (int64_t)v * RANK + slice * EPT);
-    e.load(E + (int64_t)v * RANK + slice * EPT);
+    const unsigned char* gw = (const unsigned char*)(W + (int64_t)v * RANK + slice * EPT);
+    const unsigned char* ge = (const unsigned char*)(E + (int64_t)v * RANK + slice * EPT);
+    unsigned char* sl = dyn + (s % D) * SLOT + wave * 64 * PB;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) dma_granule<GR>(gw + q * GR, sl + q * 64 * GR);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) dma_granule<GR>(ge + q * GR, sl + 256 * PB + q * 64 * GR);
   };
+  __syncthreads();  // the merge's reads of the lists are done before the ring overwrites them
 #pragma unroll
-  for (int s = 1; s < D; ++s) fetch(s, wb[s - 1], eb[s - 1]);
+  for (int s = 1; s < D; ++s) fetch(s);
 
-  for (int i0 = 1; i0 <= gamma; i0 += D) {
+  for (int i = 1; i <= gamma; ++i) {
+    fetch(i + D - 1);
+    wait_vmcnt<(D - 1) * 2 * NQ>();  // step i's pieces have landed
+    __builtin_amdgcn_sched_barrier(0);
+    const unsigned char* sl = dyn + (i % D) * SLOT + wave * 64 * PB;
+    RawPiece<T, EPT> wp;
+    wp.template load_lds<GR>(sl, lane);
+    float d = 0.f, ee = 0.f;
 #pragma unroll
-    for (int u = 0; u < D; ++u) {
-      const int i = i0 + u;
-      if (i > gamma) break;
-      fetch(i + D - 1, wb[(u + D - 1) % D], eb[(u + D - 1) % D]);
-      float d = 0.f, ee = 0.f;
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        const float ej = es[slice * EPT + j];
-        d = fmaf(wb[u].at(j), ej, d);
-        ee = fmaf(ej, ej, ee);
-      }
-      d = row16_sum(d);
-      ee = row16_sum(ee);
-      const uint64_t key = ck[i - 1][kc];
-      if (slice == 0) zs[kc] = key ? key_value(key) + d * inv_t : -INFINITY;  // fewer than kTopK candidates
-      __syncthreads();
-      if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
-        uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
-        float v2 = -INFINITY;
-        top2_merge(k1, v2, dpp_u64<kDppXor1>(k1), dpp_f<kDppXor1>(v2));
-        top2_merge(k1, v2, dpp_u64<kDppXor2>(k1), dpp_f<kDppXor2>(v2));
-        top2_merge(k1, v2, dpp_u64<kDppHalfMirror>(k1), dpp_f<kDppHalfMirror>(v2));
-        top2_merge(k1, v2, dpp_u64<kDppMirror>(k1), dpp_f<kDppMirror>(v2));
-        if (tid == 0) {
-          const float lb = key_value(ck[i - 1][kTopK]);
-          const float bound = lb + wmax_t * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
-          const bool ok = v2 > bound;
-          const int y = (int)key_index(k1);
-          if (ok) {
-            drafts[b * gamma + i - 1] = y;
-            next_spine[b * (gamma + 1) + i] = y;
-            if (margins) margins[b * gamma + i - 1] = key_value(k1) - v2;
-          } else {
-            atomicOr(flag, 2);
-          }
-          stop = ok ? 0 : 1;
-          ybc = y;
-        }
-      }
-      __syncthreads();
-      if (stop) return;
-      if ((int)key_index(key) == ybc) {  // the winner's row holds E(y_i)
-#pragma unroll
-        for (int j = 0; j < EPT; ++j) es[slice * EPT + j] = eb[u].at(j);
-      }
-      __syncthreads();
+    for (int j = 0; j < EPT; ++j) {
+      const float ej = es[slice * EPT + j];
+      d = fmaf(wp.at(j), ej, d);
+      ee = fmaf(ej, ej, ee);
     }
+    d = row16_sum(d);
+    ee = row16_sum(ee);
+    const uint64_t key = ck[i - 1][kc];
+    if (slice == 0) zs[kc] = key ? key_value(key) + d * inv_t : -INFINITY;  // fewer than kTopK candidates
+    lds_barrier();
+    if (tid < 16) {  // the top two of z over the 16 candidates, one lane each
+      uint64_t k1 = argmax_key(zs[tid], key_index(ck[i - 1][tid]));
+      float v2 = -INFINITY;
+      top2_merge(k1, v2, dpp_u64<kDppXor1>(k1), dpp_f<kDppXor1>(v2));
+      top2_merge(k1, v2, dpp_u64<kDppXor2>(k1), dpp_f<kDppXor2>(v2));
+      top2_merge(k1, v2, dpp_u64<kDppHalfMirror>(k1), dpp_f<kDppHalfMirror>(v2));
+      top2_merge(k1, v2, dpp_u64<kDppMirror>(k1), dpp_f<kDppMirror>(v2));
+      if (tid == 0) {
+        const float lb = key_value(ck[i - 1][kTopK]);
+        const float bound = lb + wmax_t * sqrtf(ee) + 1e-4f + 1e-5f * fabsf(lb);
+        const bool ok = v2 > bound;
+        const int y = (int)key_index(k1);
+        ys[i - 1] = y;
+        ms[i - 1] = key_value(k1) - v2;
+        stop = ok ? 0 : 1;
+        ybc = y;
+      }
+    }
+    lds_barrier();
+    if (stop) {
+      wait_vmcnt<0>();
+      if (tid == 0) atomicOr(flag, 2);
+      return;
+    }
+    if ((int)key_index(key) == ybc) {  // the winner's row holds E(y_i)
+      RawPiece<T, EPT> ep;
+      ep.template load_lds<GR>(sl + 256 * PB, lane);
+#pragma unroll
+      for (int j = 0; j < EPT; ++j) es[slice * EPT + j] = ep.at(j);
+    }
+    lds_barrier();
+  }
+  wait_vmcnt<0>();  // the D - 1 fetches past the last step
+  for (int i = tid; i < gamma; i += 256) {
+    drafts[b * gamma + i] = ys[i];
+    next_spine[b * (gamma + 1) + i + 1] = ys[i];
+    if (margins) margins[b * gamma + i] = ms[i];
   }
 }
 
@@ -651,7 +743,12 @@ hipError_t launch_pruned(int B, int gamma, int V, int S, const uint64_t* cand, c
                          const void* E, const void* W, const int* bonus, int* drafts, int* next_spine,
                          float* margins, int* flag, int* status, const int* accept_len, const int* pre_flag,
                          float inv_t, hipStream_t st) {
-  hipLaunchKernelGGL((ar_pruned<T, RANK>), dim3(B), dim3(256), 0, st, gamma, V, S, cand, wpart, nw, (const T*)E,
+  constexpr int lds = PrunedRing<T, RANK>::kDynBytes;
+  static_assert(lds + 16384 <= 163840, "pruned-head LDS exceeds 160 KB");
+  auto kern = ar_pruned<T, RANK>;
+  static const hipError_t attr = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kern, dim3(B), dim3(256), lds, st, gamma, V, S, cand, wpart, nw, (const T*)E,
                      (const T*)W, bonus, drafts, next_spine, margins, flag, status, accept_len, pre_flag, inv_t);
   return hipGetLastError();
 }
