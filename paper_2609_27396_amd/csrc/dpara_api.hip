@@ -811,8 +811,10 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
   int* status = at<int>(ws, 0);
   float* G = at<float>(ws, p.G);
   bf16_t* Gs = at<bf16_t>(ws, p.Gsplit);
+  // the gather also clears the pruned head's fallback flag (no kernel before the pruned
+  // steps reads it)
   HIP_TRY(launch_gather_branch(batch, g, H, reps, accept_len, G, gathered, Gs, at<uint64_t>(ws, p.arpart),
-                               (int64_t)2 * 16 * p.ar_grid * 2, status, st),
+                               (int64_t)2 * 16 * p.ar_grid * 2, status, st, at<int>(ws, p.hflag)),
           "gather_branch");
   const bool bf = cfg->dtype == DPARA_BF16;
   // Greedy bf16 head over more than 128 gathered rows with the embedding's max row norm
@@ -878,7 +880,7 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
               "perturbed logits");
       pe = launch_head_pruned(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.plogits), w->ar_E, w->ar_W,
                               bonus, drafts, next_spine, margins, at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart),
-                              hflag, status, st, smp->inv_t, w->ar_w_norm2_max);
+                              hflag, status, st, smp->inv_t, w->ar_w_norm2_max, true);
       if (pe != hipSuccess && pe != hipErrorNotSupported) return hip_fail(pe, "sampled pruned head");
     }
     HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
@@ -899,7 +901,7 @@ int select_and_head_impl(const dpara_config_t* cfg, const dpara_weights_t* w, in
   const hipError_t pe = launch_head_pruned(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits),
                                            w->ar_E, w->ar_W, bonus, drafts, next_spine, margins,
                                            at<uint64_t>(ws, p.hcand), at<float>(ws, p.hwpart), hflag, status, st,
-                                           1.0f, w->ar_w_norm2_max);
+                                           1.0f, w->ar_w_norm2_max, true);
   if (pe != hipSuccess && pe != hipErrorNotSupported) return hip_fail(pe, "pruned head");
   HIP_TRY(launch_ar_head(cfg->dtype, batch, g, V, cfg->ar_rank, at<float>(ws, p.logits), w->ar_E, w->ar_W, bonus,
                          drafts, next_spine, margins, at<uint64_t>(ws, p.hpart), p.h_chunks, p.h_chunk,

@@ -916,7 +916,7 @@ size_t head_prune_cand_bytes(int rows, int V) { return (size_t)rows * head_prune
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                               uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st, float inv_t,
-                              const float* wnorm_pre) {
+                              const float* wnorm_pre, bool flag_cleared) {
   if (!head_prune_supported(dtype, gamma, V, rank) || B < 1) return hipErrorNotSupported;
   const int rows = B * gamma;
   const int S = head_prune_splits(rows, V);
@@ -925,7 +925,8 @@ hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, cons
   Phase ph("ar_step", st);
   // the weights' max row norm: prepared once (one float), or one pass over W here (which also
   // clears the fallback flag)
-  hipError_t e = wnorm_pre ? launch_clear_status(flag, st) : launch_wnorm(dtype, rank, W, V, wpart, flag, st);
+  hipError_t e = wnorm_pre ? (flag_cleared ? hipSuccess : launch_clear_status(flag, st))
+                           : launch_wnorm(dtype, rank, W, V, wpart, flag, st);
   if (e != hipSuccess) return e;
   if (wnorm_pre) {
     wpart = const_cast<float*>(wnorm_pre);

@@ -190,7 +190,8 @@ hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, cons
 // Also zeroes n_clear uint64 words at `clear` (the persistent AR head's step tags).
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps,
                                 const int* accept_len, float* G, float* G_out, bf16_t* Ghi,
-                                uint64_t* clear, int64_t n_clear, int* status, hipStream_t st);
+                                uint64_t* clear, int64_t n_clear, int* status, hipStream_t st,
+                                int* flag = nullptr);  // flag: set to 0 (the pruned head's fallback flag)
 int ar_head_chunk(int dtype, int rank);  // vocabulary rows per AR-step workgroup
 // Persistent bf16 AR head: grid size for (rank, V), 0 if unsupported; the partial buffer is
 // [2][16][grid][2] uint64 and must hold zero tags when the launch starts.  Returns
@@ -222,7 +223,7 @@ size_t head_prune_cand_bytes(int rows, int V);
 hipError_t launch_head_pruned(int dtype, int B, int gamma, int V, int rank, const float* logits, const void* E,
                               const void* W, const int* bonus, int* drafts, int* next_spine, float* margins,
                               uint64_t* cand, float* wpart, int* flag, int* status, hipStream_t st,
-                              float inv_t = 1.0f, const float* wnorm_pre = nullptr);
+                              float inv_t = 1.0f, const float* wnorm_pre = nullptr, bool flag_cleared = false);
 // max_v |W_v|^2 into out (one float); parts: head_prune_wparts() floats of scratch, scratch_flag
 // one int.
 hipError_t launch_head_prepare(int dtype, int rank, const void* W, int V, float* parts, int* scratch_flag, float* out,

@@ -109,8 +109,9 @@ __global__ __launch_bounds__(64 * kFinWaves) void verify_finalize(int gamma, int
 
 __global__ __launch_bounds__(256) void gather_branch(int gamma, int H, const float* reps, const int* accept_len,
                                                      float* G, float* G_out, bf16_t* Ghi, int64_t lo_off,
-                                                     uint64_t* clear, int64_t n_clear, int* status) {
+                                                     uint64_t* clear, int64_t n_clear, int* status, int* flag) {
   const int i = blockIdx.x, b = blockIdx.y;
+  if (flag && i == 0 && b == 0 && threadIdx.x == 0) *flag = 0;
   for (int64_t k = ((int64_t)b * gridDim.x + i) * 256 + threadIdx.x; k < n_clear; k += (int64_t)gridDim.x * gridDim.y * 256)
     clear[k] = 0;
   int r = accept_len[b];
@@ -714,10 +715,10 @@ hipError_t launch_verify_sampled(int logits_dtype, int B, int gamma, int V, cons
 
 hipError_t launch_gather_branch(int B, int gamma, int H, const float* reps, const int* accept_len, float* G,
                                 float* G_out, bf16_t* Ghi, uint64_t* clear, int64_t n_clear, int* status,
-                                hipStream_t st) {
+                                hipStream_t st, int* flag) {
   Phase ph("gather", st);
   hipLaunchKernelGGL(gather_branch, dim3(gamma, B), dim3(256), 0, st, gamma, H, reps, accept_len, G, G_out, Ghi,
-                     (int64_t)B * gamma * H, clear, n_clear, status);
+                     (int64_t)B * gamma * H, clear, n_clear, status, flag);
   return hipGetLastError();
 }
 
