@@ -116,13 +116,29 @@ __global__ __launch_bounds__(64 * NW) void attn_mfma(AttnArgs a) {
 
   // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs, so physical id p
   // maps to logical id lid with each XCD taking a contiguous range of lid; row tiles run
-  // fastest in lid, so the tiles that read the same key blocks share one XCD's L2.
+  // fastest in lid, so the tiles that read the same key blocks share one XCD's L2.  KV heads
+  // are the slowest index, so an XCD's range holds the same heads of every request (with 8 KV
+  // heads, one head each) and the XCDs get equal shares of a batch of mixed context lengths;
+  // within it the requests come longest context first, so the short ones fill the last round.
   const int n_tiles = (grp_rows(a) + ROWS_WG - 1) / ROWS_WG;
   const int total = n_tiles * a.S * a.B * a.n_kv;
   const int p = blockIdx.x, per_xcd = total >> 3;
   const int lid = p < (per_xcd << 3) ? (p & 7) * per_xcd + (p >> 3) : p;
-  const int tile = lid % n_tiles, split = (lid / n_tiles) % a.S, bh = lid / (n_tiles * a.S);
-  const int b = bh / a.n_kv, kvh = bh % a.n_kv;
+  const int tile = lid % n_tiles, split = (lid / n_tiles) % a.S, hb = lid / (n_tiles * a.S);
+  const int kvh = hb / a.B, rank = hb % a.B;
+  int b = rank;
+  if (a.B > 1 && a.B <= 64) {
+    // the request of this rank by (context length descending, index ascending): lane t ranks
+    // request t, every wave the same (no barrier), and the ballot picks the one lane
+    const int t = threadIdx.x & 63;
+    const int Lt = t < a.B ? min(max(a.ctx_len[t], 0), a.cap) : -1;
+    int r = 0;
+    for (int u = 0; u < a.B; ++u) {
+      const int Lu = min(max(a.ctx_len[u], 0), a.cap);
+      r += (Lu > Lt) | ((Lu == Lt) & (u < t));
+    }
+    b = __builtin_ctzll(__ballot(t < a.B && r == rank));
+  }
   const int grp = a.n_q / a.n_kv;
   const int nrows = grp * a.R;
   const int L = min(max(a.ctx_len[b], 0), a.cap);
