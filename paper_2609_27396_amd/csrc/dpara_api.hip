@@ -311,10 +311,9 @@ int run_decoder(const dpara_config_t* cfg, const dpara_layer_weights_t* layers, 
 
   {
   Phase ph("assemble", st);
-  HIP_TRY(launch_assemble_rows(dt, batch, R, g, H, cfg->vocab, tokens, embed, mask_emb, X, status, st),
+  HIP_TRY(launch_assemble_rows_rope(dt, batch, R, g, H, cfg->vocab, tokens, embed, mask_emb, X, status, 2 * g + 1,
+                                    hd, cfg->rope_base, ctx->ctx_len, at<float2>(ws, p.rope), st),
           "assemble_rows");
-  HIP_TRY(launch_rope_table(batch, 2 * g + 1, hd, cfg->rope_base, ctx->ctx_len, 0, at<float2>(ws, p.rope), st),
-          "rope_table");
   }
   float* P = at<float>(ws, p.P);
   int pend = 0;  // split-K planes of the last O / down projection not yet added into X

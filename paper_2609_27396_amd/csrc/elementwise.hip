@@ -31,11 +31,11 @@ __device__ __forceinline__ float4 sum_planes4(float4 acc, const float* p, int64_
   return acc;
 }
 
+// Row `row` of request b of the block: spine rows take their token's embedding, mask rows the
+// mask embedding.
 template <typename T>
-__global__ __launch_bounds__(256) void assemble_rows(int R, int gamma, int H, int V, const int* spine,
-                                                     const T* embed, const T* mask_emb, float* X,
-                                                     int* status) {
-  const int row = blockIdx.x, b = blockIdx.y;
+__device__ __forceinline__ void assemble_row(int row, int b, int R, int gamma, int H, int V, const int* spine,
+                                             const T* embed, const T* mask_emb, float* X, int* status) {
   const T* src = mask_emb;
   if (row <= gamma) {
     int t = spine[b * (gamma + 1) + row];
@@ -113,16 +113,33 @@ __global__ __launch_bounds__(NTH) void rmsnorm_rows(int H, float* X, int grp, in
   }
 }
 
-__global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx_len, int pos_off,
-                                  float2* table) {
-  const int b = blockIdx.y;
+// Entry idx of request b's RoPE table: (cos, sin) of position ctx_len + pos_off + idx / (hd/2).
+__device__ __forceinline__ void rope_entry(int b, int idx, int n_pos, int hd, double base, const int* ctx_len,
+                                           int pos_off, float2* table) {
   const int half = hd / 2;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= n_pos * half) return;
   const int i = idx / half, p = idx % half;
   float c, s;
   rope_cs(max(ctx_len[b], 0) + pos_off + i, p, hd, base, &c, &s);
   table[((int64_t)b * n_pos + i) * half + p] = make_float2(c, s);
+}
+
+__global__ void rope_table_kernel(int n_pos, int hd, double base, const int* ctx_len, int pos_off,
+                                  float2* table) {
+  rope_entry(blockIdx.y, blockIdx.x * blockDim.x + threadIdx.x, n_pos, hd, base, ctx_len, pos_off, table);
+}
+
+// The backbone's first two steps in one launch: blocks x < R assemble rows, the blocks past R
+// fill the RoPE table (256 entries each).
+template <typename T>
+__global__ __launch_bounds__(256) void assemble_rows_rope(int R, int gamma, int H, int V, const int* spine,
+                                                          const T* embed, const T* mask_emb, float* X, int* status,
+                                                          int n_pos, int hd, double base, const int* ctx_len,
+                                                          float2* table) {
+  if ((int)blockIdx.x < R)
+    assemble_row(blockIdx.x, blockIdx.y, R, gamma, H, V, spine, embed, mask_emb, X, status);
+  else
+    rope_entry(blockIdx.y, ((int)blockIdx.x - R) * 256 + threadIdx.x, n_pos, hd, base, ctx_len, 0, table);
 }
 
 // Grid (head-slot groups, rows): HD/4 lanes per (row, head slot), 4 consecutive entries per
@@ -331,19 +348,6 @@ __global__ void clear_status_kernel(int* status) { status[threadIdx.x] = 0; }
 
 }  // namespace
 
-hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V, const int* spine,
-                                const void* embed, const void* mask_emb, float* X, int* status,
-                                hipStream_t st) {
-  dim3 grid(R, B);
-  if (dtype == 1)
-    hipLaunchKernelGGL(assemble_rows<bf16_t>, grid, dim3(256), 0, st, R, gamma, H, V, spine,
-                       (const bf16_t*)embed, (const bf16_t*)mask_emb, X, status);
-  else
-    hipLaunchKernelGGL(assemble_rows<float>, grid, dim3(256), 0, st, R, gamma, H, V, spine,
-                       (const float*)embed, (const float*)mask_emb, X, status);
-  return hipGetLastError();
-}
-
 template <typename TO, int VN>
 void rmsnorm_launch(int rows, int H, float* X, int grp, int64_t in_stride, int in_off, const float* P, int S,
                     int64_t pstride, int write_back, const float* g, float eps, void* Y, hipStream_t st) {
@@ -400,6 +404,21 @@ hipError_t launch_rmsnorm_frag(int rows, int H, float* X, const float* P, int S,
     case 4: return go(rmsnorm_rows<bf16_t, 4, 1>);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_assemble_rows_rope(int dtype, int B, int R, int gamma, int H, int V, const int* spine,
+                                     const void* embed, const void* mask_emb, float* X, int* status, int n_pos,
+                                     int hd, float base, const int* ctx_len, float2* table, hipStream_t st) {
+  dim3 grid(R + (n_pos * (hd / 2) + 255) / 256, B);
+  if (dtype == 1)
+    hipLaunchKernelGGL(assemble_rows_rope<bf16_t>, grid, dim3(256), 0, st, R, gamma, H, V, spine,
+                       (const bf16_t*)embed, (const bf16_t*)mask_emb, X, status, n_pos, hd, (double)base, ctx_len,
+                       table);
+  else
+    hipLaunchKernelGGL(assemble_rows_rope<float>, grid, dim3(256), 0, st, R, gamma, H, V, spine,
+                       (const float*)embed, (const float*)mask_emb, X, status, n_pos, hd, (double)base, ctx_len,
+                       table);
+  return hipGetLastError();
 }
 
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len, int pos_off,

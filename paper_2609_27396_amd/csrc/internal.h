@@ -109,9 +109,6 @@ constexpr int kMaxAttnSplits = 16;
 int attn_rows_per_workgroup();  // query rows (over the heads of a KV group) per bf16 workgroup
 
 // ---------------------------------------------------------------- elementwise
-hipError_t launch_assemble_rows(int dtype, int B, int R, int gamma, int H, int V,
-                                const int* spine, const void* embed, const void* mask_emb,
-                                float* X, int* status, hipStream_t st);
 // Y[m] = rmsnorm(x) * g with x = X[in_row(m)] + sum_{s<S} P[s][in_row(m)] (P planes share
 // X's layout, plane stride pstride floats), in_row(m) = (m / grp) * in_stride + in_off + m % grp.
 // write_back: also store x into X (folds the pending partial sums into the residual stream).
@@ -122,6 +119,11 @@ hipError_t launch_rmsnorm(int out_dtype, int rows, int H, float* X, int grp, int
 // `rows` in the last 16-row block are left untouched).  H a multiple of 32.
 hipError_t launch_rmsnorm_frag(int rows, int H, float* X, const float* P, int S, int64_t pstride,
                                const float* g, float eps, void* Y, hipStream_t st);
+// The backbone input rows (spine rows: their tokens' embeddings; mask rows: the mask embedding)
+// and the RoPE table of positions ctx_len .. ctx_len + n_pos - 1, in one launch
+hipError_t launch_assemble_rows_rope(int dtype, int B, int R, int gamma, int H, int V, const int* spine,
+                                     const void* embed, const void* mask_emb, float* X, int* status, int n_pos,
+                                     int hd, float base, const int* ctx_len, float2* table, hipStream_t st);
 hipError_t launch_rope_table(int B, int n_pos, int hd, float base, const int* ctx_len,
                              int pos_off, float2* table, hipStream_t st);
 // QKV: S fp32 planes [S][B*R][(n_q+2n_kv)*hd], summed in order.
