@@ -134,6 +134,15 @@ SMALL_CASES = {
     "h256_g63": (synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
                                     vocab=2000, gamma=63, ar_rank=64, qk_norm=True, dtype="bf16"),
                  [100, 3]),
+    # mixed context lengths with ties and empty contexts: attention orders the requests longest
+    # context first (ties by index)
+    "h256_g3_ties": (synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
+                                        vocab=1500, gamma=3, ar_rank=64, qk_norm=True, dtype="bf16"),
+                     [90, 90, 5, 200, 90, 0, 200, 7, 7, 150, 0, 33]),
+    # more than 64 requests: attention keeps the batch order
+    "h256_g2_b70": (synth.DrafterShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
+                                       vocab=1000, gamma=2, ar_rank=64, qk_norm=True, dtype="bf16"),
+                    [(37 * i) % 180 for i in range(70)]),
     # float32 model with several tiles, hd 128
     "f32_h256_g7": (synth.DrafterShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=1, head_dim=128, ffn=320,
                                        vocab=3001, gamma=7, ar_rank=64, qk_norm=True, dtype="f32"),
