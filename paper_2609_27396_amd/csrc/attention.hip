@@ -6,13 +6,13 @@
 // form one virtual sequence: ceil(L/64) blocks of context followed by ceil(R/64) blocks of
 // in-block keys (dense, masked per element).  Workgroups split that sequence evenly.
 //
-// bf16 path (attn_mfma): one workgroup = 4 waves x 32 query rows (all query heads of the
+// bf16 path (attn_mfma): one workgroup = 8 waves x 16 query rows (all query heads of the
 // KV group share the keys) over a contiguous range of 64-key blocks.  K (keys x head_dim)
 // and V^T (head_dim x keys; both the cache and the in-block values are stored transposed)
-// are staged through a double-buffered, XOR-swizzled LDS ring: the next block's global
-// loads are issued into registers before the current block's MFMAs, so their latency
-// hides behind the math.  S^T = K Q^T and O^T += V^T P^T use v_mfma_f32_16x16x32_bf16
-// with an online softmax in log2 units.  The K operand rows are permuted so that each
+// stream through a double-buffered, XOR-swizzled LDS ring filled by direct global->LDS DMA:
+// the next block's DMA is issued before the current block's MFMAs, so its latency hides
+// behind the math.  S^T = K Q^T and O^T += V^T P^T use v_mfma_f32_16x16x32_bf16 with an
+// online softmax in log2 units.  The K operand rows are permuted so that each
 // lane's probabilities form 8 consecutive keys, which makes every V^T operand one
 // 16-byte LDS read.  P enters the PV product as a bf16 hi + lo pair (two MFMAs), so the
 // probabilities keep ~16 significant bits: a single bf16 rounding of P moves the result
