@@ -63,11 +63,16 @@ def backbone_work(shape, B, ctx_lens):
     kv_bytes = L * sum(int(n) for n in ctx_lens) * 2 * nkv * hd * esz
     reps_bytes = B * (g + 1) * g * H * 4
     dense = 2.0 * M * per_layer_w * L
+    return wbytes + kv_bytes + reps_bytes, dense + attention_flops(shape, ctx_lens)
+
+
+def attention_flops(shape, ctx_lens):
+    """Algorithmic flops of the backbone's attention (all layers): QK^T and PV over the keys
+    each row sees under the tree mask (the whole context plus its visible in-block keys)."""
+    nq, hd, L, g = shape.n_q_heads, shape.head_dim, shape.n_layers, shape.gamma
+    R = (g + 1) ** 2
     vis_in_block = (g + 1) * (g + 2) // 2 + sum(g * (r + 1 + g) for r in range(g + 1))
-    attn = 0.0
-    for n in ctx_lens:
-        attn += 4.0 * nq * hd * (R * int(n) + vis_in_block) * L
-    return wbytes + kv_bytes + reps_bytes, dense + attn
+    return sum(4.0 * nq * hd * (R * int(n) + vis_in_block) * L for n in ctx_lens)
 
 
 def host_cores():
@@ -504,6 +509,11 @@ def step_bench(wl, dr, ri, steps, warmup, graph=True, prof_steps=5):
                      "GFLOP": bb_flops / 1e9, "GB_s": bb_bytes / bb_s / 1e9, "TFLOP_s": bb_flops / bb_s / 1e12,
                      "hbm_frac": bb_bytes / bb_s / 1e9 / PEAK_HBM_GBS,
                      "mfma_frac": bb_flops / bb_s / 1e12 / peak_flops},
+        # attention (MFMA pass + fold) against the bf16 peak, counting each useful product once
+        "attention": {"us_per_layer": 1000.0 * sum_ms(["attn_ctx", "attn_merge"]) / shape.n_layers,
+                      "TFLOP_s": attention_flops(shape, ri.ctx_lens) / (sum_ms(["attn_ctx", "attn_merge"]) * 1e-3) / 1e12,
+                      "mfma_frac": attention_flops(shape, ri.ctx_lens) / (sum_ms(["attn_ctx", "attn_merge"]) * 1e-3)
+                      / 1e12 / peak_flops},
         "head_us_per_round": 1000.0 * sum_ms(["gather", "lm_head", "ar_step"]),
         "head_full_fallback": dr.head_fallback(),
         "verify_us_per_round": 1000.0 * sum_ms(["verify"]),
